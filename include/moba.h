@@ -1,0 +1,187 @@
+/*
+ * moba.h -- C ABI of the MI355X (gfx950) MoBA causal prefill library.
+ *
+ * MoBA (Mixture of Block Attention, arXiv 2502.13189) lets every query attend
+ * to its own block plus the top-scoring past blocks of its sequence.  The
+ * library computes, on one GPU:
+ *   block mean-pool of the keys  -> gate (unscaled q . block key, causal mask,
+ *   forced current block, top-k)  -> routing inversion (queries per block)
+ *   -> attention over the routed history blocks and the causal current block
+ *   -> log-sum-exp merge of the partial results,
+ * following Sec. 2.2 (Eq. 2-6) and Algorithm 1 of the paper; plus dense causal
+ * attention (Eq. 1) built from the same kernels, for comparison.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Tensors are passed as moba_tensor descriptors: a data pointer, a dtype, and
+ * shape/stride in ELEMENTS.  The caller owns every tensor; the library never
+ * frees caller memory.  All tensors except cu_seqlens live in device memory of
+ * the current HIP device.
+ *
+ *   q    [T, Hq,  D]  bf16 or f32; last dim contiguous, any token/head stride
+ *   k, v [T, Hkv, D]  same dtype as q; last dim contiguous
+ *   out  [T, Hq,  D]  same dtype as q; last dim contiguous
+ *   lse  [Hq, T]      f32, contiguous; natural-log log-sum-exp of the scaled
+ *                      logits over the keys each query attended
+ *   cu_seqlens [S+1]  int32, contiguous, host OR device memory: cu[0] = 0,
+ *                      non-decreasing, cu[S] = T.  Sequence s holds tokens
+ *                      [cu[s], cu[s+1]); blocks restart at every sequence and
+ *                      nothing is attended across sequences.  A device
+ *                      cu_seqlens costs one device-to-host copy and a sync;
+ *                      pass it in host memory to keep the call asynchronous.
+ *
+ * Head dimension D must be 128.  Hq must be a multiple of Hkv (GQA: query head
+ * h uses kv-head h / (Hq / Hkv)) and Hq / Hkv <= 128.  Logits are scaled by
+ * 1/sqrt(D); gate scores are not scaled (Eq. 6).
+ *
+ * Every call enqueues its device work on `stream` and returns without waiting,
+ * except as noted.  Arguments are validated before any HIP call; invalid
+ * arguments return a status code and touch nothing.  Kernel launch failures
+ * return MOBA_ERR_HIP.  No function throws.
+ *
+ * The library keeps one cached device workspace per device, grown on demand
+ * (growing it synchronizes the device) and capped by the environment variable
+ * MOBA_WORKSPACE_LIMIT_BYTES (default 64 GiB).  When one call needs more, the
+ * attention runs in chunks of kv-heads.  The workspace is shared by all calls
+ * on a device: calls on one device must come from one host thread, and calls
+ * enqueued on different streams of one device must not overlap in time.
+ */
+#ifndef MOBA_H_
+#define MOBA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { MOBA_F32 = 0, MOBA_BF16 = 1, MOBA_I32 = 2, MOBA_I64 = 3 } moba_dtype;
+
+typedef struct {
+  void* data;        /* host or device pointer, see each argument */
+  int32_t dtype;     /* moba_dtype */
+  int32_t ndim;      /* 1..4 */
+  int64_t shape[4];  /* elements per dimension */
+  int64_t stride[4]; /* elements between consecutive indices of a dimension */
+} moba_tensor;
+
+typedef enum {
+  MOBA_OK = 0,
+  MOBA_ERR_NULL = 1,        /* a required descriptor or data pointer is NULL */
+  MOBA_ERR_DTYPE = 2,       /* dtype mismatch or unsupported dtype */
+  MOBA_ERR_SHAPE = 3,       /* shapes disagree with each other or with cu_seqlens */
+  MOBA_ERR_LAYOUT = 4,      /* last dim not contiguous, or a contiguous tensor required */
+  MOBA_ERR_BLOCK_SIZE = 5,  /* block_size < 1 */
+  MOBA_ERR_TOPK = 6,        /* topk < 1 */
+  MOBA_ERR_SEQLENS = 7,     /* cu[0] != 0, decreasing, or cu[S] != T */
+  MOBA_ERR_UNSUPPORTED = 8, /* D != 128, Hq/Hkv > 128, > 4096 blocks per sequence,
+                               1 < topk-1 < #blocks with topk > 64, or index overflow */
+  MOBA_ERR_NO_MEMORY = 9,   /* workspace over MOBA_WORKSPACE_LIMIT_BYTES or hipMalloc failed */
+  MOBA_ERR_HIP = 10         /* a HIP call or kernel launch failed */
+} moba_status;
+
+/*
+ * MoBA causal prefill forward (Sec. 2.2 Eq. 2-6; Algorithm 1).
+ *
+ * For query token t of sequence s at local position tau = t - cu[s] and
+ * query head h: c = tau / block_size is its current block.  The gate scores
+ * every past block j < c with <q, mean of block j's keys> (unscaled, fp32),
+ * keeps the min(topk-1, c) highest (equal scores: lower block index wins),
+ * and adds block c (the current block counts toward topk).  out[t, h] is
+ * softmax attention over every key of the kept past blocks plus the keys of
+ * block c up to and including t.  lse[h, t] is its log-sum-exp.
+ * topk larger than the number of blocks selects every causal block.
+ *
+ * Arguments: see the conventions above.  block_size >= 1, topk >= 1.
+ * Returns MOBA_OK or an error status; on error nothing has been enqueued
+ * unless the status is MOBA_ERR_HIP.
+ */
+moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                         const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                         moba_tensor* out, moba_tensor* lse, hipStream_t stream);
+
+/*
+ * Dense causal attention (Eq. 1 with a causal mask and scale 1/sqrt(D)):
+ * every query attends to every key of its sequence up to and including
+ * itself.  Same tensor conventions as moba_forward.
+ */
+moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                               const moba_tensor* cu_seqlens, moba_tensor* out, moba_tensor* lse,
+                               hipStream_t stream);
+
+/*
+ * Block mean-pool of the keys (Eq. 6; Algorithm 1, mean_pool).
+ * kbar [nblk_total, Hkv, D] f32 contiguous, device: row b = blk_off[s] + j
+ * holds the mean of k over the tokens of block j of sequence s (a short last
+ * block uses its own token count), with blk_off[s] = sum over s' < s of
+ * ceil(len_s' / block_size).  Accumulated in fp64, rounded once to f32.
+ */
+moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32_t block_size,
+                      moba_tensor* kbar, hipStream_t stream);
+
+/*
+ * Gate and top-k selection (Eq. 5 and Eq. 6 with the causal rules of
+ * Sec. 2.2), including the pool.
+ * sel [T, Hq, topk] int32 contiguous, device: the kept past blocks in
+ * ascending order, then the current block c, then -1 padding; local block
+ * indices of the query's sequence.
+ * scores (nullable) [T, Hq, nmax] f32 contiguous, device: the fp32 gate score
+ * of every past block j < min(c, nmax), NaN elsewhere (a debugging aid; costs
+ * one extra write pass).
+ */
+moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_tensor* cu_seqlens,
+                        int32_t block_size, int32_t topk, moba_tensor* sel, moba_tensor* scores,
+                        hipStream_t stream);
+
+/*
+ * Routing inversion (Algorithm 1, index_select_moba_attn_block; Sec. 2.3
+ * "arrange the ordering of query tokens based on their assigned KV blocks"):
+ * for every bin (kv-head g, global block b = blk_off[s] + j) the list of
+ * history selections that chose it, by a stable counting sort.
+ *   sel      [T, Hq, topk] int32 contiguous, device (as written by moba_select)
+ *   counts   [Hkv * nblk_total] int32 contiguous, device: entries per bin,
+ *            bins ordered g-major
+ *   offsets  [Hkv * nblk_total + 1] int64 contiguous, device: exclusive scan
+ *   entries  [E] int32 contiguous, device, E = offsets[last]: entry value
+ *            e = r * (topk - 1) + x, where x is the selection slot (position
+ *            in sel) and r = g * (T * G) + t * G + (h - g * G) with G = Hq/Hkv;
+ *            ascending within a bin.  E must equal the number of history
+ *            selections, sum over rows of min(topk - 1, c).
+ * num_kv_heads gives Hkv.  The current block is not routed.
+ */
+moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, int32_t block_size,
+                       int32_t num_kv_heads, moba_tensor* counts, moba_tensor* offsets,
+                       moba_tensor* entries, hipStream_t stream);
+
+/* Bytes of device workspace the library currently holds on the current device. */
+size_t moba_workspace_bytes(void);
+
+/* Free the cached workspace of the current device (synchronizes the device). */
+moba_status moba_release_workspace(void);
+
+/* Static, human-readable name of a status. */
+const char* moba_status_string(moba_status status);
+
+/*
+ * Per-phase timing.  While enabled, every entry point records HIP events
+ * around each phase on the caller's stream.  moba_profile_read waits for the
+ * recorded events, writes up to max_phases entries and resets the counters;
+ * it returns the number of phases written.
+ */
+typedef struct {
+  char name[24];     /* "pool", "vt_pack", "gate", "route", "attn_hist", ... */
+  int64_t launches;  /* phase executions recorded */
+  double total_ms;   /* summed event-to-event time */
+} moba_phase_stat;
+
+void moba_profile_enable(int enabled);
+int moba_profile_read(moba_phase_stat* stats, int max_phases);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOBA_H_ */

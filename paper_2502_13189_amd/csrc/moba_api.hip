@@ -1,0 +1,788 @@
+// Host side of the MoBA library: argument validation, per-shape tables, the
+// cached device workspace, and the order of kernel launches behind the C ABI
+// declared in include/moba.h.
+//
+// moba_forward enqueues, on the caller's stream:
+//   pool -> [bf16: V^T pack] -> gate -> route (count, column scan, bin scan,
+//   scatter) -> per chunk of kv-heads: history attention, current-block
+//   attention, merge.
+// Only the last three depend on the chunk; their workspace (fp32 partials)
+// is what the workspace cap limits.
+#include "moba.h"
+#include "moba_internal.h"
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+using namespace moba;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kDefaultWorkspaceLimit = size_t(64) << 30;
+
+// ------------------------------------------------------------- profiling
+struct PhaseRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+bool g_prof = false;
+std::vector<PhaseRec> g_recs;
+std::mutex g_prof_mu;
+
+struct Phase {
+  hipStream_t st;
+  PhaseRec rec{};
+  bool on = false;
+  Phase(const char* name, hipStream_t s) : st(s) {
+    if (!g_prof) return;
+    rec.name = name;
+    if (hipEventCreate(&rec.a) != hipSuccess) return;
+    if (hipEventCreate(&rec.b) != hipSuccess) { (void)hipEventDestroy(rec.a); return; }
+    (void)hipEventRecord(rec.a, st);
+    on = true;
+  }
+  ~Phase() {
+    if (!on) return;
+    (void)hipEventRecord(rec.b, st);
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_recs.push_back(rec);
+  }
+};
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char* e = std::getenv("MOBA_DEBUG_SYNC");
+    return e && e[0] && e[0] != '0';
+  }();
+  return on;
+}
+
+#define MOBA_LAUNCH(expr)                                         \
+  do {                                                            \
+    hipError_t e_ = (expr);                                       \
+    if (e_ != hipSuccess) return MOBA_ERR_HIP;                    \
+    if (debug_sync() && hipStreamSynchronize(stream) != hipSuccess) \
+      return MOBA_ERR_HIP;                                        \
+  } while (0)
+
+size_t workspace_limit() {
+  const char* e = std::getenv("MOBA_WORKSPACE_LIMIT_BYTES");
+  if (!e || !e[0]) return kDefaultWorkspaceLimit;
+  char* end = nullptr;
+  unsigned long long v = std::strtoull(e, &end, 10);
+  return (end && *end == 0) ? (size_t)v : kDefaultWorkspaceLimit;
+}
+
+// ------------------------------------------------------------- validation
+struct View {
+  void* data;
+  int64_t st, sh;  // token and head strides, elements
+  int64_t H;
+};
+
+// Number of elements a descriptor spans (0 if any dimension is empty).
+int64_t numel(const moba_tensor* t) {
+  int64_t n = 1;
+  for (int d = 0; d < t->ndim && d < 4; d++) n *= std::max<int64_t>(t->shape[d], 0);
+  return n;
+}
+
+// A data pointer may be NULL only for an empty tensor.
+bool missing(const moba_tensor* t) { return !t || (!t->data && (t->ndim < 1 || t->ndim > 4 || numel(t) > 0)); }
+
+moba_status check_3d(const moba_tensor* t, int dtype, View* v) {
+  if (missing(t)) return MOBA_ERR_NULL;
+  if (t->dtype != dtype) return MOBA_ERR_DTYPE;
+  if (t->ndim != 3) return MOBA_ERR_SHAPE;
+  if (t->shape[0] < 0 || t->shape[1] < 1) return MOBA_ERR_SHAPE;
+  if (t->shape[2] != kHeadDim) return MOBA_ERR_UNSUPPORTED;
+  if (t->stride[2] != 1 || t->stride[0] < 0 || t->stride[1] < 0) return MOBA_ERR_LAYOUT;
+  // 16-byte vector accesses: base and both strides must keep rows 16-byte aligned
+  const int64_t per16 = dtype == MOBA_BF16 ? 8 : 4;
+  if ((reinterpret_cast<uintptr_t>(t->data) & 15) != 0 || t->stride[0] % per16 != 0 ||
+      t->stride[1] % per16 != 0)
+    return MOBA_ERR_LAYOUT;
+  v->data = t->data;
+  v->st = t->stride[0];
+  v->sh = t->stride[1];
+  v->H = t->shape[1];
+  return MOBA_OK;
+}
+
+moba_status check_contig(const moba_tensor* t, int dtype, int ndim, const int64_t* shape) {
+  if (missing(t)) return MOBA_ERR_NULL;
+  if (t->dtype != dtype) return MOBA_ERR_DTYPE;
+  if (t->ndim != ndim) return MOBA_ERR_SHAPE;
+  for (int d = 0; d < ndim; d++)
+    if (t->shape[d] != shape[d]) return MOBA_ERR_SHAPE;
+  if (numel(t) == 0) return MOBA_OK;  // strides of an empty tensor are irrelevant
+  int64_t expect = 1;
+  for (int d = ndim - 1; d >= 0; d--) {
+    if (t->shape[d] > 1 && t->stride[d] != expect) return MOBA_ERR_LAYOUT;
+    expect *= shape[d];
+  }
+  return MOBA_OK;
+}
+
+// Descriptor-level checks of cu_seqlens (no data access).
+moba_status check_cu_desc(const moba_tensor* cu) {
+  if (!cu || !cu->data) return MOBA_ERR_NULL;
+  if (cu->dtype != MOBA_I32) return MOBA_ERR_DTYPE;
+  if (cu->ndim != 1 || cu->shape[0] < 1) return MOBA_ERR_SHAPE;
+  if (cu->shape[0] > 1 && cu->stride[0] != 1) return MOBA_ERR_LAYOUT;
+  return MOBA_OK;
+}
+
+// Copy cu_seqlens to the host (one sync if it lives on the device) and check it.
+moba_status read_cu(const moba_tensor* cu, int64_t T, std::vector<int32_t>* out) {
+  const int64_t n = cu->shape[0];
+  out->resize(n);
+  hipPointerAttribute_t attr;
+  bool on_device = false;
+  if (hipPointerGetAttributes(&attr, cu->data) == hipSuccess)
+    on_device = attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged;
+  else
+    (void)hipGetLastError();  // plain host memory: clear the lookup error
+  if (on_device) {
+    if (hipMemcpy(out->data(), cu->data, n * sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+      return MOBA_ERR_HIP;
+  } else {
+    std::memcpy(out->data(), cu->data, n * sizeof(int32_t));
+  }
+  const std::vector<int32_t>& c = *out;
+  if (c[0] != 0) return MOBA_ERR_SEQLENS;
+  for (int64_t s = 0; s + 1 < n; s++)
+    if (c[s + 1] < c[s]) return MOBA_ERR_SEQLENS;
+  if (c[n - 1] != T) return MOBA_ERR_SEQLENS;
+  return MOBA_OK;
+}
+
+// ------------------------------------------------------------- planning
+enum TileMode { kTilesNone = 0, kTilesCur = 1, kTilesDense = 2 };
+
+struct Plan {
+  Problem p{};
+  std::vector<SeqInfo> seqs;
+  std::vector<CausalTile> tiles;
+  int64_t hist_per_head = 0;  // history selections of one query head, summed over tokens
+};
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// B = 0 means "one block per sequence" (dense attention).
+void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk, TileMode mode,
+                Plan* pl) {
+  Problem& p = pl->p;
+  const int S = (int)cu.size() - 1;
+  p.T = cu[S];
+  p.Hq = Hq;
+  p.Hkv = Hkv;
+  p.G = Hq / Hkv;
+  p.S = S;
+  p.B = B;
+  p.topk = topk;
+  p.gate_tw = std::max(1, 256 / p.G);
+  p.route_rt = std::max(1, kRouteRows / p.G);
+  pl->seqs.assign(S, SeqInfo{});
+  int64_t blk = 0, vt = 0, gate = 0, rc = 0, hw = 0, hist = 0;
+  int nbmax = 0;
+  const int64_t kh = topk - 1;
+  for (int s = 0; s < S; s++) {
+    SeqInfo& q = pl->seqs[s];
+    const int64_t L = (int64_t)cu[s + 1] - cu[s];
+    const int64_t Bs = B > 0 ? B : std::max<int64_t>(L, 1);
+    const int64_t nb = ceil_div(L, Bs);
+    q.tok_start = cu[s];
+    q.len = (int32_t)L;
+    q.blk_off = (int32_t)blk;
+    q.nblk = (int32_t)nb;
+    q.vt_tile_off = (int32_t)vt;
+    q.gate_off = (int32_t)gate;
+    q.rc_off = (int32_t)rc;
+    q.hist_off = hw;
+    blk += nb;
+    vt += ceil_div(L, kKeyTile);
+    gate += ceil_div(L, p.gate_tw);
+    rc += ceil_div(L, p.route_rt);
+    hw += ceil_div(L, p.route_rt) * nb;
+    nbmax = std::max<int>(nbmax, (int)nb);
+    if (B > 0)
+      for (int64_t c = 0; c < nb; c++) {
+        const int64_t m = std::min<int64_t>(L, (c + 1) * B) - c * B;
+        hist += m * std::min<int64_t>(kh, c);
+      }
+  }
+  p.nblk_total = (int)blk;
+  p.nblk_max = nbmax;
+  p.vt_tiles = vt;
+  p.gate_groups = gate;
+  p.route_chunks = rc;
+  p.hist_words = hw;
+  pl->hist_per_head = hist;
+  p.hist_entries = hist * Hq;
+
+  pl->tiles.clear();
+  if (mode == kTilesNone) return;
+  const int tt = std::max(1, kTileRows / p.G);  // tokens per causal tile
+  for (int s = 0; s < S; s++) {
+    const int64_t L = (int64_t)cu[s + 1] - cu[s];
+    const int64_t Bs = mode == kTilesCur ? B : std::max<int64_t>(L, 1);
+    for (int64_t b0 = 0; b0 < L; b0 += Bs) {
+      const int64_t b1 = std::min(L, b0 + Bs);
+      for (int64_t t0 = b0; t0 < b1; t0 += tt)
+        pl->tiles.push_back(CausalTile{s, (int32_t)(cu[s] + t0),
+                                       (int32_t)(cu[s] + std::min(b1, t0 + tt)),
+                                       (int32_t)(cu[s] + b0)});
+    }
+  }
+  // longest key range first, so the long tiles start early
+  std::stable_sort(pl->tiles.begin(), pl->tiles.end(), [](const CausalTile& x, const CausalTile& y) {
+    return (x.t1 - x.kbeg) > (y.t1 - y.kbeg);
+  });
+}
+
+// ------------------------------------------------------------- device cache
+struct DevCache {
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  void* tab = nullptr;
+  size_t tab_bytes = 0;
+  std::vector<int64_t> tab_key;
+  Plan plan;  // plan whose tables are on the device
+};
+std::mutex g_mu;
+std::map<int, DevCache> g_dev;
+
+DevCache* cache_for_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  return &g_dev[dev];
+}
+
+moba_status ensure_workspace(DevCache* dc, size_t bytes) {
+  if (bytes <= dc->ws_bytes) return MOBA_OK;
+  if (dc->ws) {
+    if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
+    (void)hipFree(dc->ws);
+    dc->ws = nullptr;
+    dc->ws_bytes = 0;
+  }
+  const size_t sz = (bytes + (size_t(1) << 20) - 1) & ~((size_t(1) << 20) - 1);
+  if (hipMalloc(&dc->ws, sz) != hipSuccess) {
+    (void)hipGetLastError();
+    dc->ws = nullptr;
+    return MOBA_ERR_NO_MEMORY;
+  }
+  dc->ws_bytes = sz;
+  return MOBA_OK;
+}
+
+// Plan for (cu, heads, B, topk, mode), with its tables resident on the device.
+// Rebuilt only when the key changes; the rebuild synchronizes the device
+// because kernels of earlier calls may still read the old tables.
+moba_status get_plan(DevCache* dc, const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk,
+                     TileMode mode, const Plan** out, const SeqInfo** d_seqs,
+                     const CausalTile** d_tiles) {
+  std::vector<int64_t> key = {Hq, Hkv, B, topk, mode, (int64_t)cu.size()};
+  key.insert(key.end(), cu.begin(), cu.end());
+  if (key != dc->tab_key || !dc->tab) {
+    Plan pl;
+    build_plan(cu, Hq, Hkv, B, topk, mode, &pl);
+    const size_t sb = pl.seqs.size() * sizeof(SeqInfo);
+    const size_t need = ((sb + kAlign - 1) / kAlign) * kAlign + pl.tiles.size() * sizeof(CausalTile) + kAlign;
+    if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
+    if (need > dc->tab_bytes) {
+      if (dc->tab) (void)hipFree(dc->tab);
+      dc->tab = nullptr;
+      dc->tab_bytes = 0;
+      if (hipMalloc(&dc->tab, need) != hipSuccess) {
+        (void)hipGetLastError();
+        dc->tab_key.clear();
+        return MOBA_ERR_NO_MEMORY;
+      }
+      dc->tab_bytes = need;
+    }
+    char* base = static_cast<char*>(dc->tab);
+    if (sb && hipMemcpy(base, pl.seqs.data(), sb, hipMemcpyHostToDevice) != hipSuccess)
+      return MOBA_ERR_HIP;
+    const size_t toff = ((sb + kAlign - 1) / kAlign) * kAlign;
+    if (!pl.tiles.empty() &&
+        hipMemcpy(base + toff, pl.tiles.data(), pl.tiles.size() * sizeof(CausalTile),
+                  hipMemcpyHostToDevice) != hipSuccess)
+      return MOBA_ERR_HIP;
+    dc->plan = std::move(pl);
+    dc->tab_key = std::move(key);
+  }
+  const size_t sb = dc->plan.seqs.size() * sizeof(SeqInfo);
+  *out = &dc->plan;
+  *d_seqs = static_cast<const SeqInfo*>(dc->tab);
+  *d_tiles = reinterpret_cast<const CausalTile*>(static_cast<char*>(dc->tab) +
+                                                 ((sb + kAlign - 1) / kAlign) * kAlign);
+  return MOBA_OK;
+}
+
+// Bump allocator over the workspace; the first pass (base == nullptr) sizes it.
+struct Bump {
+  char* base;
+  size_t off = 0;
+  explicit Bump(void* b) : base(static_cast<char*>(b)) {}
+  template <typename T>
+  T* take(int64_t n) {
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += (size_t)std::max<int64_t>(n, 0) * sizeof(T);
+    return p;
+  }
+};
+
+struct Inputs {
+  View q, k, v;
+  bool bf16;
+  int64_t T;
+  int Hq, Hkv;
+  std::vector<int32_t> cu;
+};
+
+// Checks shared by moba_forward and moba_dense_forward.
+moba_status check_inputs(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                         const moba_tensor* cu, const moba_tensor* out, const moba_tensor* lse,
+                         Inputs* in, View* vo) {
+  if (missing(q) || missing(k) || missing(v) || missing(out) || missing(lse) || !cu || !cu->data)
+    return MOBA_ERR_NULL;
+  if (q->dtype != MOBA_BF16 && q->dtype != MOBA_F32) return MOBA_ERR_DTYPE;
+  moba_status st;
+  if ((st = check_3d(q, q->dtype, &in->q)) != MOBA_OK) return st;
+  if ((st = check_3d(k, q->dtype, &in->k)) != MOBA_OK) return st;
+  if ((st = check_3d(v, q->dtype, &in->v)) != MOBA_OK) return st;
+  if ((st = check_3d(out, q->dtype, vo)) != MOBA_OK) return st;
+  in->T = q->shape[0];
+  in->Hq = (int)q->shape[1];
+  in->Hkv = (int)k->shape[1];
+  if (k->shape[0] != in->T || v->shape[0] != in->T || out->shape[0] != in->T) return MOBA_ERR_SHAPE;
+  if (v->shape[1] != in->Hkv || out->shape[1] != in->Hq) return MOBA_ERR_SHAPE;
+  if (in->Hq % in->Hkv != 0) return MOBA_ERR_SHAPE;
+  if (in->Hq / in->Hkv > kTileRows) return MOBA_ERR_UNSUPPORTED;
+  const int64_t lshape[2] = {in->Hq, in->T};
+  if ((st = check_contig(lse, MOBA_F32, 2, lshape)) != MOBA_OK) return st;
+  if ((st = check_cu_desc(cu)) != MOBA_OK) return st;
+  if (in->T >= (int64_t(1) << 31) - kTileRows) return MOBA_ERR_UNSUPPORTED;
+  in->bf16 = q->dtype == MOBA_BF16;
+  return MOBA_OK;
+}
+
+AttnArgs make_args(const Inputs& in, const View& vo, float* lse) {
+  AttnArgs a{};
+  a.q = in.q.data; a.q_st = in.q.st; a.q_sh = in.q.sh;
+  a.k = in.k.data; a.k_st = in.k.st; a.k_sh = in.k.sh;
+  a.v = in.v.data; a.v_st = in.v.st; a.v_sh = in.v.sh;
+  a.out = vo.data; a.o_st = vo.st; a.o_sh = vo.sh;
+  a.lse = lse;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)kHeadDim));
+  return a;
+}
+
+}  // namespace
+
+// ======================================================================= ABI
+extern "C" {
+
+moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                         const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                         moba_tensor* out, moba_tensor* lse, hipStream_t stream) {
+  Inputs in;
+  View vo;
+  moba_status st = check_inputs(q, k, v, cu_seqlens, out, lse, &in, &vo);
+  if (st != MOBA_OK) return st;
+  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (topk < 1) return MOBA_ERR_TOPK;
+  if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
+  if (in.T == 0) return MOBA_OK;
+
+  // blocks per sequence and the effective top-k (more than #blocks changes nothing)
+  int64_t nbmax = 0;
+  for (size_t s = 0; s + 1 < in.cu.size(); s++)
+    nbmax = std::max<int64_t>(nbmax, ceil_div((int64_t)in.cu[s + 1] - in.cu[s], block_size));
+  if (nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
+  const int kk = (int)std::min<int64_t>(topk, nbmax);
+  if (kk - 1 > 63 && kk - 1 < nbmax - 1) return MOBA_ERR_UNSUPPORTED;
+  if ((uint64_t)in.T * in.Hq * (uint64_t)std::max(kk - 1, 1) >= (uint64_t(1) << 32))
+    return MOBA_ERR_UNSUPPORTED;
+
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur, &pl, &d_seqs, &d_tiles)) !=
+      MOBA_OK)
+    return st;
+  const Problem& p = pl->p;
+  const int64_t kh = kk - 1;
+  const int64_t TG = p.T * p.G;
+  const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;
+
+  // workspace: fixed part, then per-kv-head chunk part
+  auto layout = [&](void* base, int nch, Bump* bp, AttnArgs* a, RouteBuffers* rb, float** kbar,
+                    __hip_bfloat16** vt, int32_t** sel) {
+    *kbar = bp->take<float>((int64_t)p.nblk_total * p.Hkv * kHeadDim);
+    *vt = in.bf16 ? bp->take<__hip_bfloat16>((int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim) : nullptr;
+    *sel = bp->take<int32_t>(p.T * p.Hq * kk);
+    rb->hist = bp->take<int32_t>((int64_t)p.Hkv * p.hist_words);
+    rb->bin_count = bp->take<int32_t>(nbins);
+    rb->bin_start = bp->take<int64_t>(nbins + 1);
+    rb->bin_tile_start = bp->take<int32_t>(nbins + 1);
+    rb->entries = bp->take<uint32_t>(p.hist_entries);
+    const int64_t rows = (int64_t)nch * TG;
+    a->o_part = bp->take<float>(rows * kh * kHeadDim);
+    a->lse_part = bp->take<float>(rows * kh);
+    a->o_cur = bp->take<float>(rows * kHeadDim);
+    a->lse_cur = bp->take<float>(rows);
+    (void)base;
+  };
+  const size_t limit = workspace_limit();
+  int nch = 0;
+  size_t need = 0;
+  for (int n = p.Hkv; n >= 1; n--) {
+    Bump bp(nullptr);
+    AttnArgs a{};
+    RouteBuffers rb{};
+    float* kb;
+    __hip_bfloat16* vt;
+    int32_t* sel;
+    layout(nullptr, n, &bp, &a, &rb, &kb, &vt, &sel);
+    if (bp.off + kAlign <= limit) { nch = n; need = bp.off + kAlign; break; }
+  }
+  if (nch == 0) return MOBA_ERR_NO_MEMORY;
+  if ((st = ensure_workspace(dc, need)) != MOBA_OK) return st;
+
+  Bump bp(dc->ws);
+  AttnArgs a = make_args(in, vo, static_cast<float*>(lse->data));
+  RouteBuffers rb{};
+  float* kbar;
+  __hip_bfloat16* vt;
+  int32_t* sel;
+  layout(dc->ws, nch, &bp, &a, &rb, &kbar, &vt, &sel);
+  a.vt = vt;
+  a.seqs = d_seqs;
+  a.bin_tile_start = rb.bin_tile_start;
+  a.bin_start = rb.bin_start;
+  a.bin_count = rb.bin_count;
+  a.entries = rb.entries;
+  a.tiles = d_tiles;
+  a.ntiles = (int64_t)pl->tiles.size();
+
+  { Phase ph("pool", stream);
+    MOBA_LAUNCH(launch_pool(in.k.data, in.bf16, in.k.st, in.k.sh, d_seqs, p, kbar, stream)); }
+  if (in.bf16) {
+    Phase ph("vt_pack", stream);
+    MOBA_LAUNCH(launch_vt_pack(static_cast<const __hip_bfloat16*>(in.v.data), in.v.st, in.v.sh,
+                               d_seqs, p, vt, stream));
+  }
+  { Phase ph("gate", stream);
+    MOBA_LAUNCH(launch_gate(in.q.data, in.bf16, in.q.st, in.q.sh, kbar, d_seqs, p, sel, nullptr, 0,
+                            stream)); }
+  if (kh > 0 && p.hist_entries > 0) {
+    Phase ph("route", stream);
+    MOBA_LAUNCH(launch_route(sel, d_seqs, p, rb, stream));
+  }
+  for (int g0 = 0; g0 < p.Hkv; g0 += nch) {
+    a.g0 = g0;
+    a.g1 = std::min(p.Hkv, g0 + nch);
+    const int64_t e_chunk = pl->hist_per_head * p.G * (a.g1 - a.g0);
+    if (kh > 0 && e_chunk > 0) {
+      const int64_t grid = ceil_div(e_chunk, kTileRows) + (int64_t)(a.g1 - a.g0) * p.nblk_total;
+      Phase ph("attn_hist", stream);
+      MOBA_LAUNCH(in.bf16 ? launch_attn_hist_bf16(a, p, grid, stream)
+                          : launch_attn_hist_f32(a, p, grid, stream));
+    }
+    { Phase ph("attn_cur", stream);
+      MOBA_LAUNCH(in.bf16 ? launch_attn_causal_bf16(false, a, p, stream)
+                          : launch_attn_causal_f32(false, a, p, stream)); }
+    { Phase ph("merge", stream);
+      MOBA_LAUNCH(launch_merge(in.bf16, a, p, stream)); }
+  }
+  return MOBA_OK;
+}
+
+moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                               const moba_tensor* cu_seqlens, moba_tensor* out, moba_tensor* lse,
+                               hipStream_t stream) {
+  Inputs in;
+  View vo;
+  moba_status st = check_inputs(q, k, v, cu_seqlens, out, lse, &in, &vo);
+  if (st != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
+  if (in.T == 0) return MOBA_OK;
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, 0, 1, kTilesDense, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
+    return st;
+  const Problem& p = pl->p;
+  Bump sz(nullptr);
+  sz.take<__hip_bfloat16>(in.bf16 ? (int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim : 0);
+  if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
+  if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
+  Bump bp(dc->ws);
+  AttnArgs a = make_args(in, vo, static_cast<float*>(lse->data));
+  __hip_bfloat16* vt =
+      bp.take<__hip_bfloat16>(in.bf16 ? (int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim : 0);
+  a.vt = vt;
+  a.seqs = d_seqs;
+  a.tiles = d_tiles;
+  a.ntiles = (int64_t)pl->tiles.size();
+  a.g0 = 0;
+  a.g1 = p.Hkv;
+  if (in.bf16) {
+    Phase ph("vt_pack", stream);
+    MOBA_LAUNCH(launch_vt_pack(static_cast<const __hip_bfloat16*>(in.v.data), in.v.st, in.v.sh,
+                               d_seqs, p, vt, stream));
+  }
+  { Phase ph("dense", stream);
+    MOBA_LAUNCH(in.bf16 ? launch_attn_causal_bf16(true, a, p, stream)
+                        : launch_attn_causal_f32(true, a, p, stream)); }
+  return MOBA_OK;
+}
+
+moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32_t block_size,
+                      moba_tensor* kbar, hipStream_t stream) {
+  if (missing(k) || missing(kbar) || !cu_seqlens || !cu_seqlens->data) return MOBA_ERR_NULL;
+  if (k->dtype != MOBA_BF16 && k->dtype != MOBA_F32) return MOBA_ERR_DTYPE;
+  View vk;
+  moba_status st = check_3d(k, k->dtype, &vk);
+  if (st != MOBA_OK) return st;
+  if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
+  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  std::vector<int32_t> cu;
+  if ((st = read_cu(cu_seqlens, k->shape[0], &cu)) != MOBA_OK) return st;
+  const int Hkv = (int)k->shape[1];
+  int64_t nb = 0;
+  for (size_t s = 0; s + 1 < cu.size(); s++) nb += ceil_div((int64_t)cu[s + 1] - cu[s], block_size);
+  const int64_t shp[3] = {nb, Hkv, kHeadDim};
+  if ((st = check_contig(kbar, MOBA_F32, 3, shp)) != MOBA_OK) return st;
+  if (nb == 0) return MOBA_OK;
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  if ((st = get_plan(dc, cu, Hkv, Hkv, block_size, 1, kTilesNone, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
+    return st;
+  Phase ph("pool", stream);
+  MOBA_LAUNCH(launch_pool(vk.data, k->dtype == MOBA_BF16, vk.st, vk.sh, d_seqs, pl->p,
+                          static_cast<float*>(kbar->data), stream));
+  return MOBA_OK;
+}
+
+moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_tensor* cu_seqlens,
+                        int32_t block_size, int32_t topk, moba_tensor* sel, moba_tensor* scores,
+                        hipStream_t stream) {
+  if (missing(q) || missing(k) || missing(sel) || !cu_seqlens || !cu_seqlens->data)
+    return MOBA_ERR_NULL;
+  if (q->dtype != MOBA_BF16 && q->dtype != MOBA_F32) return MOBA_ERR_DTYPE;
+  View vq, vk;
+  moba_status st;
+  if ((st = check_3d(q, q->dtype, &vq)) != MOBA_OK) return st;
+  if ((st = check_3d(k, q->dtype, &vk)) != MOBA_OK) return st;
+  const int64_t T = q->shape[0];
+  const int Hq = (int)q->shape[1], Hkv = (int)k->shape[1];
+  if (k->shape[0] != T || Hq % Hkv != 0) return MOBA_ERR_SHAPE;
+  if (Hq / Hkv > kTileRows) return MOBA_ERR_UNSUPPORTED;
+  if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
+  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (topk < 1) return MOBA_ERR_TOPK;
+  const int64_t sshape[3] = {T, Hq, topk};
+  if ((st = check_contig(sel, MOBA_I32, 3, sshape)) != MOBA_OK) return st;
+  int nmax = 0;
+  if (scores) {
+    if (missing(scores)) return MOBA_ERR_NULL;
+    if (scores->ndim != 3) return MOBA_ERR_SHAPE;
+    const int64_t scs[3] = {T, Hq, scores->shape[2]};
+    if (scores->shape[2] < 1 || scores->shape[2] > (1 << 20)) return MOBA_ERR_SHAPE;
+    if ((st = check_contig(scores, MOBA_F32, 3, scs)) != MOBA_OK) return st;
+    nmax = (int)scores->shape[2];
+  }
+  std::vector<int32_t> cu;
+  if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
+  if (T == 0) return MOBA_OK;
+  int64_t nbmax = 0;
+  for (size_t s = 0; s + 1 < cu.size(); s++)
+    nbmax = std::max<int64_t>(nbmax, ceil_div((int64_t)cu[s + 1] - cu[s], block_size));
+  if (topk - 1 > 63 && topk - 1 < nbmax - 1) return MOBA_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  if ((st = get_plan(dc, cu, Hq, Hkv, block_size, topk, kTilesNone, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
+    return st;
+  const Problem& p = pl->p;
+  Bump sz(nullptr);
+  sz.take<float>((int64_t)p.nblk_total * Hkv * kHeadDim);
+  if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
+  if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
+  Bump bp(dc->ws);
+  float* kbar = bp.take<float>((int64_t)p.nblk_total * Hkv * kHeadDim);
+  { Phase ph("pool", stream);
+    MOBA_LAUNCH(launch_pool(vk.data, q->dtype == MOBA_BF16, vk.st, vk.sh, d_seqs, p, kbar, stream)); }
+  { Phase ph("gate", stream);
+    MOBA_LAUNCH(launch_gate(vq.data, q->dtype == MOBA_BF16, vq.st, vq.sh, kbar, d_seqs, p,
+                            static_cast<int32_t*>(sel->data),
+                            scores ? static_cast<float*>(scores->data) : nullptr, nmax, stream)); }
+  return MOBA_OK;
+}
+
+moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, int32_t block_size,
+                       int32_t num_kv_heads, moba_tensor* counts, moba_tensor* offsets,
+                       moba_tensor* entries, hipStream_t stream) {
+  if (missing(sel) || !cu_seqlens || !cu_seqlens->data || missing(counts) || missing(offsets) ||
+      !entries)
+    return MOBA_ERR_NULL;
+  if (sel->dtype != MOBA_I32) return MOBA_ERR_DTYPE;
+  if (sel->ndim != 3) return MOBA_ERR_SHAPE;
+  const int64_t T = sel->shape[0];
+  const int Hq = (int)sel->shape[1];
+  const int topk = (int)sel->shape[2];
+  const int64_t ss[3] = {T, Hq, topk};
+  moba_status st;
+  if ((st = check_contig(sel, MOBA_I32, 3, ss)) != MOBA_OK) return st;
+  if (num_kv_heads < 1 || Hq < 1 || Hq % num_kv_heads != 0) return MOBA_ERR_SHAPE;
+  if (Hq / num_kv_heads > kTileRows) return MOBA_ERR_UNSUPPORTED;
+  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (topk < 1) return MOBA_ERR_TOPK;
+  if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
+  std::vector<int32_t> cu;
+  if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
+  int64_t nbmax = 0, nb = 0;
+  for (size_t s = 0; s + 1 < cu.size(); s++) {
+    const int64_t n = ceil_div((int64_t)cu[s + 1] - cu[s], block_size);
+    nbmax = std::max(nbmax, n);
+    nb += n;
+  }
+  if (nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
+  if ((uint64_t)T * Hq * (uint64_t)std::max(topk - 1, 1) >= (uint64_t(1) << 32))
+    return MOBA_ERR_UNSUPPORTED;
+  const int64_t nbins = nb * num_kv_heads;
+  const int64_t cs[1] = {nbins};
+  const int64_t os[1] = {nbins + 1};
+  if ((st = check_contig(counts, MOBA_I32, 1, cs)) != MOBA_OK) return st;
+  if ((st = check_contig(offsets, MOBA_I64, 1, os)) != MOBA_OK) return st;
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  if ((st = get_plan(dc, cu, Hq, num_kv_heads, block_size, topk, kTilesNone, &pl, &d_seqs,
+                     &d_tiles)) != MOBA_OK)
+    return st;
+  const Problem& p = pl->p;
+  const int64_t es[1] = {p.hist_entries};
+  if (p.hist_entries > 0) {
+    if (missing(entries)) return MOBA_ERR_NULL;
+    if ((st = check_contig(entries, MOBA_I32, 1, es)) != MOBA_OK) return st;
+  } else if (entries->ndim != 1 || entries->shape[0] != 0) {
+    return MOBA_ERR_SHAPE;
+  }
+  if (nbins == 0) return MOBA_OK;
+  Bump sz(nullptr);
+  sz.take<int32_t>((int64_t)p.Hkv * p.hist_words);
+  sz.take<int32_t>(nbins + 1);
+  if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
+  if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
+  Bump bp(dc->ws);
+  RouteBuffers rb{};
+  rb.hist = bp.take<int32_t>((int64_t)p.Hkv * p.hist_words);
+  rb.bin_tile_start = bp.take<int32_t>(nbins + 1);
+  rb.bin_count = static_cast<int32_t*>(counts->data);
+  rb.bin_start = static_cast<int64_t*>(offsets->data);
+  rb.entries = static_cast<uint32_t*>(entries->data);
+  Phase ph("route", stream);
+  MOBA_LAUNCH(launch_route(static_cast<const int32_t*>(sel->data), d_seqs, p, rb, stream));
+  return MOBA_OK;
+}
+
+size_t moba_workspace_bytes(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  auto it = g_dev.find(dev);
+  return it == g_dev.end() ? 0 : it->second.ws_bytes;
+}
+
+moba_status moba_release_workspace(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOBA_ERR_HIP;
+  auto it = g_dev.find(dev);
+  if (it == g_dev.end()) return MOBA_OK;
+  if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
+  if (it->second.ws) (void)hipFree(it->second.ws);
+  if (it->second.tab) (void)hipFree(it->second.tab);
+  g_dev.erase(it);
+  return MOBA_OK;
+}
+
+const char* moba_status_string(moba_status s) {
+  switch (s) {
+    case MOBA_OK: return "MOBA_OK";
+    case MOBA_ERR_NULL: return "MOBA_ERR_NULL";
+    case MOBA_ERR_DTYPE: return "MOBA_ERR_DTYPE";
+    case MOBA_ERR_SHAPE: return "MOBA_ERR_SHAPE";
+    case MOBA_ERR_LAYOUT: return "MOBA_ERR_LAYOUT";
+    case MOBA_ERR_BLOCK_SIZE: return "MOBA_ERR_BLOCK_SIZE";
+    case MOBA_ERR_TOPK: return "MOBA_ERR_TOPK";
+    case MOBA_ERR_SEQLENS: return "MOBA_ERR_SEQLENS";
+    case MOBA_ERR_UNSUPPORTED: return "MOBA_ERR_UNSUPPORTED";
+    case MOBA_ERR_NO_MEMORY: return "MOBA_ERR_NO_MEMORY";
+    case MOBA_ERR_HIP: return "MOBA_ERR_HIP";
+  }
+  return "MOBA_ERR_UNKNOWN";
+}
+
+void moba_profile_enable(int enabled) { g_prof = enabled != 0; }
+
+int moba_profile_read(moba_phase_stat* stats, int max_phases) {
+  std::vector<PhaseRec> recs;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    recs.swap(g_recs);
+  }
+  std::vector<moba_phase_stat> acc;
+  for (const PhaseRec& r : recs) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      auto it = std::find_if(acc.begin(), acc.end(),
+                             [&](const moba_phase_stat& x) { return std::strcmp(x.name, r.name) == 0; });
+      if (it == acc.end()) {
+        moba_phase_stat z{};
+        std::strncpy(z.name, r.name, sizeof(z.name) - 1);
+        acc.push_back(z);
+        it = acc.end() - 1;
+      }
+      it->launches += 1;
+      it->total_ms += ms;
+    }
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  const int n = std::min<int>((int)acc.size(), std::max(max_phases, 0));
+  for (int i = 0; i < n; i++) stats[i] = acc[i];
+  return n;
+}
+
+}  // extern "C"

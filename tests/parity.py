@@ -1,0 +1,151 @@
+"""Comparison helpers for the GPU parity tests: run the library and the fp64
+oracle on the same inputs and compare selections and outputs.
+
+Selection rule.  On fp32 inputs the selection must equal the oracle's
+exactly.  On bf16 inputs the fp32 gate may order two blocks whose exact
+scores are closer than its rounding error differently from the fp64 oracle;
+such a row is accepted iff every block the GPU kept instead of an oracle block
+is tie-explained: s_oracle_block - s_gpu_block <= tau_a + tau_b, with
+tau_j = 2^-14 * sum_i |q_i| * mean_over_block(|K[., g, i]|) (a bound on the
+fp32 rounding of the block mean and the 128-term dot product, with margin).
+Outputs of tie-explained rows are compared with the oracle's attention over
+the GPU's own selection.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import oracle
+from paper_2502_13189_amd import binding, inputs
+
+TAU_SCALE = 2.0 ** -14
+
+# output tolerances: max-abs and mean-abs for bf16; max-abs for fp32
+BF16_MAX_ABS, BF16_MEAN_ABS = 2e-2, 2e-3
+F32_MAX_ABS = 1e-4
+LSE_ABS = {"bf16": 1e-3, "f32": 1e-5}
+
+
+def host_inputs(q, k, v):
+    return inputs.to_oracle(q), inputs.to_oracle(k), inputs.to_oracle(v)
+
+
+def block_offsets(cu, B):
+    cu = list(cu)
+    off, acc = [], 0
+    for s in range(len(cu) - 1):
+        off.append(acc)
+        acc += (cu[s + 1] - cu[s] + B - 1) // B
+    return off
+
+
+def seq_of_tokens(cu, t):
+    cu = np.asarray(cu)
+    return np.searchsorted(cu, t, side="right") - 1
+
+
+def check_selection(gpu_sel, rows, qn, kn, cu, B, topk, exact):
+    """Compare GPU selections (for `rows`) with the oracle's.  Returns
+    (oracle_sel, mismatch_rows).  Raises AssertionError on a mismatch that is
+    not allowed."""
+    cu = np.asarray(cu)
+    kbar, kabs = oracle.pool(kn, cu, B, with_abs=True)
+    osel = oracle.select(qn, kbar, cu, B, topk, rows=rows)
+    gsel = np.asarray(gpu_sel).reshape(len(rows), topk)
+    bad = np.nonzero((gsel != osel).any(axis=1))[0]
+    if exact:
+        assert bad.size == 0, "selection differs on %d rows, first rows %s" % (bad.size, rows[bad[:5]])
+        return osel, bad
+    if bad.size == 0:
+        return osel, bad
+    Hq = qn.shape[1]
+    G = Hq // kn.shape[1]
+    nmax = int(max(osel.max(), gsel.max())) + 1
+    _, sc = oracle.select(qn, kbar, cu, B, topk, rows=rows[bad], nmax=nmax)
+    boff = block_offsets(cu, B)
+    qf = np.abs(_widen(qn))
+    af = kabs
+    for n, i in enumerate(bad):
+        r = int(rows[i])
+        t, h = r // Hq, r % Hq
+        g = h // G
+        s = int(seq_of_tokens(cu, t))
+        o_set = set(int(x) for x in osel[i] if x >= 0)
+        g_set = set(int(x) for x in gsel[i] if x >= 0)
+        assert len(o_set) == len(g_set) and max(o_set) == max(g_set), (r, o_set, g_set)
+        for jg in g_set - o_set:
+            for jo in o_set - g_set:
+                tau = TAU_SCALE * (qf[t, h] @ af[boff[s] + jg, g] + qf[t, h] @ af[boff[s] + jo, g])
+                gap = sc[n, jo] - sc[n, jg]
+                assert gap <= tau, ("row %d: GPU kept block %d over block %d, score gap %.3e > "
+                                    "tolerance %.3e" % (r, jg, jo, gap, tau))
+    return osel, bad
+
+
+def _widen(x):
+    if x.dtype == np.uint16:
+        return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return x.astype(np.float64)
+
+
+def compare_outputs(gout, glse, oout, olse, dtype, what=""):
+    gout = np.asarray(gout, dtype=np.float64)
+    err = np.abs(gout - oout)
+    lerr = np.abs(np.asarray(glse, np.float64) - olse)
+    if dtype == "f32":
+        assert err.max() <= F32_MAX_ABS, "%s out max-abs %.3e" % (what, err.max())
+    else:
+        assert err.max() <= BF16_MAX_ABS, "%s out max-abs %.3e" % (what, err.max())
+        assert err.mean() <= BF16_MEAN_ABS, "%s out mean-abs %.3e" % (what, err.mean())
+    assert lerr.max() <= LSE_ABS[dtype], "%s lse max-abs %.3e" % (what, lerr.max())
+    return float(err.max()), float(err.mean()), float(lerr.max())
+
+
+def gather_rows(out, lse, rows):
+    """Rows (t*Hq+h) of a GPU output [T, Hq, D] and lse [Hq, T], on the host."""
+    T, Hq, D = out.shape
+    rows_t = torch.as_tensor(rows, dtype=torch.int64, device=out.device)
+    t, h = rows_t // Hq, rows_t % Hq
+    o = out[t, h].float().cpu().numpy()
+    l = lse[h, t].float().cpu().numpy()
+    return o, l
+
+
+def moba_parity(q, k, v, cu, B, topk, rows=None, dtype="bf16", exact_sel=None):
+    """Run the library and the oracle; assert selection and output parity on
+    `rows` (all rows if None).  Returns a dict of error figures."""
+    cu_t = cu if isinstance(cu, torch.Tensor) else torch.tensor(cu, dtype=torch.int32)
+    out, lse = binding.forward(q, k, v, cu_t, B, topk)
+    gsel_full = binding.select(q, k, cu_t, B, topk)
+    torch.cuda.synchronize()
+    T, Hq, D = q.shape
+    if rows is None:
+        rows = np.arange(T * Hq, dtype=np.int64)
+    qn, kn, vn = host_inputs(q, k, v)
+    cun = cu_t.numpy()
+    rows_t = torch.as_tensor(rows, device=q.device)
+    gsel = gsel_full.view(T * Hq, topk)[rows_t].cpu().numpy()
+    exact = (dtype == "f32") if exact_sel is None else exact_sel
+    osel, bad = check_selection(gsel, rows, qn, kn, cun, B, topk, exact)
+    use_sel = osel.copy()
+    use_sel[bad] = gsel[bad]
+    oout, olse = oracle.attend(qn, kn, vn, cun, B, use_sel, rows=rows)
+    gout, glse = gather_rows(out, lse, rows)
+    mx, mean, lmx = compare_outputs(gout, glse, oout, olse, dtype)
+    return {"rows": len(rows), "tie_rows": int(bad.size), "max_abs": mx, "mean_abs": mean,
+            "lse_max_abs": lmx, "out": out, "lse": lse, "sel": gsel_full}
+
+
+def dense_parity(q, k, v, cu, rows=None, dtype="bf16"):
+    cu_t = cu if isinstance(cu, torch.Tensor) else torch.tensor(cu, dtype=torch.int32)
+    out, lse = binding.dense_forward(q, k, v, cu_t)
+    torch.cuda.synchronize()
+    T, Hq, D = q.shape
+    if rows is None:
+        rows = np.arange(T * Hq, dtype=np.int64)
+    qn, kn, vn = host_inputs(q, k, v)
+    oout, olse = oracle.dense(qn, kn, vn, cu_t.numpy(), rows=rows)
+    gout, glse = gather_rows(out, lse, rows)
+    mx, mean, lmx = compare_outputs(gout, glse, oout, olse, dtype, "dense")
+    return {"rows": len(rows), "max_abs": mx, "mean_abs": mean, "lse_max_abs": lmx}

@@ -1,0 +1,190 @@
+"""C ABI checks that need no GPU: libmoba.so loads, exports every function that
+include/moba.h declares, and rejects invalid arguments with the documented
+status before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2502_13189_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moba.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2502_13189_amd import build
+        build.build()
+    return binding.load()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moba_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ["moba_forward", "moba_dense_forward", "moba_pool", "moba_select", "moba_route",
+              "moba_workspace_bytes", "moba_release_workspace", "moba_status_string",
+              "moba_profile_enable", "moba_profile_read"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(lib):
+    for i, name in enumerate(binding.STATUS):
+        assert lib.moba_status_string(i).decode() == name
+
+
+# ---------------------------------------------------------------- validation
+FAKE = 0x10000  # a 16-byte aligned address that validation never dereferences
+
+
+def desc(shape, dtype=binding.MOBA_BF16, data=FAKE, strides=None):
+    d = binding.MobaTensor()
+    d.data = data
+    d.dtype = dtype
+    d.ndim = len(shape)
+    if strides is None:
+        strides, acc = [], 1
+        for s in reversed(shape):
+            strides.insert(0, acc)
+            acc *= s
+    for i, (s, st) in enumerate(zip(shape, strides)):
+        d.shape[i] = s
+        d.stride[i] = st
+    return d
+
+
+class Case:
+    def __init__(self, T=256, hq=4, hkv=2, d=128, dtype=binding.MOBA_BF16, cu=(0, 100, 256)):
+        self.cu_arr = np.array(cu, dtype=np.int32)
+        self.q = desc([T, hq, d], dtype)
+        self.k = desc([T, hkv, d], dtype)
+        self.v = desc([T, hkv, d], dtype)
+        self.out = desc([T, hq, d], dtype)
+        self.lse = desc([hq, T], binding.MOBA_F32)
+        self.cu = desc([len(cu)], binding.MOBA_I32, data=self.cu_arr.ctypes.data)
+
+    def forward(self, lib, B=16, topk=3):
+        r = ctypes.byref
+        return binding.STATUS[lib.moba_forward(r(self.q), r(self.k), r(self.v), r(self.cu), B, topk,
+                                               r(self.out), r(self.lse), None)]
+
+    def dense(self, lib):
+        r = ctypes.byref
+        return binding.STATUS[lib.moba_dense_forward(r(self.q), r(self.k), r(self.v), r(self.cu),
+                                                     r(self.out), r(self.lse), None)]
+
+
+def test_null_pointer(lib):
+    c = Case()
+    c.q.data = None
+    assert c.forward(lib) == "MOBA_ERR_NULL"
+    assert binding.STATUS[lib.moba_forward(None, None, None, None, 16, 3, None, None, None)] == "MOBA_ERR_NULL"
+
+
+def test_dtype_errors(lib):
+    c = Case()
+    c.k.dtype = binding.MOBA_F32
+    assert c.forward(lib) == "MOBA_ERR_DTYPE"
+    c = Case()
+    c.q.dtype = c.k.dtype = c.v.dtype = c.out.dtype = binding.MOBA_I32
+    assert c.forward(lib) == "MOBA_ERR_DTYPE"
+    c = Case()
+    c.lse.dtype = binding.MOBA_BF16
+    assert c.forward(lib) == "MOBA_ERR_DTYPE"
+    c = Case()
+    c.cu.dtype = binding.MOBA_I64
+    assert c.forward(lib) == "MOBA_ERR_DTYPE"
+
+
+def test_shape_errors(lib):
+    c = Case(hq=6, hkv=4)
+    assert c.forward(lib) == "MOBA_ERR_SHAPE"  # Hq not a multiple of Hkv
+    c = Case()
+    c.k.shape[0] = 255
+    assert c.forward(lib) == "MOBA_ERR_SHAPE"
+    c = Case()
+    c.lse.shape[1] = 255
+    assert c.forward(lib) == "MOBA_ERR_SHAPE"
+    c = Case()
+    c.out.shape[1] = 2
+    assert c.forward(lib) == "MOBA_ERR_SHAPE"
+
+
+def test_unsupported(lib):
+    assert Case(d=64).forward(lib) == "MOBA_ERR_UNSUPPORTED"
+    assert Case(hq=256, hkv=1).forward(lib) == "MOBA_ERR_UNSUPPORTED"  # group > 128
+    # more than 4096 blocks in one sequence
+    assert Case(T=5000, cu=(0, 5000)).forward(lib, B=1, topk=2) == "MOBA_ERR_UNSUPPORTED"
+    # 64 < topk-1 < number of past blocks
+    assert Case(T=4096, cu=(0, 4096)).forward(lib, B=8, topk=100) == "MOBA_ERR_UNSUPPORTED"
+
+
+def test_layout_errors(lib):
+    c = Case()
+    c.q.stride[2] = 2
+    assert c.forward(lib) == "MOBA_ERR_LAYOUT"
+    c = Case()
+    c.q.data = FAKE + 2  # not 16-byte aligned
+    assert c.forward(lib) == "MOBA_ERR_LAYOUT"
+    c = Case()
+    c.k.stride[0] = 2 * 128 + 4  # rows not 16-byte aligned for bf16
+    assert c.forward(lib) == "MOBA_ERR_LAYOUT"
+    c = Case()
+    c.lse.stride[0] = 300  # lse must be contiguous [Hq, T]
+    assert c.forward(lib) == "MOBA_ERR_LAYOUT"
+
+
+def test_block_size_and_topk(lib):
+    assert Case().forward(lib, B=0) == "MOBA_ERR_BLOCK_SIZE"
+    assert Case().forward(lib, B=-3) == "MOBA_ERR_BLOCK_SIZE"
+    assert Case().forward(lib, topk=0) == "MOBA_ERR_TOPK"
+
+
+@pytest.mark.parametrize("cu", [(1, 100, 256), (0, 200, 100, 256), (0, 100, 255)])
+def test_seqlens_errors(lib, cu):
+    assert Case(cu=cu).forward(lib) == "MOBA_ERR_SEQLENS"
+    assert Case(cu=cu).dense(lib) == "MOBA_ERR_SEQLENS"
+
+
+def test_empty_problem_is_a_no_op(lib):
+    c = Case(T=0, cu=(0, 0, 0))
+    for t in (c.q, c.k, c.v, c.out, c.lse):
+        t.data = None
+    assert c.forward(lib) == "MOBA_OK"
+    assert c.dense(lib) == "MOBA_OK"
+
+
+def test_debug_exports_validate(lib):
+    r = ctypes.byref
+    c = Case()
+    kbar = desc([0, 2, 128], binding.MOBA_F32)
+    assert binding.STATUS[lib.moba_pool(r(c.k), r(c.cu), 16, r(kbar), None)] == "MOBA_ERR_SHAPE"
+    assert binding.STATUS[lib.moba_pool(r(c.k), r(c.cu), 0, r(kbar), None)] == "MOBA_ERR_BLOCK_SIZE"
+    sel = desc([256, 4, 2], binding.MOBA_I32)
+    assert binding.STATUS[lib.moba_select(r(c.q), r(c.k), r(c.cu), 16, 3, r(sel), None, None)] == "MOBA_ERR_SHAPE"
+    sel = desc([256, 4, 3], binding.MOBA_I32)
+    counts = desc([10], binding.MOBA_I32)
+    offs = desc([11], binding.MOBA_I64)
+    ent = desc([1], binding.MOBA_I32)
+    assert binding.STATUS[lib.moba_route(r(sel), r(c.cu), 16, 2, r(counts), r(offs), r(ent), None)] == "MOBA_ERR_SHAPE"
+    assert binding.STATUS[lib.moba_route(r(sel), r(c.cu), 16, 3, r(counts), r(offs), r(ent), None)] == "MOBA_ERR_SHAPE"
+
+
+def test_binding_refuses_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError):
+        binding.load()

@@ -1,0 +1,223 @@
+"""Parity of the HIP library with the fp64 oracle, through the C ABI.
+
+Small cases cover every row; they span several attention tiles, ragged
+sequence tails, empty sequences, block sizes that do and do not divide the
+64-key tile, GQA groups, fp32 and bf16.  The full-size workloads compare every
+row where the oracle finishes in seconds and a fixed row sample otherwise.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2502_13189_amd import binding, inputs
+from oracle import oracle
+import parity
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _gpu_available():
+    return torch.cuda.is_available()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not _gpu_available():
+        pytest.skip("no GPU")
+    binding.load()
+
+
+def make(seqlens, hq, hkv, dtype, B, offset=0.0, seed=0):
+    q, k, v, cu = inputs.make(seqlens, hq, hkv, 128, dtype, B, offset, seed, device=DEV)
+    return q, k, v, cu
+
+
+SMALL = [
+    # seqlens, hq, hkv, B, topk, dtype
+    ((300,), 2, 2, 64, 3, torch.bfloat16),
+    ((1000, 0, 517), 4, 2, 128, 3, torch.bfloat16),
+    ((777,), 8, 2, 100, 4, torch.bfloat16),
+    ((513, 129, 64), 4, 1, 48, 5, torch.bfloat16),
+    ((640,), 3, 3, 64, 1, torch.bfloat16),
+    ((700,), 4, 4, 96, 20, torch.bfloat16),
+    ((2048,), 16, 2, 256, 3, torch.bfloat16),
+    ((333, 1), 2, 1, 7, 6, torch.bfloat16),
+    ((300,), 2, 2, 64, 3, torch.float32),
+    ((600, 250), 4, 2, 128, 4, torch.float32),
+    ((515,), 2, 1, 50, 3, torch.float32),
+]
+
+
+@pytest.mark.parametrize("seqlens,hq,hkv,B,topk,dtype", SMALL,
+                         ids=["-".join(map(str, c[0])) + "_h%dx%d_B%d_k%d_%s" % (c[1], c[2], c[3], c[4], str(c[5])[6:]) for c in SMALL])
+def test_moba_small(seqlens, hq, hkv, B, topk, dtype):
+    q, k, v, cu = make(seqlens, hq, hkv, dtype, B, offset=0.5, seed=sum(seqlens) + B)
+    r = parity.moba_parity(q, k, v, cu, B, topk, dtype="f32" if dtype == torch.float32 else "bf16")
+    print("rows %d tie_rows %d max_abs %.2e mean_abs %.2e lse %.2e" %
+          (r["rows"], r["tie_rows"], r["max_abs"], r["mean_abs"], r["lse_max_abs"]))
+
+
+@pytest.mark.parametrize("seqlens,hq,hkv,dtype", [
+    ((300,), 2, 2, torch.bfloat16), ((1000, 0, 517), 4, 2, torch.bfloat16),
+    ((129, 64, 1), 8, 1, torch.bfloat16), ((300, 77), 2, 1, torch.float32)])
+def test_dense_small(seqlens, hq, hkv, dtype):
+    q, k, v, cu = make(seqlens, hq, hkv, dtype, 64, seed=7)
+    parity.dense_parity(q, k, v, cu, dtype="f32" if dtype == torch.float32 else "bf16")
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_pool_matches_oracle(dtype):
+    seqlens, B = (1000, 0, 333, 64), 100
+    q, k, v, cu = make(seqlens, 4, 2, dtype, B, offset=0.5, seed=3)
+    kbar = binding.pool(k, cu, B).cpu().numpy().astype(np.float64)
+    ref, kabs = oracle.pool(inputs.to_oracle(k), cu.numpy(), B, with_abs=True)
+    # fp64 accumulation rounded once to fp32: within one fp32 ulp of the mean
+    tol = 2.0 ** -23 * np.abs(ref) + 1e-12 * kabs
+    assert np.all(np.abs(kbar - ref) <= tol)
+
+
+def test_select_constructed_ties():
+    """Every block holds the same keys: all scores tie exactly and the lower
+    block index must win on the GPU too."""
+    B, L, topk = 64, 900, 4
+    q, k, v, cu = make((L,), 4, 2, torch.bfloat16, B, seed=5)
+    blk = k[:B].clone()
+    k = blk.repeat((L + B - 1) // B, 1, 1)[:L].contiguous()
+    sel = binding.select(q, k, cu, B, topk).cpu().numpy()
+    for t in range(L):
+        c = t // B
+        expect = list(range(min(topk - 1, c))) + [c] + [-1] * (topk - 1 - min(topk - 1, c))
+        assert (sel[t] == np.array(expect)).all(), (t, sel[t], expect)
+
+
+def test_select_scores_within_bound():
+    """The GPU's fp32 gate scores stay within the tie tolerance of the fp64
+    scores (this is what justifies the tie-aware comparison)."""
+    seqlens, B, topk = (2000, 900), 128, 3
+    q, k, v, cu = make(seqlens, 4, 2, torch.bfloat16, B, offset=0.5, seed=9)
+    nmax = 16
+    sel, sc = binding.select(q, k, cu, B, topk, nmax=nmax)
+    qn, kn = inputs.to_oracle(q), inputs.to_oracle(k)
+    kbar, kabs = oracle.pool(kn, cu.numpy(), B, with_abs=True)
+    rows = np.arange(q.shape[0] * q.shape[1])
+    _, osc = oracle.select(qn, kbar, cu.numpy(), B, topk, rows=rows, nmax=nmax)
+    gsc = sc.view(-1, nmax).cpu().numpy().astype(np.float64)
+    valid = ~np.isnan(osc)
+    assert np.array_equal(valid, ~np.isnan(gsc))
+    T, Hq = q.shape[0], q.shape[1]
+    qa = np.abs(parity._widen(qn)).reshape(T * Hq, 128)
+    boff = parity.block_offsets(cu.numpy(), B)
+    s_of = parity.seq_of_tokens(cu.numpy(), rows // Hq)
+    g_of = (rows % Hq) // (Hq // 2)
+    for j in range(nmax):
+        m = valid[:, j]
+        if not m.any():
+            continue
+        a = kabs[np.array(boff)[s_of[m]] + j, g_of[m]]
+        tau = parity.TAU_SCALE * np.einsum("rd,rd->r", qa[m], a)
+        assert np.all(np.abs(gsc[m, j] - osc[m, j]) <= tau)
+
+
+def test_route_matches_cpu_inversion():
+    seqlens, hq, hkv, B, topk = (1500, 0, 700, 33), 8, 2, 64, 4
+    q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, offset=0.5, seed=11)
+    sel = binding.select(q, k, cu, B, topk)
+    counts, offsets, entries = binding.route(sel, cu, B, hkv)
+    sel_h = sel.cpu().numpy()
+    T = q.shape[0]
+    G = hq // hkv
+    cun = cu.numpy()
+    boff = parity.block_offsets(cun, B)
+    nb = oracle.num_blocks(cun, B)
+    bins = [[] for _ in range(hkv * nb)]
+    for t in range(T):
+        s = int(parity.seq_of_tokens(cun, t))
+        c = (t - cun[s]) // B
+        for h in range(hq):
+            g, hl = h // G, h % G
+            r = g * T * G + t * G + hl
+            for x in range(min(topk - 1, c)):
+                j = int(sel_h[t, h, x])
+                bins[g * nb + boff[s] + j].append(r * (topk - 1) + x)
+    exp_counts = np.array([len(b) for b in bins])
+    exp_off = np.concatenate([[0], np.cumsum(exp_counts)])
+    exp_entries = np.array([e for b in bins for e in b], dtype=np.int64)
+    assert np.array_equal(counts.cpu().numpy(), exp_counts)
+    assert np.array_equal(offsets.cpu().numpy(), exp_off)
+    assert np.array_equal(entries.cpu().numpy().astype(np.int64) & 0xffffffff, exp_entries)
+
+
+def test_deterministic():
+    q, k, v, cu = make((1500, 800), 8, 2, torch.bfloat16, 128, offset=0.5, seed=13)
+    o1, l1 = binding.forward(q, k, v, cu, 128, 4)
+    o2, l2 = binding.forward(q, k, v, cu, 128, 4)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_gqa_equals_mha_with_repeated_kv():
+    q, k, v, cu = make((900, 300), 8, 2, torch.bfloat16, 64, offset=0.5, seed=17)
+    o1, l1 = binding.forward(q, k, v, cu, 64, 3)
+    o2, l2 = binding.forward(q, k.repeat_interleave(4, dim=1).contiguous(),
+                             v.repeat_interleave(4, dim=1).contiguous(), cu, 64, 3)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_varlen_equals_separate_calls():
+    seqlens = (700, 0, 1200, 65)
+    q, k, v, cu = make(seqlens, 4, 2, torch.bfloat16, 128, offset=0.5, seed=19)
+    o, l = binding.forward(q, k, v, cu, 128, 3)
+    a = 0
+    for L in seqlens:
+        if L == 0:
+            continue
+        cs = torch.tensor([0, L], dtype=torch.int32)
+        os_, ls = binding.forward(q[a:a + L].contiguous(), k[a:a + L].contiguous(),
+                                  v[a:a + L].contiguous(), cs, 128, 3)
+        assert torch.equal(os_, o[a:a + L]) and torch.equal(ls, l[:, a:a + L])
+        a += L
+
+
+def test_strided_inputs():
+    """q, k, v as column slices of one packed projection (token stride > H*D)."""
+    T, hq, hkv = 1100, 4, 2
+    q, k, v, cu = make((T,), hq, hkv, torch.bfloat16, 128, offset=0.5, seed=23)
+    packed = torch.cat([q, k, v], dim=1)
+    qs, ks, vs = packed[:, :hq], packed[:, hq:hq + hkv], packed[:, hq + hkv:]
+    o1, l1 = binding.forward(q, k, v, cu, 128, 3)
+    o2, l2 = binding.forward(qs, ks, vs, cu, 128, 3)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_workspace_chunking_is_invisible(monkeypatch):
+    """A small workspace cap splits the attention into kv-head chunks; the
+    result must not change."""
+    q, k, v, cu = make((2000, 900), 8, 4, torch.bfloat16, 128, offset=0.5, seed=29)
+    o1, l1 = binding.forward(q, k, v, cu, 128, 4)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("MOBA_WORKSPACE_LIMIT_BYTES", str(40 << 20))
+    o2, l2 = binding.forward(q, k, v, cu, 128, 4)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("MOBA_WORKSPACE_LIMIT_BYTES", str(1 << 20))
+    with pytest.raises(binding.MobaError) as ei:
+        binding.forward(q, k, v, cu, 128, 4)
+    assert ei.value.name == "MOBA_ERR_NO_MEMORY"
+    monkeypatch.delenv("MOBA_WORKSPACE_LIMIT_BYTES")
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_device_cu_seqlens():
+    q, k, v, cu = make((500, 300), 4, 2, torch.bfloat16, 64, seed=31)
+    o1, l1 = binding.forward(q, k, v, cu, 64, 3)
+    o2, l2 = binding.forward(q, k, v, cu.to(DEV), 64, 3)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_empty_batch():
+    q = torch.empty((0, 4, 128), dtype=torch.bfloat16, device=DEV)
+    k = torch.empty((0, 2, 128), dtype=torch.bfloat16, device=DEV)
+    o, l = binding.forward(q, k, k, torch.tensor([0, 0], dtype=torch.int32), 64, 3)
+    assert o.shape == (0, 4, 128) and l.shape == (4, 0)
