@@ -1,0 +1,234 @@
+"""Benchmark of the MoBA causal prefill forward on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--dense-steps N] [--no-cpu]
+
+One step = one moba_forward call over the whole workload (pool, gate, route,
+history and current-block attention, merge), inputs resident in HBM.  The
+default workload is the 1M-token prefill (32 query heads, 8 kv-heads, head
+dim 128, bf16, block 4096, top-12).  Prints one JSON line:
+  value          attended TFLOP/s of the whole forward (4*D per attended
+                 query-key pair; the causal triangle of the current block plus
+                 B keys per selected history block)
+  ms_per_step    forward latency
+  config         workload, bf16-peak fraction, dense latency and speedup
+  roofline       the history-attention kernel (the dominant one): algorithmic
+                 FLOPs per launch / its mean launch time from HIP events on
+                 the library's stream, against the 2516.6 TFLOP/s bf16 peak
+  cpu_baseline   the fp64 oracle on a fixed sample of rows, host cores
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+from paper_2502_13189_amd import binding, inputs  # noqa: E402
+
+BF16_PEAK_TFLOPS = 2516.6   # 256 CUs x 4096 bf16 FLOP/clk x 2.4 GHz (dense)
+HBM_PEAK_GBS = 8000.0
+
+
+def attended_keys(seqlens, B, topk):
+    """(current-block keys, history keys, history selections) per query head."""
+    cur = hist = sel = 0
+    for L in seqlens:
+        n = (L + B - 1) // B
+        for c in range(n):
+            m = min(L, (c + 1) * B) - c * B
+            cur += m * (m + 1) // 2
+            h = min(topk - 1, c)
+            hist += m * B * h
+            sel += m * h
+    return cur, hist, sel
+
+
+def dense_keys(seqlens):
+    return sum(L * (L + 1) // 2 for L in seqlens)
+
+
+def time_steps(fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / max(steps, 1)
+
+
+def cpu_baseline(w, q, k, v, cu, n_rows, seed=7):
+    """The oracle on n_rows seeded rows of the workload: pool over all keys,
+    gate and attention for the sampled rows.  Returns a dict."""
+    from oracle import oracle
+
+    cores = len(os.sched_getaffinity(0))
+    oracle.set_threads(cores)
+    T, Hq = q.shape[0], q.shape[1]
+    rng = np.random.default_rng(seed)
+    rows = np.sort(rng.choice(T * Hq, size=n_rows, replace=False)).astype(np.int64)
+    t_copy = time.perf_counter()
+    rows_t = torch.as_tensor(rows, device=q.device)
+    kn, vn = inputs.to_oracle(k), inputs.to_oracle(v)
+    qn = inputs.to_oracle(q)
+    t_copy = time.perf_counter() - t_copy
+    cun = cu.numpy()
+    t0 = time.perf_counter()
+    kbar = oracle.pool(kn, cun, w.block_size)
+    t1 = time.perf_counter()
+    sel = oracle.select(qn, kbar, cun, w.block_size, w.topk, rows=rows)
+    _, _ = oracle.attend(qn, kn, vn, cun, w.block_size, sel, rows=rows)
+    t2 = time.perf_counter()
+    # attended keys of the sampled rows
+    cum = np.asarray(cun, np.int64)
+    t = rows // Hq
+    s = np.searchsorted(cum, t, side="right") - 1
+    tau = t - cum[s]
+    c = tau // w.block_size
+    keys = (tau - c * w.block_size + 1) + w.block_size * np.minimum(w.topk - 1, c)
+    flop = 4.0 * w.d * float(keys.sum())
+    del rows_t
+    return {
+        "value": flop / (t2 - t1) / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.threads(),
+        "kind": "oracle",
+        "sample": ("fp64 oracle gate + attention for %d seeded rows (t*Hq+h) of the %s workload "
+                   "(%.3g attended FLOP) in %.1f s; its block mean-pool over all keys took %.1f s "
+                   "and is not in the rate; host copy %.1f s" %
+                   (n_rows, w.name, flop, t2 - t1, t1 - t0, t_copy)),
+        "cpu_model": _cpu_model(),
+    }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=inputs.HEADLINE, choices=sorted(inputs.WORKLOADS))
+    ap.add_argument("--dense-steps", type=int, default=1)
+    ap.add_argument("--cpu-rows", type=int, default=5000)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    w = inputs.WORKLOADS[args.workload]
+    binding.load()
+    dev = torch.device("cuda:0")
+    print("[bench] generating %s" % w.name, file=sys.stderr, flush=True)
+    q, k, v, cu = inputs.make_workload(w, device=dev)
+    torch.cuda.synchronize()
+    out = torch.empty_like(q)
+    lse = torch.empty((w.hq, q.shape[0]), dtype=torch.float32, device=dev)
+
+    def step():
+        binding.forward(q, k, v, cu, w.block_size, w.topk, out=out, lse=lse)
+
+    print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    binding.profile_read()
+    binding.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    binding.profile_enable(False)
+    phases = binding.profile_read()
+
+    cur, hist, nsel = attended_keys(w.seqlens, w.block_size, w.topk)
+    flop = 4.0 * w.d * w.hq * (cur + hist)
+    tflops = flop / (ms * 1e-3) / 1e12
+    hist_flop_step = 4.0 * w.d * w.hq * hist
+    hl, hms = phases.get("attn_hist", (0, 0.0))
+    launches_per_step = hl / max(args.steps, 1)
+    achieved = (hist_flop_step / launches_per_step) / (hms / hl * 1e-3) / 1e12 if hl else 0.0
+
+    dense_ms = None
+    if args.dense_steps > 0:
+        print("[bench] dense x%d" % args.dense_steps, file=sys.stderr, flush=True)
+        dout = torch.empty_like(q)
+        dlse = torch.empty_like(lse)
+        dense_ms = time_steps(lambda: binding.dense_forward(q, k, v, cu, out=dout, lse=dlse),
+                              args.dense_steps, 1)
+        del dout, dlse
+    dflop = 4.0 * w.d * w.hq * dense_keys(w.seqlens)
+
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] oracle baseline on %d rows" % args.cpu_rows, file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, q, k, v, cu, args.cpu_rows)
+
+    res = {
+        "metric": "MoBA prefill ms + attended TFLOP/s (% bf16 MFMA peak) at 1M ctx; speedup vs dense",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "seqlens": list(w.seqlens),
+            "q_heads": w.hq, "kv_heads": w.hkv, "head_dim": w.d,
+            "block_size": w.block_size, "topk": w.topk,
+            "attended_flop": flop,
+            "pct_bf16_peak": round(100.0 * tflops / BF16_PEAK_TFLOPS, 2),
+            "dense_ms": None if dense_ms is None else round(dense_ms, 2),
+            "dense_flop": dflop,
+            "dense_tflops": None if dense_ms is None else round(dflop / (dense_ms * 1e-3) / 1e12, 2),
+            "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 3),
+            "phases_ms_per_step": {n: round(t / args.steps, 3) for n, (c, t) in phases.items()},
+        },
+        "roofline": {
+            "kernel": "attn_mfma_kernel<history> (history-block attention)",
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+            "flop_per_launch": hist_flop_step / max(launches_per_step, 1),
+            "launches_per_step": launches_per_step,
+            "mean_launch_ms": round(hms / hl, 3) if hl else None,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
