@@ -5,15 +5,20 @@
 //
 // Work-group = 4 waves = 128 query rows; wave w owns rows 32w..32w+31, one
 // query per lane column.  Keys are consumed in tiles of 64 through a
-// double-buffered LDS stage (K as 64 rows x 256 B, V^T as 128 rows x 128 B,
-// 16-byte chunks XOR-swizzled by row so that the MFMA operand reads of eight
-// consecutive rows hit distinct banks).
+// double-buffered LDS stage: K as 64 rows of 256 B and V^T as 128 rows of
+// 128 B, each row padded by 16 B so that the MFMA operand reads (eight lanes
+// on eight consecutive rows at one column) fall on distinct banks, and every
+// read address is a per-lane base plus an immediate offset.
 //
 // Per key tile and wave, on v_mfma_f32_32x32x16_bf16:
 //   S^T (keys x queries) = K_tile . Q^T      2 x 8 MFMAs, K from LDS, Q^T in registers
 //   online softmax in fp32 on S^T: every lane holds one query and 32 of the
 //   tile's 64 keys, so the row max needs one exchange with the partner lane
-//   (lane ^ 32) and the row sum is kept per lane and combined at the end
+//   (lane ^ 32) and the row sum is kept per lane and combined at the end.
+//   The running max is only raised when a tile's max exceeds it by more than
+//   2^8 (in exp2 units): the weights then stay below 2^8, and the accumulator
+//   rescale, a multiply of all 64 accumulators, is skipped on most tiles.
+//   The row sum adds the fp32 weights, so lse is as accurate as fp32 allows.
 //   O^T (dims x queries) += V^T_tile . P^T  4 x 4 MFMAs, P^T straight from the
 //   softmax registers (converted to bf16), V^T from LDS
 // The accumulator layout of a 32x32 MFMA gives lane l the column l % 32 and
@@ -39,20 +44,28 @@ enum { kHist = 0, kCur = 1, kDense = 2 };
 
 constexpr int kChunksK = kKeyTile * kHeadDim / 8;  // 16-byte chunks per K tile (1024)
 constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // per V^T tile (1024)
-constexpr int kStageChunks = kChunksK + kChunksV;
+constexpr int kRowK = kHeadDim / 8 + 1;            // LDS K row: 16 chunks + 1 pad
+constexpr int kRowV = kKeyTile / 8 + 1;            // LDS V^T row: 8 chunks + 1 pad
+constexpr int kStageK = kKeyTile * kRowK;          // chunks of one K stage
+constexpr int kStageChunks = kStageK + kHeadDim * kRowV;
+constexpr float kRescaleSlack = 8.0f;              // exp2 units
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to a packed bf16 pair, round-to-nearest-even.
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  __hip_bfloat16 x = __float2bfloat16(a), y = __float2bfloat16(b);
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
+
 
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
 
 // Global -> registers: this thread's four 16-byte chunks of K tile i (64 keys
-// x 256 B, rows past the sequence end read as zeros) and of the packed V^T
-// tile i (contiguous 16 KiB).
+// x 256 B) and of the packed V^T tile i (contiguous 16 KiB).
 __device__ __forceinline__ void load_tile(int i, int tid, const __hip_bfloat16* kbase, int64_t k_st,
                                           int64_t tok0, int64_t seq_end, const u32x4* vtbase,
                                           u32x4 (&kreg)[4], u32x4 (&vreg)[4]) {
@@ -60,24 +73,22 @@ __device__ __forceinline__ void load_tile(int i, int tid, const __hip_bfloat16* 
   for (int x = 0; x < 4; x++) {
     const int c = tid + 256 * x;
     const int r = c >> 4, col = c & 15;
-    const int64_t u = tok0 + (int64_t)i * kKeyTile + r;
-    kreg[x] = u < seq_end ? *reinterpret_cast<const u32x4*>(kbase + u * k_st + col * 8)
-                          : u32x4{0u, 0u, 0u, 0u};
+    // rows past the sequence end repeat its last key; they are always masked
+    const int64_t u = min(tok0 + (int64_t)i * kKeyTile + r, seq_end - 1);
+    kreg[x] = *reinterpret_cast<const u32x4*>(kbase + u * k_st + col * 8);
     vreg[x] = vtbase[(int64_t)i * kChunksV + c];
   }
 }
 
-// Registers -> one LDS stage, chunk index XOR (row & 7).
+// Registers -> one LDS stage (padded rows).
 __device__ __forceinline__ void store_tile(u32x4* kl, int tid, const u32x4 (&kreg)[4],
                                            const u32x4 (&vreg)[4]) {
-  u32x4* vl = kl + kChunksK;
+  u32x4* vl = kl + kStageK;
 #pragma unroll
   for (int x = 0; x < 4; x++) {
     const int c = tid + 256 * x;
-    const int kr = c >> 4, kc = c & 15;
-    kl[kr * 16 + (kc ^ (kr & 7))] = kreg[x];
-    const int vr = c >> 3, vc = c & 7;
-    vl[vr * 8 + (vc ^ (vr & 7))] = vreg[x];
+    kl[(c >> 4) * kRowK + (c & 15)] = kreg[x];
+    vl[(c >> 3) * kRowV + (c & 7)] = vreg[x];
   }
 }
 
@@ -90,7 +101,7 @@ struct RowInfo {
 
 template <int MODE>
 __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p) {
-  __shared__ u32x4 lds[2 * kStageChunks];  // 64 KiB
+  __shared__ u32x4 lds[2 * kStageChunks];  // 70 KiB
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
@@ -180,13 +191,16 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
 
   load_tile(i0, tid, kbase, kst, tok0, seq_end, vtbase, kreg, vreg);
   store_tile(lds, tid, kreg, vreg);
+  // Let every load of the prologue (Q included) land here: otherwise the
+  // loop would carry waits on Q that, in steady state, stall on the prefetch.
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int i = i0; i < i1; i++) {
     const int stage = (i - i0) & 1;
     if (i + 1 < i1) load_tile(i + 1, tid, kbase, kst, tok0, seq_end, vtbase, kreg, vreg);
-    const u32x4* kl = lds + stage * kStageChunks;
-    const u32x4* vl = kl + kChunksK;
+    const u32x4* kl = lds + stage * kStageChunks + qc * kRowK + hh;
+    const u32x4* vl = lds + stage * kStageChunks + kStageK + qc * kRowV + hh;
 
     // S^T = K . Q^T
     f32x16 sacc[2];
@@ -198,8 +212,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     for (int kk = 0; kk < 8; kk++) {
 #pragma unroll
       for (int th = 0; th < 2; th++) {
-        const int kr = 32 * th + qc;
-        const bf16x8 ka = as_bf16x8(kl[kr * 16 + ((2 * kk + hh) ^ (kr & 7))]);
+        const bf16x8 ka = as_bf16x8(kl[32 * th * kRowK + 2 * kk]);
         sacc[th] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], sacc[th], 0, 0, 0);
       }
     }
@@ -218,47 +231,42 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
         }
     }
 
-    // online softmax (log2 domain)
+    // online softmax (exp2 units), lazily rescaled
     float mx = -INFINITY;
 #pragma unroll
     for (int th = 0; th < 2; th++)
 #pragma unroll
       for (int r = 0; r < 16; r++) mx = fmaxf(mx, sacc[th][r]);
-    mx = fmaxf(mx, xor32(mx));
-    const float m_new = fmaxf(m_run, mx * c2);
-    const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float rs = 0.0f;
+    mx = fmaxf(mx, xor32(mx)) * c2;
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack) != 0) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
 #pragma unroll
-    for (int th = 0; th < 2; th++)
+      for (int dt = 0; dt < 4; dt++)
 #pragma unroll
-      for (int r = 0; r < 16; r++) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[th][r], c2, -m_use));
-        sacc[th][r] = pv;
-        rs += pv;
-      }
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) o[dt][r] *= alpha;
+        for (int r = 0; r < 16; r++) o[dt][r] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = m_run == -INFINITY ? 0.0f : m_run;
 
-    // O^T += V^T . P^T
+    // weights, row sums, P^T in bf16, O^T += V^T . P^T
 #pragma unroll
     for (int th = 0; th < 2; th++) {
 #pragma unroll
       for (int s2 = 0; s2 < 2; s2++) {
-        const u32x4 pu = {pack_bf16(sacc[th][8 * s2 + 0], sacc[th][8 * s2 + 1]),
-                          pack_bf16(sacc[th][8 * s2 + 2], sacc[th][8 * s2 + 3]),
-                          pack_bf16(sacc[th][8 * s2 + 4], sacc[th][8 * s2 + 5]),
-                          pack_bf16(sacc[th][8 * s2 + 6], sacc[th][8 * s2 + 7])};
-        const bf16x8 pb = as_bf16x8(pu);
-        const int vc = 4 * th + 2 * s2 + hh;
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[th][8 * s2 + 2 * e], c2, -m_use));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[th][8 * s2 + 2 * e + 1], c2, -m_use));
+          w[e] = pack_bf16(p0, p1);
+          l_run += p0 + p1;
+        }
+        const bf16x8 pb = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
 #pragma unroll
         for (int dt = 0; dt < 4; dt++) {
-          const int vr = 32 * dt + qc;
-          const bf16x8 va = as_bf16x8(vl[vr * 8 + (vc ^ (vr & 7))]);
+          const bf16x8 va = as_bf16x8(vl[32 * dt * kRowV + 4 * th + 2 * s2]);
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[dt], 0, 0, 0);
         }
       }
