@@ -1,7 +1,8 @@
 // fp32 attention on the vector ALUs, for fp32 inputs (the tolerance of an
 // fp32 problem rules out bf16 matrix-core products).  Same tiles, rows and
-// outputs as the bf16 MFMA kernel: history-block tiles, causal current-block
-// tiles and dense causal tiles.
+// outputs as the bf16 MFMA kernel: history-block tiles (partials),
+// causal current-block tiles (merged with the partials into the output) and
+// dense causal tiles.
 //
 // Work-group = 128 threads, one query row per thread, with the query and the
 // output accumulator in registers (2 x 128 fp32).  Keys arrive in tiles of 32
@@ -140,17 +141,53 @@ __global__ __launch_bounds__(128, 1) void attn_f32_kernel(AttnArgs a, Problem p)
     }
     m_run = m_new;
   }
-  if (!valid) return;
-  const float inv = 1.0f / l_run;
-  const float lse = (m_run + __builtin_amdgcn_logf(l_run)) * 0.69314718055994531f;
-  float* orow;
-  if constexpr (MODE == kDense) {
-    orow = static_cast<float*>(a.out) + t * a.o_st + (int64_t)h * a.o_sh;
-    a.lse[(int64_t)h * p.T + t] = lse;
-  } else {
-    orow = (MODE == kHist ? a.o_part : a.o_cur) + dst * kHeadDim;
-    (MODE == kHist ? a.lse_part : a.lse_cur)[dst] = lse;
+  float inv = 1.0f / l_run;
+  float lse = (m_run + __builtin_amdgcn_logf(l_run)) * 0.69314718055994531f;
+  if constexpr (MODE == kHist) {
+    if (!valid) return;
+    float* orow = a.o_part + dst * kHeadDim;
+    a.lse_part[dst] = lse;
+#pragma unroll
+    for (int c = 0; c < kHeadDim / 4; c++)
+      reinterpret_cast<float4*>(orow)[c] =
+          make_float4(of[4 * c] * inv, of[4 * c + 1] * inv, of[4 * c + 2] * inv, of[4 * c + 3] * inv);
+    return;
   }
+  if constexpr (MODE == kCur) {
+    // merge with the row's history partials (same order and formula as the
+    // bf16 kernel: current block first, then slots ascending)
+    const int kh = p.topk - 1;
+    const int nh = min(kh, (int)((kbeg - sq.tok_start) / p.B));
+    if (nh > 0) {
+      const float* lp = a.lse_part + dst * kh;
+      const float* op = a.o_part + dst * kh * kHeadDim;
+      float M = lse;
+      for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
+      constexpr float kLog2e = 1.4426950408889634f;
+      const float wc = __builtin_amdgcn_exp2f((lse - M) * kLog2e);
+      float wsum = wc;
+#pragma unroll
+      for (int d = 0; d < kHeadDim; d++) of[d] *= wc * inv;
+      for (int x = 0; x < nh; x++) {
+        const float w = __builtin_amdgcn_exp2f((lp[x] - M) * kLog2e);
+        wsum += w;
+        const float4* ox = reinterpret_cast<const float4*>(op + x * kHeadDim);
+#pragma unroll
+        for (int c = 0; c < kHeadDim / 4; c++) {
+          const float4 v = ox[c];
+          of[4 * c] = fmaf(w, v.x, of[4 * c]);
+          of[4 * c + 1] = fmaf(w, v.y, of[4 * c + 1]);
+          of[4 * c + 2] = fmaf(w, v.z, of[4 * c + 2]);
+          of[4 * c + 3] = fmaf(w, v.w, of[4 * c + 3]);
+        }
+      }
+      inv = 1.0f / wsum;
+      lse = M + __builtin_amdgcn_logf(wsum) * 0.69314718055994531f;
+    }
+  }
+  if (!valid) return;
+  float* orow = static_cast<float*>(a.out) + t * a.o_st + (int64_t)h * a.o_sh;
+  a.lse[(int64_t)h * p.T + t] = lse;
 #pragma unroll
   for (int c = 0; c < kHeadDim / 4; c++)
     reinterpret_cast<float4*>(orow)[c] =

@@ -27,8 +27,9 @@
 // of a 16-key group, which is the order the V^T pack stores them in.
 //
 // Logits use scale 1/sqrt(D), folded with log2(e) into one FMA before exp2.
-// Outputs: history and current tiles write normalised fp32 partials and
-// their natural-log lse (merged later); dense tiles write the final output.
+// Outputs: history tiles write normalised fp32 partials and their natural-log
+// lse; current-block tiles merge those partials into the final output (the
+// log-sum-exp combine of Algorithm 1); dense tiles write the final output.
 #include "moba_internal.h"
 
 #include <math.h>
@@ -42,7 +43,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chun
 
 enum { kHist = 0, kCur = 1, kDense = 2 };
 
-constexpr int kChunksK = kKeyTile * kHeadDim / 8;  // 16-byte chunks per K tile (1024)
 constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // per V^T tile (1024)
 constexpr int kRowK = kHeadDim / 8 + 1;            // LDS K row: 16 chunks + 1 pad
 constexpr int kRowV = kKeyTile / 8 + 1;            // LDS V^T row: 8 chunks + 1 pad
@@ -280,22 +280,9 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
   const float l_tot = l_run + xor32(l_run);
   const float inv = 1.0f / l_tot;
   const float lse = (m_run + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f;
-  if (!ri.valid) return;
-  if constexpr (MODE == kDense) {
-    __hip_bfloat16* orow = static_cast<__hip_bfloat16*>(a.out) + ri.t * a.o_st + (int64_t)ri.h * a.o_sh;
-#pragma unroll
-    for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; r4++) {
-        const int d = 32 * dt + 8 * r4 + 4 * hh;
-        uint2 w;
-        w.x = pack_bf16(o[dt][4 * r4 + 0] * inv, o[dt][4 * r4 + 1] * inv);
-        w.y = pack_bf16(o[dt][4 * r4 + 2] * inv, o[dt][4 * r4 + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + d) = w;
-      }
-    if (hh == 0) a.lse[(int64_t)ri.h * p.T + ri.t] = lse;
-  } else {
-    float* orow = (MODE == kHist ? a.o_part : a.o_cur) + ri.dst * kHeadDim;
+  if constexpr (MODE == kHist) {
+    if (!ri.valid) return;
+    float* orow = a.o_part + ri.dst * kHeadDim;
 #pragma unroll
     for (int dt = 0; dt < 4; dt++)
 #pragma unroll
@@ -305,7 +292,60 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
             make_float4(o[dt][4 * r4 + 0] * inv, o[dt][4 * r4 + 1] * inv, o[dt][4 * r4 + 2] * inv,
                         o[dt][4 * r4 + 3] * inv);
       }
-    if (hh == 0) (MODE == kHist ? a.lse_part : a.lse_cur)[ri.dst] = lse;
+    if (hh == 0) a.lse_part[ri.dst] = lse;
+  } else {
+    float scale = inv, lse_out = lse;
+    if constexpr (MODE == kCur) {
+      // Merge with the row's history partials (all rows of a tile share the
+      // current block c, so the slot count is uniform):
+      //   lse = M + ln(sum_i e^{lse_i - M}),  out = sum_i e^{lse_i - lse} O_i
+      // summed in a fixed order: current block first, then slots ascending.
+      const int kh = p.topk - 1;
+      const int nh = min(kh, (int)((tmin - sq.tok_start) / p.B));
+      if (nh > 0) {
+        const float* lp = a.lse_part + ri.dst * kh;
+        const float* op = a.o_part + ri.dst * kh * kHeadDim;
+        float M = lse;
+        for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
+        constexpr float kLog2e = 1.4426950408889634f;
+        const float wc = __builtin_amdgcn_exp2f((lse - M) * kLog2e);
+        float wsum = wc;
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+          for (int r = 0; r < 16; r++) o[dt][r] *= wc * inv;
+        for (int x = 0; x < nh; x++) {
+          const float w = __builtin_amdgcn_exp2f((lp[x] - M) * kLog2e);
+          wsum += w;
+          const float* ox = op + x * kHeadDim;
+#pragma unroll
+          for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; r4++) {
+              const float4 v = *reinterpret_cast<const float4*>(ox + 32 * dt + 8 * r4 + 4 * hh);
+              o[dt][4 * r4 + 0] = fmaf(w, v.x, o[dt][4 * r4 + 0]);
+              o[dt][4 * r4 + 1] = fmaf(w, v.y, o[dt][4 * r4 + 1]);
+              o[dt][4 * r4 + 2] = fmaf(w, v.z, o[dt][4 * r4 + 2]);
+              o[dt][4 * r4 + 3] = fmaf(w, v.w, o[dt][4 * r4 + 3]);
+            }
+        }
+        scale = 1.0f / wsum;
+        lse_out = M + __builtin_amdgcn_logf(wsum) * 0.69314718055994531f;
+      }
+    }
+    if (!ri.valid) return;
+    __hip_bfloat16* orow = static_cast<__hip_bfloat16*>(a.out) + ri.t * a.o_st + (int64_t)ri.h * a.o_sh;
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; r4++) {
+        const int d = 32 * dt + 8 * r4 + 4 * hh;
+        uint2 w;
+        w.x = pack_bf16(o[dt][4 * r4 + 0] * scale, o[dt][4 * r4 + 1] * scale);
+        w.y = pack_bf16(o[dt][4 * r4 + 2] * scale, o[dt][4 * r4 + 3] * scale);
+        *reinterpret_cast<uint2*>(orow + d) = w;
+      }
+    if (hh == 0) a.lse[(int64_t)ri.h * p.T + ri.t] = lse_out;
   }
 }
 

@@ -4,8 +4,8 @@
 //
 // moba_forward enqueues, on the caller's stream:
 //   pool -> [bf16: V^T pack] -> gate -> route (count, column scan, bin scan,
-//   scatter) -> per chunk of kv-heads: history attention, current-block
-//   attention, merge.
+//   scatter) -> per chunk of kv-heads: history attention, then current-block
+//   attention with the merge of the history partials.
 // Only the last three depend on the chunk; their workspace (fp32 partials)
 // is what the workspace cap limits.
 #include "moba.h"
@@ -444,8 +444,6 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
     const int64_t rows = (int64_t)nch * TG;
     a->o_part = bp->take<float>(rows * kh * kHeadDim);
     a->lse_part = bp->take<float>(rows * kh);
-    a->o_cur = bp->take<float>(rows * kHeadDim);
-    a->lse_cur = bp->take<float>(rows);
     (void)base;
   };
   const size_t limit = workspace_limit();
@@ -504,11 +502,9 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
       MOBA_LAUNCH(in.bf16 ? launch_attn_hist_bf16(a, p, grid, stream)
                           : launch_attn_hist_f32(a, p, grid, stream));
     }
-    { Phase ph("attn_cur", stream);
+    { Phase ph("attn_cur_merge", stream);
       MOBA_LAUNCH(in.bf16 ? launch_attn_causal_bf16(false, a, p, stream)
                           : launch_attn_causal_f32(false, a, p, stream)); }
-    { Phase ph("merge", stream);
-      MOBA_LAUNCH(launch_merge(in.bf16, a, p, stream)); }
   }
   return MOBA_OK;
 }

@@ -87,9 +87,7 @@ struct AttnArgs {
   // causal tiles
   const CausalTile* tiles;
   int64_t ntiles;
-  float* o_cur;   // [rows_chunk, D]
-  float* lse_cur;
-  // dense output
+  // final output (current-block and dense tiles)
   void* out; int64_t o_st, o_sh;
   float* lse;
   int g0, g1;     // kv-heads of this chunk
@@ -102,8 +100,6 @@ hipError_t launch_attn_hist_bf16(const AttnArgs& a, const Problem& p, int64_t gr
 hipError_t launch_attn_causal_bf16(bool dense, const AttnArgs& a, const Problem& p, hipStream_t st);
 hipError_t launch_attn_hist_f32(const AttnArgs& a, const Problem& p, int64_t grid, hipStream_t st);
 hipError_t launch_attn_causal_f32(bool dense, const AttnArgs& a, const Problem& p, hipStream_t st);
-
-hipError_t launch_merge(bool bf16, const AttnArgs& a, const Problem& p, hipStream_t st);
 
 // ------------------------------------------------------------ device helpers
 // Largest s with key[s] <= x among sequences, skipping empty ones that share
