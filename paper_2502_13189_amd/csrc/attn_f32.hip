@@ -42,8 +42,8 @@ __global__ __launch_bounds__(128, 1) void attn_f32_kernel(AttnArgs a, Problem p)
     const int64_t bin = lo;
     g = (int)(bin / nb);
     const int b = (int)(bin % nb);
-    const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kTileRows;
-    const int n = (int)min((int64_t)kTileRows, a.bin_start[bin] + a.bin_count[bin] - e0);
+    const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kTileRowsF32;
+    const int n = (int)min((int64_t)kTileRowsF32, a.bin_start[bin] + a.bin_count[bin] - e0);
     s = find_seq(a.seqs, p.S, b, [](const SeqInfo& x) { return x.blk_off; });
     const SeqInfo sq = a.seqs[s];
     kbeg = (int64_t)sq.tok_start + (int64_t)(b - sq.blk_off) * p.B;

@@ -4,23 +4,31 @@
 // causal attention (Eq. 1), from one kernel template.
 //
 // Work-group = 4 waves = 128 query rows; wave w owns rows 32w..32w+31, one
-// query per lane column.  Keys are consumed in tiles of 64 through a
-// double-buffered LDS stage: K as 64 rows of 256 B and V^T as 128 rows of
-// 128 B, each row padded by 16 B so that the MFMA operand reads (eight lanes
-// on eight consecutive rows at one column) fall on distinct banks, and every
-// read address is a per-lane base plus an immediate offset.
+// query per lane column; two work-groups share a CU (two waves per SIMD).
+// Keys are consumed in tiles of 64.  LDS holds two K buffers (64 rows of
+// 256 B) and two V^T buffers (128 rows of 128 B), filled straight from global
+// memory by global_load_lds_dwordx4 (no registers, no LDS store
+// instructions).  Each such instruction writes 1 KiB contiguously (lane L to
+// 16-byte chunk L), so rows are not padded; instead 16-byte chunk c of row r
+// is stored at position c ^ (r & 7) (the permutation is applied to the
+// global addresses).  An operand read then has eight lanes on eight
+// consecutive rows hitting eight distinct chunk positions, i.e. all 32 banks.
+//
+// Iteration i computes S(i) = K(i) . Q^T, its softmax and O += V(i) . P(i)
+// while the DMA fills the other K and V^T buffers with tile i+1; one barrier
+// per tile.  The two waves of a SIMD belong to different work-groups, so one
+// wave's softmax overlaps the other's MFMAs.
 //
 // Per key tile and wave, on v_mfma_f32_32x32x16_bf16:
-//   S^T (keys x queries) = K_tile . Q^T      2 x 8 MFMAs, K from LDS, Q^T in registers
-//   online softmax in fp32 on S^T: every lane holds one query and 32 of the
+//   S^T (keys x queries) = K . Q^T         2 halves x 8 k-steps
+//   online softmax in fp32 on S^T: a lane holds one query and 32 of the
 //   tile's 64 keys, so the row max needs one exchange with the partner lane
 //   (lane ^ 32) and the row sum is kept per lane and combined at the end.
 //   The running max is only raised when a tile's max exceeds it by more than
-//   2^8 (in exp2 units): the weights then stay below 2^8, and the accumulator
-//   rescale, a multiply of all 64 accumulators, is skipped on most tiles.
-//   The row sum adds the fp32 weights, so lse is as accurate as fp32 allows.
-//   O^T (dims x queries) += V^T_tile . P^T  4 x 4 MFMAs, P^T straight from the
-//   softmax registers (converted to bf16), V^T from LDS
+//   2^8 (exp2 units): the weights then stay below 2^8 and the rescale of the
+//   accumulators is skipped on most tiles.
+//   O^T (dims x queries) += V^T . P^T      4 dim tiles x 4 k-steps, P^T
+//   straight from the softmax registers (packed to bf16).
 // The accumulator layout of a 32x32 MFMA gives lane l the column l % 32 and
 // rows 8*(i/4) + 4*(l/32) + i%4 for its 16 values i; so the 8 keys a lane
 // feeds into one k=16 step are keys {0-3, 8-11} (+4 for the upper half-wave)
@@ -38,22 +46,25 @@ namespace moba {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
 
 enum { kHist = 0, kCur = 1, kDense = 2 };
 
-constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // per V^T tile (1024)
-constexpr int kRowK = kHeadDim / 8 + 1;            // LDS K row: 16 chunks + 1 pad
-constexpr int kRowV = kKeyTile / 8 + 1;            // LDS V^T row: 8 chunks + 1 pad
-constexpr int kStageK = kKeyTile * kRowK;          // chunks of one K stage
-constexpr int kStageChunks = kStageK + kHeadDim * kRowV;
+constexpr int kRows = kTileRowsMfma;               // query rows per work-group (128)
+constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // 16-byte chunks per V^T tile (1024)
+constexpr int kRowK = kHeadDim / 8;                // LDS K row: 16 chunks
+constexpr int kRowV = kKeyTile / 8;                // LDS V^T row: 8 chunks
+constexpr int kBufK = kKeyTile * kRowK;            // 1024 chunks
+constexpr int kBufV = kHeadDim * kRowV;            // 1024 chunks
+constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 64 KiB
 constexpr float kRescaleSlack = 8.0f;              // exp2 units
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // Two fp32 values to a packed bf16 pair, round-to-nearest-even.
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
@@ -61,56 +72,156 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
-
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
 
-// Global -> registers: this thread's four 16-byte chunks of K tile i (64 keys
-// x 256 B) and of the packed V^T tile i (contiguous 16 KiB).
-__device__ __forceinline__ void load_tile(int i, int tid, const __hip_bfloat16* kbase, int64_t k_st,
-                                          int64_t tok0, int64_t seq_end, const u32x4* vtbase,
-                                          u32x4 (&kreg)[4], u32x4 (&vreg)[4]) {
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Global sources of this thread's lane in the LDS DMA of a tile.  Wave w
+// writes chunks 256w + 64x + L (x = 0..3, L = lane) of each buffer.
+//   K: chunk p is row p/16 at position p%16, holding logical chunk
+//      (p%16) ^ (row & 7); for x = 0, 2 and x = 1, 3 the logical chunk is
+//      the same, and the rows differ by 8.
+//   V^T: chunk p is row p/8 at position p%8, logical chunk (p%8) ^ (row & 7),
+//      the same for all x; rows differ by 8 per x (64 chunks).
+struct Dma {
+  const __hip_bfloat16* kp[2];     // tile-0 source for x = 0 and x = 1
+  const __hip_bfloat16* klast[2];  // the sequence's last key, same logical chunk
+  int krow[2];                     // tile row for x = 0 and x = 1
+  int64_t k_row;                   // elements between key rows
+  int64_t len;                     // sequence length
+  const u32x4* vp;                 // tile-0 source chunk for x = 0
+  int dst;                         // this wave's first chunk: 256 w
+};
+
+__device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
+  const int64_t base = (int64_t)i * kKeyTile;
+  const bool tail = base + kKeyTile > D.len;  // uniform
 #pragma unroll
   for (int x = 0; x < 4; x++) {
-    const int c = tid + 256 * x;
-    const int r = c >> 4, col = c & 15;
+    const int row = D.krow[x & 1] + 8 * (x >> 1);
+    const __hip_bfloat16* src = D.kp[x & 1] + (base + 8 * (x >> 1)) * D.k_row;
     // rows past the sequence end repeat its last key; they are always masked
-    const int64_t u = min(tok0 + (int64_t)i * kKeyTile + r, seq_end - 1);
-    kreg[x] = *reinterpret_cast<const u32x4*>(kbase + u * k_st + col * 8);
-    vreg[x] = vtbase[(int64_t)i * kChunksV + c];
+    if (tail && base + row >= D.len) src = D.klast[x & 1];
+    __builtin_amdgcn_global_load_lds(src, buf + D.dst + 64 * x, 16, 0, 0);
   }
 }
 
-// Registers -> one LDS stage (padded rows).
-__device__ __forceinline__ void store_tile(u32x4* kl, int tid, const u32x4 (&kreg)[4],
-                                           const u32x4 (&vreg)[4]) {
-  u32x4* vl = kl + kStageK;
+__device__ __forceinline__ void dma_v(const Dma& D, int i, u32x4* buf) {
 #pragma unroll
-  for (int x = 0; x < 4; x++) {
-    const int c = tid + 256 * x;
-    kl[(c >> 4) * kRowK + (c & 15)] = kreg[x];
-    vl[(c >> 3) * kRowV + (c & 7)] = vreg[x];
-  }
+  for (int x = 0; x < 4; x++)
+    __builtin_amdgcn_global_load_lds(D.vp + (int64_t)i * kChunksV + 64 * x, buf + D.dst + 64 * x,
+                                     16, 0, 0);
+}
+
+// Wait for this wave's LDS DMA (and everything else) before a barrier.
+__device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Lane read offsets (chunks) into a K and a V^T buffer.  For the lane's row
+// r = 32*half + qc the logical chunk c sits at r*row + (c ^ (qc & 7)).
+//   K, chunk 2kk + hh:  kq[kk & 3] + 8 * (kk >> 2) + 512 * th
+//   V^T, chunk 2st + hh: vq[st] + 256 * dt
+struct ReadOff {
+  int kq[4];
+  int vq[4];
+};
+
+// S^T: 16 MFMAs from the K buffer at kb.
+__device__ __forceinline__ void qk(f32x16 (&s)[2], const u32x4* kb, const ReadOff& ro,
+                                   const bf16x8 (&qf)[8]) {
+#pragma unroll
+  for (int th = 0; th < 2; th++)
+#pragma unroll
+    for (int r = 0; r < 16; r++) s[th][r] = 0.0f;
+#pragma unroll
+  for (int kk = 0; kk < 8; kk++)
+#pragma unroll
+    for (int th = 0; th < 2; th++)
+      s[th] = mfma(as_bf16x8(kb[ro.kq[kk & 3] + 8 * (kk >> 2) + 32 * kRowK * th]), qf[kk], s[th]);
+}
+
+// O^T += V^T . P^T: 16 MFMAs from the V^T buffer at vb.
+__device__ __forceinline__ void pv(f32x16 (&o)[4], const u32x4* vb, const ReadOff& ro,
+                                   const bf16x8 (&pb)[4]) {
+#pragma unroll
+  for (int st = 0; st < 4; st++)
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+      o[dt] = mfma(as_bf16x8(vb[ro.vq[st] + 32 * kRowV * dt]), pb[st], o[dt]);
 }
 
 struct RowInfo {
   int64_t t;
   int h;
   bool valid;
-  int64_t dst;  // partial index (history / current) or unused (dense)
+  int64_t dst;  // partial index (history) or chunk-relative row (current block)
 };
+
+// Masking and online softmax of S(i); the weights leave as bf16 P^T operands
+// pb[2*th + s2] (keys 32*th + 16*s2 .. +15).
+// On edge tiles only keys k of the tile with lo <= k < hi are kept; lo and
+// hi come relative to this lane's key offset 4*hh, so each element compares
+// a compile-time constant with a lane value.
+__device__ __forceinline__ void mask_keys(f32x16 (&s)[2], int lo, int hi) {
+#pragma unroll
+  for (int th = 0; th < 2; th++)
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      const int k = 32 * th + 8 * (r >> 2) + (r & 3);
+      s[th][r] = (k >= lo && k < hi) ? s[th][r] : -INFINITY;
+    }
+}
+
+template <int MODE>
+__device__ __forceinline__ void softmax(f32x16 (&s)[2], float& m, float& l, f32x16 (&o)[4],
+                                        bf16x8 (&pb)[4], bool edge, int lo, int hi, float c2) {
+  if (edge) mask_keys(s, lo, hi);
+  float mx = -INFINITY;
+#pragma unroll
+  for (int th = 0; th < 2; th++)
+#pragma unroll
+    for (int r = 0; r < 16; r++) mx = fmaxf(mx, s[th][r]);
+  mx = fmaxf(mx, xor32(mx)) * c2;
+  if (__builtin_amdgcn_ballot_w64(mx > m + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(m, mx);
+    const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m - m_new);
+    l *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) o[dt][r] *= alpha;
+    m = m_new;
+  }
+  const float m_use = m == -INFINITY ? 0.0f : m;
+#pragma unroll
+  for (int th = 0; th < 2; th++)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; s2++) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[th][8 * s2 + 2 * e], c2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[th][8 * s2 + 2 * e + 1], c2, -m_use));
+        w[e] = pack_bf16(p0, p1);
+        l += p0 + p1;
+      }
+      pb[2 * th + s2] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+    }
+}
 
 template <int MODE>
 __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p) {
-  __shared__ u32x4 lds[2 * kStageChunks];  // 70 KiB
+  __shared__ u32x4 lds[kLdsChunks];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
-  const int rloc = wave * 32 + qc;  // this lane's query row within the tile
 
   // ------------------------------------------------------------ tile setup
   int g, s;
   int64_t kbeg, kend, tmin;
   RowInfo ri;
+  const int rloc = wave * 32 + qc;  // this lane's query row within the tile
   if constexpr (MODE == kHist) {
     const int64_t nb = p.nblk_total;
     const int64_t tbeg = a.bin_tile_start[a.g0 * nb];
@@ -129,23 +240,22 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     const int64_t bin = lo;
     g = (int)(bin / nb);
     const int b = (int)(bin % nb);
-    const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kTileRows;
-    const int n = (int)min((int64_t)kTileRows, a.bin_start[bin] + a.bin_count[bin] - e0);
+    const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kRows;
+    const int n = (int)min((int64_t)kRows, a.bin_start[bin] + a.bin_count[bin] - e0);
     s = find_seq(a.seqs, p.S, b, [](const SeqInfo& x) { return x.blk_off; });
     const SeqInfo sq = a.seqs[s];
     kbeg = (int64_t)sq.tok_start + (int64_t)(b - sq.blk_off) * p.B;
     kend = kbeg + p.B;
     tmin = kend;  // every key precedes every routed query
-    const uint32_t kh = (uint32_t)(p.topk - 1);
-    const uint64_t ev = a.entries[e0 + min(rloc, n - 1)];
-    const uint64_t gr = ev / kh;
+    const uint64_t kh = (uint64_t)(p.topk - 1);
     const uint64_t TG = (uint64_t)p.T * p.G;
-    const uint64_t rem = gr - (uint64_t)g * TG;
-    ri.t = (int64_t)(rem / p.G);
-    ri.h = g * p.G + (int)(rem % p.G);
+    const uint64_t ev = a.entries[e0 + min(rloc, n - 1)];
+    const uint64_t rem = ev / kh - (uint64_t)g * TG;
+    const bool ok = rem < TG;
+    ri.valid = rloc < n && ok;
+    ri.t = ok ? (int64_t)(rem / p.G) : kbeg;
+    ri.h = g * p.G + (ok ? (int)(rem % p.G) : 0);
     ri.dst = (int64_t)(ev - (uint64_t)a.g0 * TG * kh);
-    ri.valid = rloc < n && rem < TG;
-    if (!(rem < TG)) { ri.t = kbeg; ri.h = g * p.G; }
   } else {
     const CausalTile ct = a.tiles[blockIdx.x];
     g = a.g0 + blockIdx.y;
@@ -161,191 +271,167 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     ri.dst = (int64_t)(g - a.g0) * p.T * p.G + ri.t * p.G + (rr % p.G);
   }
   const SeqInfo sq = a.seqs[s];
-  const int64_t seq_end = (int64_t)sq.tok_start + sq.len;
+  const int64_t tok0 = sq.tok_start;
+  const int64_t seq_end = tok0 + sq.len;
 
-  // ---------------------------------------------------------- Q^T operand
-  const __hip_bfloat16* qbase = static_cast<const __hip_bfloat16*>(a.q);
-  const __hip_bfloat16* qrow = qbase + ri.t * a.q_st + (int64_t)ri.h * a.q_sh + 8 * hh;
+  // ---------------------------------------------------------- Q^T operands
   bf16x8 qf[8];
+  {
+    const __hip_bfloat16* qrow = static_cast<const __hip_bfloat16*>(a.q) + ri.t * a.q_st +
+                                 (int64_t)ri.h * a.q_sh + 8 * hh;
 #pragma unroll
-  for (int kk = 0; kk < 8; kk++) qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 16 * kk));
+    for (int kk = 0; kk < 8; kk++)
+      qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 16 * kk));
+  }
 
   // ------------------------------------------------------------ key tiles
-  const int64_t rb = kbeg - sq.tok_start, re = kend - sq.tok_start;
+  const int64_t rb = kbeg - tok0, re = kend - tok0;
   const int i0 = (int)(rb / kKeyTile), i1 = (int)((re + kKeyTile - 1) / kKeyTile);
-  const __hip_bfloat16* kbase = static_cast<const __hip_bfloat16*>(a.k) + (int64_t)g * a.k_sh;
-  const u32x4* vtbase = reinterpret_cast<const u32x4*>(
-      a.vt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) * (kKeyTile * kHeadDim));
-
-  const int64_t tok0 = sq.tok_start;
-  const int64_t kst = a.k_st;
-  u32x4 kreg[4], vreg[4];
-
+  Dma D;
+  {
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    D.dst = 256 * wv;
+    const __hip_bfloat16* kbase = static_cast<const __hip_bfloat16*>(a.k) + (int64_t)g * a.k_sh;
+#pragma unroll
+    for (int x = 0; x < 2; x++) {
+      const int p = 256 * wv + 64 * x + lane;
+      const int row = p >> 4;
+      const int lc = (p & 15) ^ (row & 7);
+      D.krow[x] = row;
+      D.kp[x] = kbase + (tok0 + row) * a.k_st + lc * 8;
+      D.klast[x] = kbase + (seq_end - 1) * a.k_st + lc * 8;
+    }
+    D.k_row = a.k_st;
+    D.len = sq.len;
+    const int vrow = (256 * wv + lane) >> 3;
+    const int vlc = (lane & 7) ^ (vrow & 7);
+    D.vp = reinterpret_cast<const u32x4*>(a.vt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) *
+                                                     (kKeyTile * kHeadDim)) + vrow * kRowV + vlc;
+  }
+  ReadOff ro;
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    ro.kq[j] = qc * kRowK + ((2 * j + hh) ^ (qc & 7));
+    ro.vq[j] = qc * kRowV + ((2 * j + hh) ^ (qc & 7));
+  }
   const float c2 = a.scale_log2;
-  float m_run = -INFINITY, l_run = 0.0f;
   f32x16 o[4];
+  float m = -INFINITY, l = 0.0f;
 #pragma unroll
   for (int dt = 0; dt < 4; dt++)
 #pragma unroll
     for (int r = 0; r < 16; r++) o[dt][r] = 0.0f;
 
-  load_tile(i0, tid, kbase, kst, tok0, seq_end, vtbase, kreg, vreg);
-  store_tile(lds, tid, kreg, vreg);
-  // Let every load of the prologue (Q included) land here: otherwise the
-  // loop would carry waits on Q that, in steady state, stall on the prefetch.
-  __builtin_amdgcn_s_waitcnt(0);
+  // tile i lives in K and V^T buffers (i - i0) % 2
+  dma_k(D, i0, lds);
+  dma_v(D, i0, lds + 2 * kBufK);
+  // Every prologue load (Q included) lands here, so the loop carries no
+  // waits on Q.
+  dma_wait();
   __syncthreads();
 
+  f32x16 sc[2];
+  bf16x8 pb[4];
   for (int i = i0; i < i1; i++) {
-    const int stage = (i - i0) & 1;
-    if (i + 1 < i1) load_tile(i + 1, tid, kbase, kst, tok0, seq_end, vtbase, kreg, vreg);
-    const u32x4* kl = lds + stage * kStageChunks + qc * kRowK + hh;
-    const u32x4* vl = lds + stage * kStageChunks + kStageK + qc * kRowV + hh;
-
-    // S^T = K . Q^T
-    f32x16 sacc[2];
-#pragma unroll
-    for (int th = 0; th < 2; th++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) sacc[th][r] = 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < 8; kk++) {
-#pragma unroll
-      for (int th = 0; th < 2; th++) {
-        const bf16x8 ka = as_bf16x8(kl[32 * th * kRowK + 2 * kk]);
-        sacc[th] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], sacc[th], 0, 0, 0);
-      }
+    const int cur = (i - i0) & 1;
+    u32x4* const kcur = lds + cur * kBufK;
+    u32x4* const vcur = lds + 2 * kBufK + cur * kBufV;
+    if (i + 1 < i1) {
+      dma_k(D, i + 1, lds + (cur ^ 1) * kBufK);
+      dma_v(D, i + 1, lds + 2 * kBufK + (cur ^ 1) * kBufV);
     }
-
-    // mask keys outside [kbeg, kend) and, on causal tiles, keys after the query
-    const int64_t u0 = (int64_t)sq.tok_start + (int64_t)i * kKeyTile;
-    const bool edge = u0 < kbeg || u0 + kKeyTile > kend || (MODE != kHist && u0 + kKeyTile - 1 > tmin);
+    qk(sc, kcur, ro, qf);
+    const int64_t u0 = tok0 + (int64_t)i * kKeyTile;
+    const bool edge =
+        u0 < kbeg || u0 + kKeyTile > kend || (MODE != kHist && u0 + kKeyTile - 1 > tmin);
+    int lo = 0, hi = kKeyTile;
     if (edge) {
-#pragma unroll
-      for (int th = 0; th < 2; th++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-          const int64_t u = u0 + 32 * th + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const bool ok = u >= kbeg && u < kend && (MODE == kHist || u <= ri.t);
-          sacc[th][r] = ok ? sacc[th][r] : -INFINITY;
-        }
+      lo = (int)max((int64_t)0, kbeg - u0) - 4 * hh;
+      const int64_t lim = min((int64_t)kKeyTile, kend - u0);
+      hi = (int)(MODE == kHist ? lim : min(lim, ri.t + 1 - u0)) - 4 * hh;
     }
-
-    // online softmax (exp2 units), lazily rescaled
-    float mx = -INFINITY;
-#pragma unroll
-    for (int th = 0; th < 2; th++)
-#pragma unroll
-      for (int r = 0; r < 16; r++) mx = fmaxf(mx, sacc[th][r]);
-    mx = fmaxf(mx, xor32(mx)) * c2;
-    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack) != 0) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-        for (int r = 0; r < 16; r++) o[dt][r] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = m_run == -INFINITY ? 0.0f : m_run;
-
-    // weights, row sums, P^T in bf16, O^T += V^T . P^T
-#pragma unroll
-    for (int th = 0; th < 2; th++) {
-#pragma unroll
-      for (int s2 = 0; s2 < 2; s2++) {
-        uint32_t w[4];
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[th][8 * s2 + 2 * e], c2, -m_use));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[th][8 * s2 + 2 * e + 1], c2, -m_use));
-          w[e] = pack_bf16(p0, p1);
-          l_run += p0 + p1;
-        }
-        const bf16x8 pb = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
-#pragma unroll
-        for (int dt = 0; dt < 4; dt++) {
-          const bf16x8 va = as_bf16x8(vl[32 * dt * kRowV + 4 * th + 2 * s2]);
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[dt], 0, 0, 0);
-        }
-      }
-    }
-
-    if (i + 1 < i1) store_tile(lds + (stage ^ 1) * kStageChunks, tid, kreg, vreg);
+    softmax<MODE>(sc, m, l, o, pb, edge, lo, hi, c2);
+    pv(o, vcur, ro, pb);
+    dma_wait();
     __syncthreads();
   }
 
   // -------------------------------------------------------------- epilogue
-  const float l_tot = l_run + xor32(l_run);
-  const float inv = 1.0f / l_tot;
-  const float lse = (m_run + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f;
-  if constexpr (MODE == kHist) {
-    if (!ri.valid) return;
-    float* orow = a.o_part + ri.dst * kHeadDim;
-#pragma unroll
-    for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; r4++) {
-        const int d = 32 * dt + 8 * r4 + 4 * hh;
-        *reinterpret_cast<float4*>(orow + d) =
-            make_float4(o[dt][4 * r4 + 0] * inv, o[dt][4 * r4 + 1] * inv, o[dt][4 * r4 + 2] * inv,
-                        o[dt][4 * r4 + 3] * inv);
-      }
-    if (hh == 0) a.lse_part[ri.dst] = lse;
-  } else {
-    float scale = inv, lse_out = lse;
-    if constexpr (MODE == kCur) {
-      // Merge with the row's history partials (all rows of a tile share the
-      // current block c, so the slot count is uniform):
-      //   lse = M + ln(sum_i e^{lse_i - M}),  out = sum_i e^{lse_i - lse} O_i
-      // summed in a fixed order: current block first, then slots ascending.
-      const int kh = p.topk - 1;
-      const int nh = min(kh, (int)((tmin - sq.tok_start) / p.B));
-      if (nh > 0) {
-        const float* lp = a.lse_part + ri.dst * kh;
-        const float* op = a.o_part + ri.dst * kh * kHeadDim;
-        float M = lse;
-        for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
-        constexpr float kLog2e = 1.4426950408889634f;
-        const float wc = __builtin_amdgcn_exp2f((lse - M) * kLog2e);
-        float wsum = wc;
+  {
+    const float l_tot = l + xor32(l);
+    const float inv = 1.0f / l_tot;
+    const float lse = (m + __builtin_amdgcn_logf(l_tot)) * kLn2;
+    f32x16 (&og)[4] = o;
+    const RowInfo& r = ri;
+    if constexpr (MODE == kHist) {
+      if (r.valid) {
+        float* orow = a.o_part + r.dst * kHeadDim;
 #pragma unroll
         for (int dt = 0; dt < 4; dt++)
 #pragma unroll
-          for (int r = 0; r < 16; r++) o[dt][r] *= wc * inv;
-        for (int x = 0; x < nh; x++) {
-          const float w = __builtin_amdgcn_exp2f((lp[x] - M) * kLog2e);
-          wsum += w;
-          const float* ox = op + x * kHeadDim;
+          for (int r4 = 0; r4 < 4; r4++) {
+            const int d = 32 * dt + 8 * r4 + 4 * hh;
+            *reinterpret_cast<float4*>(orow + d) =
+                make_float4(og[dt][4 * r4 + 0] * inv, og[dt][4 * r4 + 1] * inv,
+                            og[dt][4 * r4 + 2] * inv, og[dt][4 * r4 + 3] * inv);
+          }
+        if (hh == 0) a.lse_part[r.dst] = lse;
+      }
+    } else {
+      float scale = inv, lse_out = lse;
+      if constexpr (MODE == kCur) {
+        // Merge with the row's history partials (all rows of a tile share the
+        // current block c, so the slot count is uniform):
+        //   lse = M + ln(sum_i e^{lse_i - M}),  out = sum_i e^{lse_i - lse} O_i
+        // summed in a fixed order: current block first, then slots ascending.
+        const int kh = p.topk - 1;
+        const int nh = min(kh, (int)((tmin - tok0) / p.B));
+        if (nh > 0) {
+          const float* lp = a.lse_part + r.dst * kh;
+          const float* op = a.o_part + r.dst * kh * kHeadDim;
+          float M = lse;
+          for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
+          const float wc = __builtin_amdgcn_exp2f((lse - M) * kLog2e);
+          float wsum = wc;
 #pragma unroll
           for (int dt = 0; dt < 4; dt++)
 #pragma unroll
-            for (int r4 = 0; r4 < 4; r4++) {
-              const float4 v = *reinterpret_cast<const float4*>(ox + 32 * dt + 8 * r4 + 4 * hh);
-              o[dt][4 * r4 + 0] = fmaf(w, v.x, o[dt][4 * r4 + 0]);
-              o[dt][4 * r4 + 1] = fmaf(w, v.y, o[dt][4 * r4 + 1]);
-              o[dt][4 * r4 + 2] = fmaf(w, v.z, o[dt][4 * r4 + 2]);
-              o[dt][4 * r4 + 3] = fmaf(w, v.w, o[dt][4 * r4 + 3]);
-            }
+            for (int q = 0; q < 16; q++) og[dt][q] *= wc * inv;
+          for (int x = 0; x < nh; x++) {
+            const float w = __builtin_amdgcn_exp2f((lp[x] - M) * kLog2e);
+            wsum += w;
+            const float* ox = op + x * kHeadDim;
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+              for (int r4 = 0; r4 < 4; r4++) {
+                const float4 v = *reinterpret_cast<const float4*>(ox + 32 * dt + 8 * r4 + 4 * hh);
+                og[dt][4 * r4 + 0] = fmaf(w, v.x, og[dt][4 * r4 + 0]);
+                og[dt][4 * r4 + 1] = fmaf(w, v.y, og[dt][4 * r4 + 1]);
+                og[dt][4 * r4 + 2] = fmaf(w, v.z, og[dt][4 * r4 + 2]);
+                og[dt][4 * r4 + 3] = fmaf(w, v.w, og[dt][4 * r4 + 3]);
+              }
+          }
+          scale = 1.0f / wsum;
+          lse_out = M + __builtin_amdgcn_logf(wsum) * kLn2;
         }
-        scale = 1.0f / wsum;
-        lse_out = M + __builtin_amdgcn_logf(wsum) * 0.69314718055994531f;
+      }
+      if (r.valid) {
+        __hip_bfloat16* orow =
+            static_cast<__hip_bfloat16*>(a.out) + r.t * a.o_st + (int64_t)r.h * a.o_sh;
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; r4++) {
+            const int d = 32 * dt + 8 * r4 + 4 * hh;
+            uint2 w;
+            w.x = pack_bf16(og[dt][4 * r4 + 0] * scale, og[dt][4 * r4 + 1] * scale);
+            w.y = pack_bf16(og[dt][4 * r4 + 2] * scale, og[dt][4 * r4 + 3] * scale);
+            *reinterpret_cast<uint2*>(orow + d) = w;
+          }
+        if (hh == 0) a.lse[(int64_t)r.h * p.T + r.t] = lse_out;
       }
     }
-    if (!ri.valid) return;
-    __hip_bfloat16* orow = static_cast<__hip_bfloat16*>(a.out) + ri.t * a.o_st + (int64_t)ri.h * a.o_sh;
-#pragma unroll
-    for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; r4++) {
-        const int d = 32 * dt + 8 * r4 + 4 * hh;
-        uint2 w;
-        w.x = pack_bf16(o[dt][4 * r4 + 0] * scale, o[dt][4 * r4 + 1] * scale);
-        w.y = pack_bf16(o[dt][4 * r4 + 2] * scale, o[dt][4 * r4 + 3] * scale);
-        *reinterpret_cast<uint2*>(orow + d) = w;
-      }
-    if (hh == 0) a.lse[(int64_t)ri.h * p.T + ri.t] = lse_out;
   }
 }
 

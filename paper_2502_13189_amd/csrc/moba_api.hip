@@ -179,7 +179,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // B = 0 means "one block per sequence" (dense attention).
 void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk, TileMode mode,
-                Plan* pl) {
+                int tile_rows, Plan* pl) {
   Problem& p = pl->p;
   const int S = (int)cu.size() - 1;
   p.T = cu[S];
@@ -189,6 +189,7 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
   p.S = S;
   p.B = B;
   p.topk = topk;
+  p.tile_rows = tile_rows;
   p.gate_tw = std::max(1, 256 / p.G);
   p.route_rt = std::max(1, kRouteRows / p.G);
   pl->seqs.assign(S, SeqInfo{});
@@ -231,7 +232,7 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
 
   pl->tiles.clear();
   if (mode == kTilesNone) return;
-  const int tt = std::max(1, kTileRows / p.G);  // tokens per causal tile
+  const int tt = std::max(1, tile_rows / p.G);  // tokens per causal tile
   for (int s = 0; s < S; s++) {
     const int64_t L = (int64_t)cu[s + 1] - cu[s];
     const int64_t Bs = mode == kTilesCur ? B : std::max<int64_t>(L, 1);
@@ -289,13 +290,13 @@ moba_status ensure_workspace(DevCache* dc, size_t bytes) {
 // Rebuilt only when the key changes; the rebuild synchronizes the device
 // because kernels of earlier calls may still read the old tables.
 moba_status get_plan(DevCache* dc, const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk,
-                     TileMode mode, const Plan** out, const SeqInfo** d_seqs,
+                     TileMode mode, int tile_rows, const Plan** out, const SeqInfo** d_seqs,
                      const CausalTile** d_tiles) {
-  std::vector<int64_t> key = {Hq, Hkv, B, topk, mode, (int64_t)cu.size()};
+  std::vector<int64_t> key = {Hq, Hkv, B, topk, mode, tile_rows, (int64_t)cu.size()};
   key.insert(key.end(), cu.begin(), cu.end());
   if (key != dc->tab_key || !dc->tab) {
     Plan pl;
-    build_plan(cu, Hq, Hkv, B, topk, mode, &pl);
+    build_plan(cu, Hq, Hkv, B, topk, mode, tile_rows, &pl);
     const size_t sb = pl.seqs.size() * sizeof(SeqInfo);
     const size_t need = ((sb + kAlign - 1) / kAlign) * kAlign + pl.tiles.size() * sizeof(CausalTile) + kAlign;
     if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
@@ -369,11 +370,11 @@ moba_status check_inputs(const moba_tensor* q, const moba_tensor* k, const moba_
   if (k->shape[0] != in->T || v->shape[0] != in->T || out->shape[0] != in->T) return MOBA_ERR_SHAPE;
   if (v->shape[1] != in->Hkv || out->shape[1] != in->Hq) return MOBA_ERR_SHAPE;
   if (in->Hq % in->Hkv != 0) return MOBA_ERR_SHAPE;
-  if (in->Hq / in->Hkv > kTileRows) return MOBA_ERR_UNSUPPORTED;
+  if (in->Hq / in->Hkv > kMaxGroup) return MOBA_ERR_UNSUPPORTED;
   const int64_t lshape[2] = {in->Hq, in->T};
   if ((st = check_contig(lse, MOBA_F32, 2, lshape)) != MOBA_OK) return st;
   if ((st = check_cu_desc(cu)) != MOBA_OK) return st;
-  if (in->T >= (int64_t(1) << 31) - kTileRows) return MOBA_ERR_UNSUPPORTED;
+  if (in->T >= (int64_t(1) << 31) - kTileRowsMfma) return MOBA_ERR_UNSUPPORTED;
   in->bf16 = q->dtype == MOBA_BF16;
   return MOBA_OK;
 }
@@ -422,7 +423,8 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur, &pl, &d_seqs, &d_tiles)) !=
+  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur,
+                     in.bf16 ? kTileRowsMfma : kTileRowsF32, &pl, &d_seqs, &d_tiles)) !=
       MOBA_OK)
     return st;
   const Problem& p = pl->p;
@@ -497,7 +499,7 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
     a.g1 = std::min(p.Hkv, g0 + nch);
     const int64_t e_chunk = pl->hist_per_head * p.G * (a.g1 - a.g0);
     if (kh > 0 && e_chunk > 0) {
-      const int64_t grid = ceil_div(e_chunk, kTileRows) + (int64_t)(a.g1 - a.g0) * p.nblk_total;
+      const int64_t grid = ceil_div(e_chunk, p.tile_rows) + (int64_t)(a.g1 - a.g0) * p.nblk_total;
       Phase ph("attn_hist", stream);
       MOBA_LAUNCH(in.bf16 ? launch_attn_hist_bf16(a, p, grid, stream)
                           : launch_attn_hist_f32(a, p, grid, stream));
@@ -524,7 +526,8 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, 0, 1, kTilesDense, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
+  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, 0, 1, kTilesDense,
+                         in.bf16 ? kTileRowsMfma : kTileRowsF32, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
   Bump sz(nullptr);
@@ -575,7 +578,8 @@ moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hkv, Hkv, block_size, 1, kTilesNone, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
+  if ((st = get_plan(dc, cu, Hkv, Hkv, block_size, 1, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+                      &d_tiles)) != MOBA_OK)
     return st;
   Phase ph("pool", stream);
   MOBA_LAUNCH(launch_pool(vk.data, k->dtype == MOBA_BF16, vk.st, vk.sh, d_seqs, pl->p,
@@ -596,7 +600,7 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
   const int64_t T = q->shape[0];
   const int Hq = (int)q->shape[1], Hkv = (int)k->shape[1];
   if (k->shape[0] != T || Hq % Hkv != 0) return MOBA_ERR_SHAPE;
-  if (Hq / Hkv > kTileRows) return MOBA_ERR_UNSUPPORTED;
+  if (Hq / Hkv > kMaxGroup) return MOBA_ERR_UNSUPPORTED;
   if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
   if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (topk < 1) return MOBA_ERR_TOPK;
@@ -624,7 +628,8 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hq, Hkv, block_size, topk, kTilesNone, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
+  if ((st = get_plan(dc, cu, Hq, Hkv, block_size, topk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+                      &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
   Bump sz(nullptr);
@@ -657,7 +662,7 @@ moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, in
   moba_status st;
   if ((st = check_contig(sel, MOBA_I32, 3, ss)) != MOBA_OK) return st;
   if (num_kv_heads < 1 || Hq < 1 || Hq % num_kv_heads != 0) return MOBA_ERR_SHAPE;
-  if (Hq / num_kv_heads > kTileRows) return MOBA_ERR_UNSUPPORTED;
+  if (Hq / num_kv_heads > kMaxGroup) return MOBA_ERR_UNSUPPORTED;
   if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (topk < 1) return MOBA_ERR_TOPK;
   if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
@@ -683,8 +688,8 @@ moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, in
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hq, num_kv_heads, block_size, topk, kTilesNone, &pl, &d_seqs,
-                     &d_tiles)) != MOBA_OK)
+  if ((st = get_plan(dc, cu, Hq, num_kv_heads, block_size, topk, kTilesNone, kTileRowsMfma, &pl,
+                     &d_seqs, &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
   const int64_t es[1] = {p.hist_entries};

@@ -9,7 +9,9 @@ namespace moba {
 
 constexpr int kHeadDim = 128;     // D; every kernel is specialised for it
 constexpr int kKeyTile = 64;      // keys per LDS tile in the attention kernels
-constexpr int kTileRows = 128;    // query rows per attention work-group
+constexpr int kTileRowsMfma = 128;  // query rows per bf16 (matrix-core) attention work-group
+constexpr int kTileRowsF32 = 128;   // query rows per fp32 attention work-group
+constexpr int kMaxGroup = 128;      // largest Hq / Hkv
 constexpr int kMaxBlocksPerSeq = 4096;  // limit of the routing kernels' LDS tables
 constexpr int kRouteRows = 4096;  // rows handled by one routing work-group
 
@@ -46,6 +48,7 @@ struct Problem {
   int route_rt;           // tokens per routing chunk
   int64_t hist_words;     // routing-histogram words per kv-head
   int64_t hist_entries;   // history selections over all rows and heads
+  int tile_rows;          // query rows per attention work-group (history and causal tiles)
 };
 
 // ---------------------------------------------------------------- launches
@@ -64,7 +67,7 @@ struct RouteBuffers {
   int32_t* hist;            // [Hkv * hist_words] per-chunk counts, then per-chunk exclusive offsets
   int32_t* bin_count;       // [Hkv * nblk_total]
   int64_t* bin_start;       // [Hkv * nblk_total + 1]
-  int32_t* bin_tile_start;  // [Hkv * nblk_total + 1] tiles of kTileRows entries
+  int32_t* bin_tile_start;  // [Hkv * nblk_total + 1] tiles of tile_rows entries
   uint32_t* entries;        // [hist_entries]
 };
 

@@ -13,7 +13,7 @@
 //   scan_cols  per bin: exclusive prefix over the chunks of its sequence (in
 //              place), and the bin total;
 //   scan_bins  one work-group: exclusive scans of bin totals (entry offsets)
-//              and of ceil(total / 128) (attention tile offsets);
+//              and of ceil(total / tile_rows) (attention tile offsets);
 //   scatter    per chunk, 256 rows at a time: every row ORs its bit into an
 //              LDS bitmask per selected block; a row's rank among the round's
 //              rows that chose the same block is the popcount of the lower
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256) void route_scan_cols_kernel(const SeqInfo* __r
 }
 
 __global__ __launch_bounds__(1024) void route_scan_bins_kernel(const int32_t* __restrict__ bin_count,
-                                                               int64_t nbins,
+                                                               int64_t nbins, int tile_rows,
                                                                int64_t* __restrict__ bin_start,
                                                                int32_t* __restrict__ bin_tile_start) {
   __shared__ int64_t se[1024];
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(1024) void route_scan_bins_kernel(const int32_t* __
   int64_t e = 0, tl = 0;
   for (int64_t b = b0; b < b1; b++) {
     e += bin_count[b];
-    tl += (bin_count[b] + kTileRows - 1) / kTileRows;
+    tl += (bin_count[b] + tile_rows - 1) / tile_rows;
   }
   se[tid] = e;
   stl[tid] = tl;
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(1024) void route_scan_bins_kernel(const int32_t* __
     bin_start[b] = eo;
     bin_tile_start[b] = (int32_t)to;
     eo += bin_count[b];
-    to += (bin_count[b] + kTileRows - 1) / kTileRows;
+    to += (bin_count[b] + tile_rows - 1) / tile_rows;
   }
   if (tid == 1023) {
     bin_start[nbins] = se[1023];
@@ -198,7 +198,8 @@ hipError_t launch_route(const int32_t* sel, const SeqInfo* seqs, const Problem& 
                                                                           rb.bin_count);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  route_scan_bins_kernel<<<1, 1024, 0, st>>>(rb.bin_count, nbins, rb.bin_start, rb.bin_tile_start);
+  route_scan_bins_kernel<<<1, 1024, 0, st>>>(rb.bin_count, nbins, p.tile_rows, rb.bin_start,
+                                              rb.bin_tile_start);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.route_chunks > 0 && p.hist_entries > 0) {
