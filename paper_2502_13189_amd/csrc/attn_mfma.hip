@@ -9,10 +9,13 @@
 // 256 B) and two V^T buffers (128 rows of 128 B), filled straight from global
 // memory by global_load_lds_dwordx4 (no registers, no LDS store
 // instructions).  Each such instruction writes 1 KiB contiguously (lane L to
-// 16-byte chunk L), so rows are not padded; instead 16-byte chunk c of row r
-// is stored at position c ^ (r & 7) (the permutation is applied to the
-// global addresses).  An operand read then has eight lanes on eight
-// consecutive rows hitting eight distinct chunk positions, i.e. all 32 banks.
+// 16-byte chunk L), so rows are not padded; instead the 16-byte chunks are
+// permuted within their rows (the permutation is applied to the global
+// addresses): chunk c of K row r sits at c ^ (r & 15), chunk c of V^T row r
+// at c ^ ((r >> 1) & 7).  LDS serves a 16-byte-per-lane read to 16 lanes at a
+// time across 64 banks (256 B); an operand read has 16 lanes on 16
+// consecutive rows at one logical chunk, and both permutations put those 16
+// chunks on distinct bank groups.
 //
 // Iteration i computes S(i) = K(i) . Q^T, its softmax and O += V(i) . P(i)
 // while the DMA fills the other K and V^T buffers with tile i+1; one barrier
@@ -80,50 +83,63 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
 
 // Global sources of this thread's lane in the LDS DMA of a tile.  Wave w
 // writes chunks 256w + 64x + L (x = 0..3, L = lane) of each buffer.
-//   K: chunk p is row p/16 at position p%16, holding logical chunk
-//      (p%16) ^ (row & 7); for x = 0, 2 and x = 1, 3 the logical chunk is
-//      the same, and the rows differ by 8.
-//   V^T: chunk p is row p/8 at position p%8, logical chunk (p%8) ^ (row & 7),
-//      the same for all x; rows differ by 8 per x (64 chunks).
+//   K: chunk p is row r = p/16 at position p%16, holding logical chunk
+//      (p%16) ^ (r & 15); each x has its own logical chunk.
+//   V^T: chunk p is row r = p/8 at position p%8, holding logical chunk
+//      (p%8) ^ ((r >> 1) & 7); x and x + 2 share it (rows 16 apart).
+// Addresses are a wave-uniform base (scalar registers, advanced per tile) plus
+// a 32-bit per-lane byte offset, the form the DMA instruction takes directly.
 struct Dma {
-  const __hip_bfloat16* kp[2];     // tile-0 source for x = 0 and x = 1
-  const __hip_bfloat16* klast[2];  // the sequence's last key, same logical chunk
-  int krow[2];                     // tile row for x = 0 and x = 1
-  int64_t k_row;                   // elements between key rows
-  int64_t len;                     // sequence length
-  const u32x4* vp;                 // tile-0 source chunk for x = 0
-  int dst;                         // this wave's first chunk: 256 w
+  const char* kbase;  // K of this kv-head at the sequence start (uniform)
+  int64_t k_tile;     // bytes between consecutive key tiles (uniform)
+  int64_t len;        // sequence length
+  const char* klast;  // the sequence's last key row (uniform)
+  uint32_t koff[4];   // per-lane byte offset of row/chunk in a tile, x = 0..3
+  uint32_t kcol[4];   // per-lane byte offset of the logical chunk in a row
+  const char* vbase;  // packed V^T tile 0 (uniform)
+  uint32_t voff[2];   // per-lane byte offset for x = 0, 1 (x = 2, 3: + 2 KiB)
+  int dst;            // this wave's first chunk: 256 w
+  int lane;
 };
+
+__device__ __forceinline__ int k_row_of(int dst, int lane, int x) { return (dst >> 4) + 4 * x + (lane >> 4); }
 
 __device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
   const int64_t base = (int64_t)i * kKeyTile;
-  const bool tail = base + kKeyTile > D.len;  // uniform
+  const char* tile = D.kbase + (int64_t)i * D.k_tile;
+  if (base + kKeyTile <= D.len) {
 #pragma unroll
-  for (int x = 0; x < 4; x++) {
-    const int row = D.krow[x & 1] + 8 * (x >> 1);
-    const __hip_bfloat16* src = D.kp[x & 1] + (base + 8 * (x >> 1)) * D.k_row;
+    for (int x = 0; x < 4; x++)
+      __builtin_amdgcn_global_load_lds(tile + D.koff[x], buf + D.dst + 64 * x, 16, 0, 0);
+  } else {
     // rows past the sequence end repeat its last key; they are always masked
-    if (tail && base + row >= D.len) src = D.klast[x & 1];
-    __builtin_amdgcn_global_load_lds(src, buf + D.dst + 64 * x, 16, 0, 0);
+#pragma unroll
+    for (int x = 0; x < 4; x++) {
+      const bool past = base + k_row_of(D.dst, D.lane, x) >= D.len;
+      const char* src = past ? D.klast + D.kcol[x] : tile + D.koff[x];
+      __builtin_amdgcn_global_load_lds(src, buf + D.dst + 64 * x, 16, 0, 0);
+    }
   }
 }
 
 __device__ __forceinline__ void dma_v(const Dma& D, int i, u32x4* buf) {
+  const char* tile = D.vbase + (int64_t)i * (kChunksV * 16);
 #pragma unroll
   for (int x = 0; x < 4; x++)
-    __builtin_amdgcn_global_load_lds(D.vp + (int64_t)i * kChunksV + 64 * x, buf + D.dst + 64 * x,
+    __builtin_amdgcn_global_load_lds(tile + D.voff[x & 1] + 2048 * (x >> 1), buf + D.dst + 64 * x,
                                      16, 0, 0);
 }
 
 // Wait for this wave's LDS DMA (and everything else) before a barrier.
 __device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0); }
 
-// Lane read offsets (chunks) into a K and a V^T buffer.  For the lane's row
-// r = 32*half + qc the logical chunk c sits at r*row + (c ^ (qc & 7)).
-//   K, chunk 2kk + hh:  kq[kk & 3] + 8 * (kk >> 2) + 512 * th
+// Lane read offsets (chunks) into a K and a V^T buffer.  The lane's rows are
+// r = 32*th + qc (K) and r = 32*dt + qc (V^T), so r & 15 = qc & 15 and
+// (r >> 1) & 7 = (qc >> 1) & 7.
+//   K, chunk 2kk + hh:  kq[kk] + 512 * th
 //   V^T, chunk 2st + hh: vq[st] + 256 * dt
 struct ReadOff {
-  int kq[4];
+  int kq[8];
   int vq[4];
 };
 
@@ -138,7 +154,7 @@ __device__ __forceinline__ void qk(f32x16 (&s)[2], const u32x4* kb, const ReadOf
   for (int kk = 0; kk < 8; kk++)
 #pragma unroll
     for (int th = 0; th < 2; th++)
-      s[th] = mfma(as_bf16x8(kb[ro.kq[kk & 3] + 8 * (kk >> 2) + 32 * kRowK * th]), qf[kk], s[th]);
+      s[th] = mfma(as_bf16x8(kb[ro.kq[kk] + 32 * kRowK * th]), qf[kk], s[th]);
 }
 
 // O^T += V^T . P^T: 16 MFMAs from the V^T buffer at vb.
@@ -291,29 +307,32 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
   {
     const int wv = __builtin_amdgcn_readfirstlane(wave);
     D.dst = 256 * wv;
-    const __hip_bfloat16* kbase = static_cast<const __hip_bfloat16*>(a.k) + (int64_t)g * a.k_sh;
+    D.lane = lane;
+    const int64_t kst = a.k_st * 2;  // bytes
+    D.kbase = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.k) +
+                                            (int64_t)g * a.k_sh) + tok0 * kst;
+    D.k_tile = kKeyTile * kst;
+    D.len = sq.len;
+    D.klast = D.kbase + (sq.len - 1) * kst;
+#pragma unroll
+    for (int x = 0; x < 4; x++) {
+      const int row = k_row_of(D.dst, lane, x);
+      D.kcol[x] = (uint32_t)(((lane & 15) ^ (row & 15)) * 16);
+      D.koff[x] = (uint32_t)(row * kst) + D.kcol[x];
+    }
+    D.vbase = reinterpret_cast<const char*>(
+        a.vt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) * (kKeyTile * kHeadDim));
 #pragma unroll
     for (int x = 0; x < 2; x++) {
-      const int p = 256 * wv + 64 * x + lane;
-      const int row = p >> 4;
-      const int lc = (p & 15) ^ (row & 7);
-      D.krow[x] = row;
-      D.kp[x] = kbase + (tok0 + row) * a.k_st + lc * 8;
-      D.klast[x] = kbase + (seq_end - 1) * a.k_st + lc * 8;
+      const int row = (D.dst + 64 * x + lane) >> 3;
+      D.voff[x] = (uint32_t)((row * kRowV + ((lane & 7) ^ ((row >> 1) & 7))) * 16);
     }
-    D.k_row = a.k_st;
-    D.len = sq.len;
-    const int vrow = (256 * wv + lane) >> 3;
-    const int vlc = (lane & 7) ^ (vrow & 7);
-    D.vp = reinterpret_cast<const u32x4*>(a.vt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) *
-                                                     (kKeyTile * kHeadDim)) + vrow * kRowV + vlc;
   }
   ReadOff ro;
 #pragma unroll
-  for (int j = 0; j < 4; j++) {
-    ro.kq[j] = qc * kRowK + ((2 * j + hh) ^ (qc & 7));
-    ro.vq[j] = qc * kRowV + ((2 * j + hh) ^ (qc & 7));
-  }
+  for (int j = 0; j < 8; j++) ro.kq[j] = qc * kRowK + ((2 * j + hh) ^ (qc & 15));
+#pragma unroll
+  for (int j = 0; j < 4; j++) ro.vq[j] = qc * kRowV + ((2 * j + hh) ^ ((qc >> 1) & 7));
   const float c2 = a.scale_log2;
   f32x16 o[4];
   float m = -INFINITY, l = 0.0f;
@@ -334,13 +353,11 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
   bf16x8 pb[4];
   for (int i = i0; i < i1; i++) {
     const int cur = (i - i0) & 1;
-    u32x4* const kcur = lds + cur * kBufK;
-    u32x4* const vcur = lds + 2 * kBufK + cur * kBufV;
     if (i + 1 < i1) {
       dma_k(D, i + 1, lds + (cur ^ 1) * kBufK);
       dma_v(D, i + 1, lds + 2 * kBufK + (cur ^ 1) * kBufV);
     }
-    qk(sc, kcur, ro, qf);
+    qk(sc, lds + cur * kBufK, ro, qf);
     const int64_t u0 = tok0 + (int64_t)i * kKeyTile;
     const bool edge =
         u0 < kbeg || u0 + kKeyTile > kend || (MODE != kHist && u0 + kKeyTile - 1 > tmin);
@@ -351,7 +368,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
       hi = (int)(MODE == kHist ? lim : min(lim, ri.t + 1 - u0)) - 4 * hh;
     }
     softmax<MODE>(sc, m, l, o, pb, edge, lo, hi, c2);
-    pv(o, vcur, ro, pb);
+    pv(o, lds + 2 * kBufK + cur * kBufV, ro, pb);
     dma_wait();
     __syncthreads();
   }
