@@ -145,7 +145,7 @@ __global__ __launch_bounds__(128, 1) void attn_f32_kernel(AttnArgs a, Problem p)
   float lse = (m_run + __builtin_amdgcn_logf(l_run)) * 0.69314718055994531f;
   if constexpr (MODE == kHist) {
     if (!valid) return;
-    float* orow = a.o_part + dst * kHeadDim;
+    float* orow = static_cast<float*>(a.o_part) + dst * kHeadDim;
     a.lse_part[dst] = lse;
 #pragma unroll
     for (int c = 0; c < kHeadDim / 4; c++)
@@ -160,7 +160,7 @@ __global__ __launch_bounds__(128, 1) void attn_f32_kernel(AttnArgs a, Problem p)
     const int nh = min(kh, (int)((kbeg - sq.tok_start) / p.B));
     if (nh > 0) {
       const float* lp = a.lse_part + dst * kh;
-      const float* op = a.o_part + dst * kh * kHeadDim;
+      const float* op = static_cast<const float*>(a.o_part) + dst * kh * kHeadDim;
       float M = lse;
       for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
       constexpr float kLog2e = 1.4426950408889634f;

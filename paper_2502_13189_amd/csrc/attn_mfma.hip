@@ -38,9 +38,11 @@
 // of a 16-key group, which is the order the V^T pack stores them in.
 //
 // Logits use scale 1/sqrt(D), folded with log2(e) into one FMA before exp2.
-// Outputs: history tiles write normalised fp32 partials and their natural-log
-// lse; current-block tiles merge those partials into the final output (the
-// log-sum-exp combine of Algorithm 1); dense tiles write the final output.
+// Outputs: history tiles write normalised partials, rounded once to bf16 (the
+// output dtype of the per-block attention calls of Algorithm 1), and their
+// natural-log lse in fp32; current-block tiles merge those partials into the
+// final output in fp32 (the log-sum-exp combine of Algorithm 1); dense tiles
+// write the final output.
 #include "moba_internal.h"
 
 #include <math.h>
@@ -288,7 +290,6 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
   }
   const SeqInfo sq = a.seqs[s];
   const int64_t tok0 = sq.tok_start;
-  const int64_t seq_end = tok0 + sq.len;
 
   // ---------------------------------------------------------- Q^T operands
   bf16x8 qf[8];
@@ -382,15 +383,17 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     const RowInfo& r = ri;
     if constexpr (MODE == kHist) {
       if (r.valid) {
-        float* orow = a.o_part + r.dst * kHeadDim;
+        // 4 consecutive dims per (dt, r4): one 8-byte store of 4 bf16
+        uint2* orow = reinterpret_cast<uint2*>(static_cast<__hip_bfloat16*>(a.o_part) +
+                                               r.dst * kHeadDim);
 #pragma unroll
         for (int dt = 0; dt < 4; dt++)
 #pragma unroll
           for (int r4 = 0; r4 < 4; r4++) {
-            const int d = 32 * dt + 8 * r4 + 4 * hh;
-            *reinterpret_cast<float4*>(orow + d) =
-                make_float4(og[dt][4 * r4 + 0] * inv, og[dt][4 * r4 + 1] * inv,
-                            og[dt][4 * r4 + 2] * inv, og[dt][4 * r4 + 3] * inv);
+            uint2 w;
+            w.x = pack_bf16(og[dt][4 * r4 + 0] * inv, og[dt][4 * r4 + 1] * inv);
+            w.y = pack_bf16(og[dt][4 * r4 + 2] * inv, og[dt][4 * r4 + 3] * inv);
+            orow[(32 * dt + 8 * r4 + 4 * hh) >> 2] = w;
           }
         if (hh == 0) a.lse_part[r.dst] = lse;
       }
@@ -405,7 +408,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
         const int nh = min(kh, (int)((tmin - tok0) / p.B));
         if (nh > 0) {
           const float* lp = a.lse_part + r.dst * kh;
-          const float* op = a.o_part + r.dst * kh * kHeadDim;
+          const uint2* op = reinterpret_cast<const uint2*>(
+              static_cast<const __hip_bfloat16*>(a.o_part) + r.dst * kh * kHeadDim);
           float M = lse;
           for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
           const float wc = __builtin_amdgcn_exp2f((lse - M) * kLog2e);
@@ -414,19 +418,20 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
           for (int dt = 0; dt < 4; dt++)
 #pragma unroll
             for (int q = 0; q < 16; q++) og[dt][q] *= wc * inv;
+#pragma unroll 2
           for (int x = 0; x < nh; x++) {
             const float w = __builtin_amdgcn_exp2f((lp[x] - M) * kLog2e);
             wsum += w;
-            const float* ox = op + x * kHeadDim;
+            const uint2* ox = op + x * (kHeadDim / 4);
 #pragma unroll
             for (int dt = 0; dt < 4; dt++)
 #pragma unroll
               for (int r4 = 0; r4 < 4; r4++) {
-                const float4 v = *reinterpret_cast<const float4*>(ox + 32 * dt + 8 * r4 + 4 * hh);
-                og[dt][4 * r4 + 0] = fmaf(w, v.x, og[dt][4 * r4 + 0]);
-                og[dt][4 * r4 + 1] = fmaf(w, v.y, og[dt][4 * r4 + 1]);
-                og[dt][4 * r4 + 2] = fmaf(w, v.z, og[dt][4 * r4 + 2]);
-                og[dt][4 * r4 + 3] = fmaf(w, v.w, og[dt][4 * r4 + 3]);
+                const uint2 v = ox[(32 * dt + 8 * r4 + 4 * hh) >> 2];
+                og[dt][4 * r4 + 0] = fmaf(w, __uint_as_float(v.x << 16), og[dt][4 * r4 + 0]);
+                og[dt][4 * r4 + 1] = fmaf(w, __uint_as_float(v.x & 0xffff0000u), og[dt][4 * r4 + 1]);
+                og[dt][4 * r4 + 2] = fmaf(w, __uint_as_float(v.y << 16), og[dt][4 * r4 + 2]);
+                og[dt][4 * r4 + 3] = fmaf(w, __uint_as_float(v.y & 0xffff0000u), og[dt][4 * r4 + 3]);
               }
           }
           scale = 1.0f / wsum;

@@ -1,22 +1,32 @@
 // Gate and top-k block selection (Eq. 5 and Eq. 6; the causal rules of
 // Sec. 2.2: no future block, current block forced on and counted toward k).
 //
-// One work-group per (sequence, group of `tw` tokens, kv-head).  Its 256
-// threads are (query head of the GQA group) x (token): thread i handles head
-// i / tw and token i % tw, so every wave scores the same kv-head's block keys
-// and its lanes read the same LDS row (broadcast).  Block keys are staged in
-// LDS 64 at a time.  Each lane keeps its query row in 128 fp32 registers and
-// a running top-(k-1) list in registers.
-//
-// Arithmetic: s_j = <q, kbar_j> in fp32 with four interleaved partial sums
-// combined pairwise.  The list is kept sorted by (score desc, block asc):
+// One work-group per (sequence, group of `tw` tokens, kv-head): 256 rows,
+// row i is query head i / tw of the GQA group and token i % tw, so every row
+// of a work-group scores the same kv-head's block keys.  Each row keeps a
+// running top-(k-1) list in registers, sorted by (score desc, block asc):
 // candidates arrive in ascending block order, so a newcomer is inserted after
 // every entry with a score >= its own, which realises the lowest-index
 // tie-break.  Unused places of the fixed-size list are +inf sentinels at the
 // top (never displaced) and -inf placeholders at the bottom.
+//
+// bf16 queries: the scores come from the matrix cores.  Each fp32 block key
+// is split exactly into three bf16 terms, kbar = hi + mid + lo (each term
+// takes the next 8 significant bits, so the sum carries at least 24 and the
+// remainder is below 2^-26 |kbar|); a bf16 query element times a term is exact
+// in fp32, so s_j = <q, hi> + <q, mid> + <q, lo> is an fp32-accumulated dot
+// product of the exact operands.  Per chunk of 32 blocks a wave computes
+// S^T (blocks x queries) for its 64 rows with v_mfma_f32_32x32x16_bf16
+// (3 terms x 8 k-steps per 32 rows), passes the tile through LDS so that each
+// lane holds its own row's 32 scores, and inserts them in block order.
+//
+// fp32 queries: s_j = <q, kbar_j> on the VALU in fp32 with four interleaved
+// partial sums combined pairwise, block keys broadcast from LDS.
 #include "moba_internal.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace moba {
 namespace {
@@ -27,26 +37,51 @@ template <typename T>
 __device__ __forceinline__ void load_q(const T* p, float* f);
 
 template <>
-__device__ __forceinline__ void load_q<__hip_bfloat16>(const __hip_bfloat16* p, float* f) {
-#pragma unroll
-  for (int c = 0; c < kHeadDim / 8; c++) {
-    uint4 u = reinterpret_cast<const uint4*>(p)[c];
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      f[8 * c + 2 * i] = __uint_as_float(w[i] << 16);
-      f[8 * c + 2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    }
-  }
-}
-
-template <>
 __device__ __forceinline__ void load_q<float>(const float* p, float* f) {
 #pragma unroll
   for (int c = 0; c < kHeadDim / 4; c++) {
     float4 u = reinterpret_cast<const float4*>(p)[c];
     f[4 * c] = u.x; f[4 * c + 1] = u.y; f[4 * c + 2] = u.z; f[4 * c + 3] = u.w;
   }
+}
+
+// Sorted insertion of block j with score sj into (sc, id) (see the header).
+template <int KM>
+__device__ __forceinline__ void insert_top(float (&sc)[KM], int (&id)[KM], float sj, int j) {
+  if (sj > sc[KM - 1]) {
+#pragma unroll
+    for (int x = KM - 1; x >= 1; x--) {
+      const bool after_prev = sj > sc[x - 1];
+      const bool here = sj > sc[x];
+      sc[x] = after_prev ? sc[x - 1] : (here ? sj : sc[x]);
+      id[x] = after_prev ? id[x - 1] : (here ? j : id[x]);
+    }
+    if (sj > sc[0]) { sc[0] = sj; id[0] = j; }
+  }
+}
+
+// Writes the row's selection: kept blocks ascending, then the current block,
+// then -1 padding.
+template <int KM>
+__device__ __forceinline__ void write_sel(int32_t* out, const int* id, int c, int K) {
+  int nh = 0;
+  if constexpr (KM > 0) {
+#pragma unroll
+    for (int x = 0; x < KM; x++) {
+      if (id[x] < c) {
+        int rank = 0;
+#pragma unroll
+        for (int y = 0; y < KM; y++) rank += (id[y] < id[x]) ? 1 : 0;
+        out[rank] = id[x];
+        nh++;
+      }
+    }
+  } else {
+    for (int j = 0; j < c; j++) out[j] = j;
+    nh = c;
+  }
+  out[nh] = c;
+  for (int x = nh + 1; x < K; x++) out[x] = -1;
 }
 
 // KM: capacity of the register list (>= topk - 1); KM == 0 selects every past
@@ -119,42 +154,163 @@ __global__ __launch_bounds__(256) void gate_kernel(const T* __restrict__ q, int6
         const float sj = (a0 + a1) + (a2 + a3);
         const int j = jc + jj;
         if (scores && j < nmax) scores[row * nmax + j] = sj;
-        if constexpr (KM > 0) {
-          if (sj > sc[KM - 1]) {
-#pragma unroll
-            for (int x = KM - 1; x >= 1; x--) {
-              const bool after_prev = sj > sc[x - 1];
-              const bool here = sj > sc[x];
-              sc[x] = after_prev ? sc[x - 1] : (here ? sj : sc[x]);
-              id[x] = after_prev ? id[x - 1] : (here ? j : id[x]);
-            }
-            if (sj > sc[0]) { sc[0] = sj; id[0] = j; }
-          }
-        }
+        if constexpr (KM > 0) insert_top<KM>(sc, id, sj, j);
       }
     }
   }
   if (!valid) return;
-  int32_t* out = sel + row * K;
-  int nh = 0;
+  write_sel<KM>(sel + row * K, id, c, K);
+}
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kChunk = 32;               // blocks per matrix tile
+constexpr int kTermRow = kHeadDim + 8;   // bf16 per LDS row of a block-key term (272 B)
+constexpr int kScoreRow = kChunk + 4;    // floats per LDS score row (144 B)
+
+template <int KM>
+__global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __restrict__ q,
+                                                        int64_t q_st, int64_t q_sh,
+                                                        const float* __restrict__ kbar,
+                                                        const SeqInfo* __restrict__ seqs, Problem p,
+                                                        int32_t* __restrict__ sel,
+                                                        float* __restrict__ scores, int nmax) {
+  __shared__ __attribute__((aligned(16))) __bf16 terms[3][kChunk][kTermRow];
+  __shared__ __attribute__((aligned(16))) float st[4][64][kScoreRow];
+  const int g = blockIdx.y;
+  const int s = find_seq(seqs, p.S, (int64_t)blockIdx.x, [](const SeqInfo& x) { return x.gate_off; });
+  const SeqInfo sq = seqs[s];
+  const int tw = p.gate_tw;
+  const int grp = blockIdx.x - sq.gate_off;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int qc = lane & 31, hh = lane >> 5;
+  const int last_tok = min(grp * tw + tw, sq.len) - 1;
+  const int cmax = last_tok / p.B;
+  const int K = p.topk;
+
+  // this lane's own row (insertion and output)
+  const int i = 64 * wave + lane;
+  const int hl = i / tw;
+  const int tl = grp * tw + i % tw;
+  const bool valid = hl < p.G && tl < sq.len;
+  const int c = valid ? tl / p.B : 0;
+  const int64_t row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;
+  if (valid && scores) {
+    for (int j = 0; j < nmax; j++) scores[row * nmax + j] = j < c ? 0.0f : NAN;
+  }
+
+  float sc[KM > 0 ? KM : 1];
+  int id[KM > 0 ? KM : 1];
   if constexpr (KM > 0) {
-    // kept entries are those with a real block index; write them ascending
 #pragma unroll
     for (int x = 0; x < KM; x++) {
-      if (id[x] < c) {
-        int rank = 0;
-#pragma unroll
-        for (int y = 0; y < KM; y++) rank += (id[y] < id[x]) ? 1 : 0;
-        out[rank] = id[x];
-        nh++;
-      }
+      const bool blocked = x < KM - (K - 1);
+      sc[x] = blocked ? INFINITY : -INFINITY;
+      id[x] = 0x7fffffff;
     }
-  } else {
-    for (int j = 0; j < c; j++) out[j] = j;
-    nh = c;
   }
-  out[nh] = c;
-  for (int x = nh + 1; x < K; x++) out[x] = -1;
+  const bool need_scores = KM > 0 || scores != nullptr;
+  if (need_scores && cmax > 0) {
+    // Q^T operands of the two 32-row sets of this wave: lane (qc, hh) holds
+    // dims 16 kk + 8 hh .. + 7 of row 64 wave + 32 set + qc.
+    bf16x8 qf[2][8];
+#pragma unroll
+    for (int set = 0; set < 2; set++) {
+      const int ib = 64 * wave + 32 * set + qc;
+      const int hb = ib / tw, tb = grp * tw + ib % tw;
+      const bool vb = hb < p.G && tb < sq.len;
+      const __hip_bfloat16* qr = q + ((int64_t)sq.tok_start + (vb ? tb : 0)) * q_st +
+                                 (int64_t)(g * p.G + (vb ? hb : 0)) * q_sh + 8 * hh;
+#pragma unroll
+      for (int kk = 0; kk < 8; kk++)
+        qf[set][kk] = vb ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qr + 16 * kk))
+                         : bf16x8{};
+    }
+    const float4* kb4 = reinterpret_cast<const float4*>(kbar);
+    // staging: thread -> block jb of the chunk, dims d0 .. d0 + 15
+    const int jb = threadIdx.x >> 3, d0 = 16 * (threadIdx.x & 7);
+    for (int jc = 0; jc < cmax; jc += kChunk) {
+      __syncthreads();  // previous chunk's terms are no longer read
+      {
+        float x[16];
+        const int j = jc + jb;
+        if (j < sq.nblk) {
+          const float4* src = kb4 + (((int64_t)sq.blk_off + j) * p.Hkv + g) * (kHeadDim / 4) + d0 / 4;
+#pragma unroll
+          for (int v = 0; v < 4; v++) {
+            const float4 f = src[v];
+            x[4 * v] = f.x; x[4 * v + 1] = f.y; x[4 * v + 2] = f.z; x[4 * v + 3] = f.w;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 16; e++) x[e] = 0.0f;
+        }
+        bf16x8 t[3][2];
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+          const __bf16 hi = (__bf16)x[e];
+          const float r1 = x[e] - (float)hi;
+          const __bf16 mid = (__bf16)r1;
+          const __bf16 lo = (__bf16)(r1 - (float)mid);
+          t[0][e >> 3][e & 7] = hi;
+          t[1][e >> 3][e & 7] = mid;
+          t[2][e >> 3][e & 7] = lo;
+        }
+#pragma unroll
+        for (int m = 0; m < 3; m++)
+#pragma unroll
+          for (int h2 = 0; h2 < 2; h2++)
+            *reinterpret_cast<bf16x8*>(&terms[m][jb][d0 + 8 * h2]) = t[m][h2];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int set = 0; set < 2; set++) {
+        f32x16 acc[3];
+#pragma unroll
+        for (int m = 0; m < 3; m++)
+#pragma unroll
+          for (int e = 0; e < 16; e++) acc[m][e] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < 8; kk++)
+#pragma unroll
+          for (int m = 0; m < 3; m++)
+            acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                *reinterpret_cast<const bf16x8*>(&terms[m][qc][16 * kk + 8 * hh]), qf[set][kk],
+                acc[m], 0, 0, 0);
+        // lane (qc, hh) holds row 32 set + qc, blocks 8 (e / 4) + 4 hh + e % 4
+#pragma unroll
+        for (int e4 = 0; e4 < 4; e4++) {
+          float4 v;
+          v.x = acc[0][4 * e4 + 0] + (acc[1][4 * e4 + 0] + acc[2][4 * e4 + 0]);
+          v.y = acc[0][4 * e4 + 1] + (acc[1][4 * e4 + 1] + acc[2][4 * e4 + 1]);
+          v.z = acc[0][4 * e4 + 2] + (acc[1][4 * e4 + 2] + acc[2][4 * e4 + 2]);
+          v.w = acc[0][4 * e4 + 3] + (acc[1][4 * e4 + 3] + acc[2][4 * e4 + 3]);
+          *reinterpret_cast<float4*>(&st[wave][32 * set + qc][8 * e4 + 4 * hh]) = v;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      // this lane's row: 32 scores in block order
+      const int jend = min(kChunk, c - jc);
+#pragma unroll
+      for (int b4 = 0; b4 < kChunk / 4; b4++) {
+        const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
+        const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          const int b = 4 * b4 + e;
+          if (b < jend) {
+            if (scores && jc + b < nmax) scores[row * nmax + jc + b] = f[e];
+            if constexpr (KM > 0) insert_top<KM>(sc, id, f[e], jc + b);
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  if (!valid) return;
+  write_sel<KM>(sel + row * K, id, c, K);
 }
 
 template <typename T, int KM>
@@ -162,8 +318,12 @@ hipError_t launch_km(const void* q, int64_t q_st, int64_t q_sh, const float* kba
                      const SeqInfo* seqs, const Problem& p, int32_t* sel, float* scores, int nmax,
                      hipStream_t st) {
   dim3 grid((unsigned)p.gate_groups, p.Hkv);
-  gate_kernel<T, KM><<<grid, 256, 0, st>>>(static_cast<const T*>(q), q_st, q_sh, kbar, seqs, p,
-                                           sel, scores, nmax);
+  if constexpr (std::is_same<T, __hip_bfloat16>::value)
+    gate_mfma_kernel<KM><<<grid, 256, 0, st>>>(static_cast<const T*>(q), q_st, q_sh, kbar, seqs, p,
+                                               sel, scores, nmax);
+  else
+    gate_kernel<T, KM><<<grid, 256, 0, st>>>(static_cast<const T*>(q), q_st, q_sh, kbar, seqs, p,
+                                             sel, scores, nmax);
   return hipGetLastError();
 }
 
@@ -172,13 +332,16 @@ hipError_t launch_typed(const void* q, int64_t q_st, int64_t q_sh, const float* 
                         const SeqInfo* seqs, const Problem& p, int32_t* sel, float* scores,
                         int nmax, hipStream_t st) {
   const int kh = p.topk - 1;
-  if (kh >= p.nblk_max - 1) return launch_km<T, 0>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  if (kh <= 1) return launch_km<T, 1>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  if (kh <= 3) return launch_km<T, 3>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  if (kh <= 7) return launch_km<T, 7>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  if (kh <= 15) return launch_km<T, 15>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  if (kh <= 31) return launch_km<T, 31>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  return launch_km<T, 63>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
+#define MOBA_GATE_KM(n) launch_km<T, n>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st)
+  if (kh >= p.nblk_max - 1) return MOBA_GATE_KM(0);
+  if (kh <= 1) return MOBA_GATE_KM(1);
+  if (kh <= 3) return MOBA_GATE_KM(3);
+  if (kh <= 7) return MOBA_GATE_KM(7);
+  if (kh <= 11) return MOBA_GATE_KM(11);
+  if (kh <= 15) return MOBA_GATE_KM(15);
+  if (kh <= 31) return MOBA_GATE_KM(31);
+  return MOBA_GATE_KM(63);
+#undef MOBA_GATE_KM
 }
 
 }  // namespace

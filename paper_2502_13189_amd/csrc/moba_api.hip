@@ -444,7 +444,8 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
     rb->bin_tile_start = bp->take<int32_t>(nbins + 1);
     rb->entries = bp->take<uint32_t>(p.hist_entries);
     const int64_t rows = (int64_t)nch * TG;
-    a->o_part = bp->take<float>(rows * kh * kHeadDim);
+    a->o_part = in.bf16 ? (void*)bp->take<__hip_bfloat16>(rows * kh * kHeadDim)
+                        : (void*)bp->take<float>(rows * kh * kHeadDim);
     a->lse_part = bp->take<float>(rows * kh);
     (void)base;
   };

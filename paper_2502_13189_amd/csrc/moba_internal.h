@@ -85,8 +85,9 @@ struct AttnArgs {
   const int64_t* bin_start;
   const int32_t* bin_count;
   const uint32_t* entries;
-  float* o_part;  // [rows_chunk * (topk-1), D]
-  float* lse_part;
+  void* o_part;     // [rows_chunk * (topk-1), D], normalised; bf16 on the bf16
+                    // path, fp32 on the fp32 path
+  float* lse_part;  // [rows_chunk * (topk-1)]
   // causal tiles
   const CausalTile* tiles;
   int64_t ntiles;
