@@ -58,6 +58,7 @@ __global__ __launch_bounds__(128, 1) void attn_f32_kernel(AttnArgs a, Problem p)
     dst = (int64_t)(ev - (uint64_t)a.g0 * TG * kh);
   } else {
     const CausalTile ct = a.tiles[blockIdx.x];
+    if (ct.t1 <= ct.t0) return;  // padding of the tile list
     g = a.g0 + blockIdx.y;
     s = ct.s;
     kbeg = ct.kbeg;

@@ -40,9 +40,9 @@
 // Logits use scale 1/sqrt(D), folded with log2(e) into one FMA before exp2.
 // Outputs: history tiles write normalised partials, rounded once to bf16 (the
 // output dtype of the per-block attention calls of Algorithm 1), and their
-// natural-log lse in fp32; current-block tiles merge those partials into the
-// final output in fp32 (the log-sum-exp combine of Algorithm 1); dense tiles
-// write the final output.
+// natural-log lse in fp32; current-block and dense tiles write the normalised
+// result to the output and its lse (the merge kernel then folds the history
+// partials into the current-block result).
 #include "moba_internal.h"
 
 #include <math.h>
@@ -67,7 +67,6 @@ constexpr int kBufV = kHeadDim * kRowV;            // 1024 chunks
 constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 64 KiB
 constexpr float kRescaleSlack = 8.0f;              // exp2 units
 constexpr float kLn2 = 0.69314718055994531f;
-constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
 
@@ -276,6 +275,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     ri.dst = (int64_t)(ev - (uint64_t)a.g0 * TG * kh);
   } else {
     const CausalTile ct = a.tiles[blockIdx.x];
+    if (ct.t1 <= ct.t0) return;  // padding of the tile list
     g = a.g0 + blockIdx.y;
     s = ct.s;
     kbeg = ct.kbeg;
@@ -398,46 +398,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
         if (hh == 0) a.lse_part[r.dst] = lse;
       }
     } else {
-      float scale = inv, lse_out = lse;
-      if constexpr (MODE == kCur) {
-        // Merge with the row's history partials (all rows of a tile share the
-        // current block c, so the slot count is uniform):
-        //   lse = M + ln(sum_i e^{lse_i - M}),  out = sum_i e^{lse_i - lse} O_i
-        // summed in a fixed order: current block first, then slots ascending.
-        const int kh = p.topk - 1;
-        const int nh = min(kh, (int)((tmin - tok0) / p.B));
-        if (nh > 0) {
-          const float* lp = a.lse_part + r.dst * kh;
-          const uint2* op = reinterpret_cast<const uint2*>(
-              static_cast<const __hip_bfloat16*>(a.o_part) + r.dst * kh * kHeadDim);
-          float M = lse;
-          for (int x = 0; x < nh; x++) M = fmaxf(M, lp[x]);
-          const float wc = __builtin_amdgcn_exp2f((lse - M) * kLog2e);
-          float wsum = wc;
-#pragma unroll
-          for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-            for (int q = 0; q < 16; q++) og[dt][q] *= wc * inv;
-#pragma unroll 2
-          for (int x = 0; x < nh; x++) {
-            const float w = __builtin_amdgcn_exp2f((lp[x] - M) * kLog2e);
-            wsum += w;
-            const uint2* ox = op + x * (kHeadDim / 4);
-#pragma unroll
-            for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-              for (int r4 = 0; r4 < 4; r4++) {
-                const uint2 v = ox[(32 * dt + 8 * r4 + 4 * hh) >> 2];
-                og[dt][4 * r4 + 0] = fmaf(w, __uint_as_float(v.x << 16), og[dt][4 * r4 + 0]);
-                og[dt][4 * r4 + 1] = fmaf(w, __uint_as_float(v.x & 0xffff0000u), og[dt][4 * r4 + 1]);
-                og[dt][4 * r4 + 2] = fmaf(w, __uint_as_float(v.y << 16), og[dt][4 * r4 + 2]);
-                og[dt][4 * r4 + 3] = fmaf(w, __uint_as_float(v.y & 0xffff0000u), og[dt][4 * r4 + 3]);
-              }
-          }
-          scale = 1.0f / wsum;
-          lse_out = M + __builtin_amdgcn_logf(wsum) * kLn2;
-        }
-      }
+      const float scale = inv, lse_out = lse;
       if (r.valid) {
         __hip_bfloat16* orow =
             static_cast<__hip_bfloat16*>(a.out) + r.t * a.o_st + (int64_t)r.h * a.o_sh;

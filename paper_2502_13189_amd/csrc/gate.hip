@@ -45,18 +45,23 @@ __device__ __forceinline__ void load_q<float>(const float* p, float* f) {
   }
 }
 
-// Sorted insertion of block j with score sj into (sc, id) (see the header).
+// Sorted insertion of block j with score sj into (sc, id) (see the header),
+// branch-free: the newcomer is carried down the list and swapped with every
+// entry it beats strictly, so an equal score stays below the earlier (lower
+// index) entry; whatever is carried out of the bottom is dropped.
 template <int KM>
 __device__ __forceinline__ void insert_top(float (&sc)[KM], int (&id)[KM], float sj, int j) {
-  if (sj > sc[KM - 1]) {
+  float cs = sj;
+  int ci = j;
 #pragma unroll
-    for (int x = KM - 1; x >= 1; x--) {
-      const bool after_prev = sj > sc[x - 1];
-      const bool here = sj > sc[x];
-      sc[x] = after_prev ? sc[x - 1] : (here ? sj : sc[x]);
-      id[x] = after_prev ? id[x - 1] : (here ? j : id[x]);
-    }
-    if (sj > sc[0]) { sc[0] = sj; id[0] = j; }
+  for (int x = 0; x < KM; x++) {
+    const bool gt = cs > sc[x];
+    const float hi = fmaxf(cs, sc[x]), lo = fminf(cs, sc[x]);
+    const int hid = gt ? ci : id[x], lid = gt ? id[x] : ci;
+    sc[x] = hi;
+    id[x] = hid;
+    cs = lo;
+    ci = lid;
   }
 }
 
@@ -300,10 +305,9 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
 #pragma unroll
         for (int e = 0; e < 4; e++) {
           const int b = 4 * b4 + e;
-          if (b < jend) {
-            if (scores && jc + b < nmax) scores[row * nmax + jc + b] = f[e];
-            if constexpr (KM > 0) insert_top<KM>(sc, id, f[e], jc + b);
-          }
+          if (scores && b < jend && jc + b < nmax) scores[row * nmax + jc + b] = f[e];
+          // blocks at or after the row's current block never enter the list
+          if constexpr (KM > 0) insert_top<KM>(sc, id, b < jend ? f[e] : -INFINITY, jc + b);
         }
       }
       __builtin_amdgcn_wave_barrier();

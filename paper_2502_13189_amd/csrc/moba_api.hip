@@ -5,9 +5,12 @@
 // moba_forward enqueues, on the caller's stream:
 //   pool -> [bf16: V^T pack] -> gate -> route (count, column scan, bin scan,
 //   scatter) -> per chunk of kv-heads: history attention, then current-block
-//   attention with the merge of the history partials.
-// Only the last three depend on the chunk; their workspace (fp32 partials)
-// is what the workspace cap limits.
+//   attention, then the merge of the history partials (bf16: a separate
+//   kernel working in place on the output; fp32: fused into the current-block
+//   kernel).
+// Only the attention steps depend on the chunk; their workspace (the
+// partials: bf16 on the bf16 path, fp32 on the fp32 path) is what the
+// workspace cap limits.
 #include "moba.h"
 #include "moba_internal.h"
 
@@ -233,9 +236,49 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
   pl->tiles.clear();
   if (mode == kTilesNone) return;
   const int tt = std::max(1, tile_rows / p.G);  // tokens per causal tile
+  if (mode == kTilesCur) {
+    // Tiles of one key block read the same K/V.  Work-groups go round-robin
+    // to the 8 XCDs (each with its own L2), so each block's tiles are put on
+    // one XCD, longest first, with blocks spread greedily over the XCDs by
+    // key work; tile x of the list runs on XCD x % 8 (the list is padded
+    // with empty tiles to a multiple of 8).
+    struct Group { int64_t work; std::vector<CausalTile> tiles; };
+    std::vector<Group> groups;
+    for (int s = 0; s < S; s++) {
+      const int64_t L = (int64_t)cu[s + 1] - cu[s];
+      for (int64_t b0 = 0; b0 < L; b0 += B) {
+        const int64_t b1 = std::min(L, b0 + B);
+        Group gr{0, {}};
+        for (int64_t t0 = b0; t0 < b1; t0 += tt) {
+          const int64_t t1 = std::min(b1, t0 + tt);
+          gr.tiles.push_back(CausalTile{s, (int32_t)(cu[s] + t0), (int32_t)(cu[s] + t1),
+                                        (int32_t)(cu[s] + b0)});
+          gr.work += t1 - b0;
+        }
+        std::reverse(gr.tiles.begin(), gr.tiles.end());
+        groups.push_back(std::move(gr));
+      }
+    }
+    std::stable_sort(groups.begin(), groups.end(),
+                     [](const Group& x, const Group& y) { return x.work > y.work; });
+    constexpr int kXcd = 8;
+    std::vector<std::vector<CausalTile>> lists(kXcd);
+    int64_t load[kXcd] = {0};
+    for (const Group& gr : groups) {
+      const int x = (int)(std::min_element(load, load + kXcd) - load);
+      lists[x].insert(lists[x].end(), gr.tiles.begin(), gr.tiles.end());
+      load[x] += gr.work;
+    }
+    size_t n = 0;
+    for (const auto& l : lists) n = std::max(n, l.size());
+    for (size_t k = 0; k < n; k++)
+      for (int x = 0; x < kXcd; x++)
+        pl->tiles.push_back(k < lists[x].size() ? lists[x][k] : CausalTile{0, 0, 0, 0});
+    return;
+  }
   for (int s = 0; s < S; s++) {
     const int64_t L = (int64_t)cu[s + 1] - cu[s];
-    const int64_t Bs = mode == kTilesCur ? B : std::max<int64_t>(L, 1);
+    const int64_t Bs = std::max<int64_t>(L, 1);
     for (int64_t b0 = 0; b0 < L; b0 += Bs) {
       const int64_t b1 = std::min(L, b0 + Bs);
       for (int64_t t0 = b0; t0 < b1; t0 += tt)
@@ -505,9 +548,17 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
       MOBA_LAUNCH(in.bf16 ? launch_attn_hist_bf16(a, p, grid, stream)
                           : launch_attn_hist_f32(a, p, grid, stream));
     }
-    { Phase ph("attn_cur_merge", stream);
-      MOBA_LAUNCH(in.bf16 ? launch_attn_causal_bf16(false, a, p, stream)
-                          : launch_attn_causal_f32(false, a, p, stream)); }
+    if (in.bf16) {
+      { Phase ph("attn_cur", stream);
+        MOBA_LAUNCH(launch_attn_causal_bf16(false, a, p, stream)); }
+      if (kh > 0) {
+        Phase ph("merge", stream);
+        MOBA_LAUNCH(launch_merge_bf16(a, p, stream));
+      }
+    } else {
+      Phase ph("attn_cur_merge", stream);
+      MOBA_LAUNCH(launch_attn_causal_f32(false, a, p, stream));
+    }
   }
   return MOBA_OK;
 }

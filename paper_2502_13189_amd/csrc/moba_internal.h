@@ -104,6 +104,8 @@ hipError_t launch_attn_hist_bf16(const AttnArgs& a, const Problem& p, int64_t gr
 hipError_t launch_attn_causal_bf16(bool dense, const AttnArgs& a, const Problem& p, hipStream_t st);
 hipError_t launch_attn_hist_f32(const AttnArgs& a, const Problem& p, int64_t grid, hipStream_t st);
 hipError_t launch_attn_causal_f32(bool dense, const AttnArgs& a, const Problem& p, hipStream_t st);
+// bf16 path: folds the history partials of chunk rows into out / lse in place.
+hipError_t launch_merge_bf16(const AttnArgs& a, const Problem& p, hipStream_t st);
 
 // ------------------------------------------------------------ device helpers
 // Largest s with key[s] <= x among sequences, skipping empty ones that share
