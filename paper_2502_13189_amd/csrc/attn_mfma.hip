@@ -5,17 +5,16 @@
 //
 // Work-group = 4 waves = 128 query rows; wave w owns rows 32w..32w+31, one
 // query per lane column; two work-groups share a CU (two waves per SIMD).
-// Keys are consumed in tiles of 64.  LDS holds two K buffers (64 rows of
-// 256 B) and two V^T buffers (128 rows of 128 B), filled straight from global
-// memory by global_load_lds_dwordx4 (no registers, no LDS store
-// instructions).  Each such instruction writes 1 KiB contiguously (lane L to
-// 16-byte chunk L), so rows are not padded; instead the 16-byte chunks are
-// permuted within their rows (the permutation is applied to the global
-// addresses): chunk c of K row r sits at c ^ (r & 15), chunk c of V^T row r
-// at c ^ ((r >> 1) & 7).  LDS serves a 16-byte-per-lane read to 16 lanes at a
-// time across 64 banks (256 B); an operand read has 16 lanes on 16
-// consecutive rows at one logical chunk, and both permutations put those 16
-// chunks on distinct bank groups.
+// Keys are consumed in tiles of 64.  LDS holds two K buffers and two V^T
+// buffers, filled straight from global memory by global_load_lds_dwordx4 (no
+// registers, no LDS store instructions).  Each such instruction writes 1 KiB
+// contiguously (lane L to 16-byte chunk L).  Rows are padded by one chunk (K:
+// 64 rows of 17 chunks, V^T: 128 rows of 9 chunks; the pad chunk receives a
+// copy of the row's last chunk), so the DMA writes whole padded rows and an
+// operand read, 16 lanes on 16 consecutive rows at one chunk, hits 16
+// distinct bank groups (LDS serves a 16-byte-per-lane read to 16 lanes at a
+// time across 64 banks of 4 bytes).  Every operand address is then a per-lane
+// base plus a compile-time offset.
 //
 // Iteration i computes S(i) = K(i) . Q^T, its softmax and O += V(i) . P(i)
 // while the DMA fills the other K and V^T buffers with tile i+1; one barrier
@@ -60,11 +59,14 @@ enum { kHist = 0, kCur = 1, kDense = 2 };
 
 constexpr int kRows = kTileRowsMfma;               // query rows per work-group (128)
 constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // 16-byte chunks per V^T tile (1024)
-constexpr int kRowK = kHeadDim / 8;                // LDS K row: 16 chunks
-constexpr int kRowV = kKeyTile / 8;                // LDS V^T row: 8 chunks
-constexpr int kBufK = kKeyTile * kRowK;            // 1024 chunks
-constexpr int kBufV = kHeadDim * kRowV;            // 1024 chunks
-constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 64 KiB
+constexpr int kRowK = kHeadDim / 8 + 1;            // LDS K row: 16 chunks + 1 pad
+constexpr int kRowV = kKeyTile / 8 + 1;            // LDS V^T row: 8 chunks + 1 pad
+constexpr int kBufK = kKeyTile * kRowK;            // 1088 chunks
+constexpr int kBufV = kHeadDim * kRowV;            // 1152 chunks
+constexpr int kDmaK = kBufK / 64;                  // DMA instructions per K tile (17)
+constexpr int kDmaV = kBufV / 64;                  // DMA instructions per V^T tile (18)
+constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 70 KiB
+static_assert(kBufK % 64 == 0 && kBufV % 64 == 0, "DMA windows cover whole buffers");
 constexpr float kRescaleSlack = 8.0f;              // exp2 units
 constexpr float kLn2 = 0.69314718055994531f;
 
@@ -82,66 +84,66 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// Global sources of this thread's lane in the LDS DMA of a tile.  Wave w
-// writes chunks 256w + 64x + L (x = 0..3, L = lane) of each buffer.
-//   K: chunk p is row r = p/16 at position p%16, holding logical chunk
-//      (p%16) ^ (r & 15); each x has its own logical chunk.
-//   V^T: chunk p is row r = p/8 at position p%8, holding logical chunk
-//      (p%8) ^ ((r >> 1) & 7); x and x + 2 share it (rows 16 apart).
-// Addresses are a wave-uniform base (scalar registers, advanced per tile) plus
-// a 32-bit per-lane byte offset, the form the DMA instruction takes directly.
+// Global sources of this thread's lane in the LDS DMA of a tile.  DMA
+// instruction j writes buffer chunks 64j .. 64j+63; wave w issues j = w + 4x
+// (x = 0..4, while j < kDmaK or kDmaV).  Lane L of instruction j fills chunk
+// p = 64j + L: K row p / 17, chunk min(p % 17, 15); V^T row p / 9, chunk
+// min(p % 9, 7).  Addresses are a wave-uniform base plus a 32-bit per-lane
+// byte offset.
 struct Dma {
   const char* kbase;  // K of this kv-head at the sequence start (uniform)
   int64_t k_tile;     // bytes between consecutive key tiles (uniform)
   int64_t len;        // sequence length
   const char* klast;  // the sequence's last key row (uniform)
-  uint32_t koff[4];   // per-lane byte offset of row/chunk in a tile, x = 0..3
-  uint32_t kcol[4];   // per-lane byte offset of the logical chunk in a row
+  uint32_t koff[5];   // per-lane byte offset of the chunk within a tile
+  uint32_t kcol[5];   // per-lane byte offset of the chunk within its row
+  int krow[5];        // tile row of the lane's chunk
   const char* vbase;  // packed V^T tile 0 (uniform)
-  uint32_t voff[2];   // per-lane byte offset for x = 0, 1 (x = 2, 3: + 2 KiB)
-  int dst;            // this wave's first chunk: 256 w
-  int lane;
+  uint32_t voff[5];
+  int wave;           // wave-uniform
 };
 
-__device__ __forceinline__ int k_row_of(int dst, int lane, int x) { return (dst >> 4) + 4 * x + (lane >> 4); }
+__device__ __forceinline__ void dma_k1(const Dma& D, const char* tile, bool tail, int64_t base,
+                                       u32x4* buf, int x) {
+  const char* src = tile + D.koff[x];
+  // rows past the sequence end repeat its last key; they are always masked
+  if (tail && base + D.krow[x] >= D.len) src = D.klast + D.kcol[x];
+  __builtin_amdgcn_global_load_lds(src, buf + 64 * (D.wave + 4 * x), 16, 0, 0);
+}
 
 __device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
   const int64_t base = (int64_t)i * kKeyTile;
   const char* tile = D.kbase + (int64_t)i * D.k_tile;
-  if (base + kKeyTile <= D.len) {
-#pragma unroll
-    for (int x = 0; x < 4; x++)
-      __builtin_amdgcn_global_load_lds(tile + D.koff[x], buf + D.dst + 64 * x, 16, 0, 0);
-  } else {
-    // rows past the sequence end repeat its last key; they are always masked
-#pragma unroll
-    for (int x = 0; x < 4; x++) {
-      const bool past = base + k_row_of(D.dst, D.lane, x) >= D.len;
-      const char* src = past ? D.klast + D.kcol[x] : tile + D.koff[x];
-      __builtin_amdgcn_global_load_lds(src, buf + D.dst + 64 * x, 16, 0, 0);
-    }
-  }
+  const bool tail = base + kKeyTile > D.len;
+  dma_k1(D, tile, tail, base, buf, 0);
+  dma_k1(D, tile, tail, base, buf, 1);
+  dma_k1(D, tile, tail, base, buf, 2);
+  dma_k1(D, tile, tail, base, buf, 3);
+  if (D.wave + 16 < kDmaK) dma_k1(D, tile, tail, base, buf, 4);
+}
+
+__device__ __forceinline__ void dma_v1(const Dma& D, const char* tile, u32x4* buf, int x) {
+  __builtin_amdgcn_global_load_lds(tile + D.voff[x], buf + 64 * (D.wave + 4 * x), 16, 0, 0);
 }
 
 __device__ __forceinline__ void dma_v(const Dma& D, int i, u32x4* buf) {
   const char* tile = D.vbase + (int64_t)i * (kChunksV * 16);
-#pragma unroll
-  for (int x = 0; x < 4; x++)
-    __builtin_amdgcn_global_load_lds(tile + D.voff[x & 1] + 2048 * (x >> 1), buf + D.dst + 64 * x,
-                                     16, 0, 0);
+  dma_v1(D, tile, buf, 0);
+  dma_v1(D, tile, buf, 1);
+  dma_v1(D, tile, buf, 2);
+  dma_v1(D, tile, buf, 3);
+  if (D.wave + 16 < kDmaV) dma_v1(D, tile, buf, 4);
 }
 
 // Wait for this wave's LDS DMA (and everything else) before a barrier.
 __device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0); }
 
-// Lane read offsets (chunks) into a K and a V^T buffer.  The lane's rows are
-// r = 32*th + qc (K) and r = 32*dt + qc (V^T), so r & 15 = qc & 15 and
-// (r >> 1) & 7 = (qc >> 1) & 7.
-//   K, chunk 2kk + hh:  kq[kk] + 512 * th
-//   V^T, chunk 2st + hh: vq[st] + 256 * dt
+// Lane read bases (chunks) into a K and a V^T buffer: K row 32*th + qc,
+// chunk 2kk + hh is kq + 32*kRowK*th + 2kk; V^T row 32*dt + qc, chunk
+// 2st + hh is vq + 32*kRowV*dt + 2st.
 struct ReadOff {
-  int kq[8];
-  int vq[4];
+  int kq;
+  int vq;
 };
 
 // S^T: 16 MFMAs from the K buffer at kb.
@@ -151,21 +153,23 @@ __device__ __forceinline__ void qk(f32x16 (&s)[2], const u32x4* kb, const ReadOf
   for (int th = 0; th < 2; th++)
 #pragma unroll
     for (int r = 0; r < 16; r++) s[th][r] = 0.0f;
+  const u32x4* k = kb + ro.kq;
 #pragma unroll
   for (int kk = 0; kk < 8; kk++)
 #pragma unroll
     for (int th = 0; th < 2; th++)
-      s[th] = mfma(as_bf16x8(kb[ro.kq[kk] + 32 * kRowK * th]), qf[kk], s[th]);
+      s[th] = mfma(as_bf16x8(k[32 * kRowK * th + 2 * kk]), qf[kk], s[th]);
 }
 
 // O^T += V^T . P^T: 16 MFMAs from the V^T buffer at vb.
 __device__ __forceinline__ void pv(f32x16 (&o)[4], const u32x4* vb, const ReadOff& ro,
                                    const bf16x8 (&pb)[4]) {
+  const u32x4* v = vb + ro.vq;
 #pragma unroll
   for (int st = 0; st < 4; st++)
 #pragma unroll
     for (int dt = 0; dt < 4; dt++)
-      o[dt] = mfma(as_bf16x8(vb[ro.vq[st] + 32 * kRowV * dt]), pb[st], o[dt]);
+      o[dt] = mfma(as_bf16x8(v[32 * kRowV * dt + 2 * st]), pb[st], o[dt]);
 }
 
 struct RowInfo {
@@ -307,8 +311,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
   Dma D;
   {
     const int wv = __builtin_amdgcn_readfirstlane(wave);
-    D.dst = 256 * wv;
-    D.lane = lane;
+    D.wave = wv;
     const int64_t kst = a.k_st * 2;  // bytes
     D.kbase = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.k) +
                                             (int64_t)g * a.k_sh) + tok0 * kst;
@@ -316,24 +319,22 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     D.len = sq.len;
     D.klast = D.kbase + (sq.len - 1) * kst;
 #pragma unroll
-    for (int x = 0; x < 4; x++) {
-      const int row = k_row_of(D.dst, lane, x);
-      D.kcol[x] = (uint32_t)(((lane & 15) ^ (row & 15)) * 16);
+    for (int x = 0; x < 5; x++) {
+      const int pk = 64 * (wv + 4 * x) + lane;
+      const int row = min(pk / kRowK, kKeyTile - 1), c = min(pk % kRowK, kRowK - 2);
+      D.krow[x] = row;
+      D.kcol[x] = (uint32_t)(c * 16);
       D.koff[x] = (uint32_t)(row * kst) + D.kcol[x];
+      const int pv_ = 64 * (wv + 4 * x) + lane;
+      const int vrow = min(pv_ / kRowV, kHeadDim - 1), vc = min(pv_ % kRowV, kRowV - 2);
+      D.voff[x] = (uint32_t)(vrow * (kKeyTile * 2) + vc * 16);
     }
     D.vbase = reinterpret_cast<const char*>(
         a.vt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) * (kKeyTile * kHeadDim));
-#pragma unroll
-    for (int x = 0; x < 2; x++) {
-      const int row = (D.dst + 64 * x + lane) >> 3;
-      D.voff[x] = (uint32_t)((row * kRowV + ((lane & 7) ^ ((row >> 1) & 7))) * 16);
-    }
   }
   ReadOff ro;
-#pragma unroll
-  for (int j = 0; j < 8; j++) ro.kq[j] = qc * kRowK + ((2 * j + hh) ^ (qc & 15));
-#pragma unroll
-  for (int j = 0; j < 4; j++) ro.vq[j] = qc * kRowV + ((2 * j + hh) ^ ((qc >> 1) & 7));
+  ro.kq = qc * kRowK + hh;
+  ro.vq = qc * kRowV + hh;
   const float c2 = a.scale_log2;
   f32x16 o[4];
   float m = -INFINITY, l = 0.0f;
