@@ -80,6 +80,12 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
 
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -114,12 +120,19 @@ __device__ __forceinline__ void dma_k1(const Dma& D, const char* tile, bool tail
 __device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
   const int64_t base = (int64_t)i * kKeyTile;
   const char* tile = D.kbase + (int64_t)i * D.k_tile;
-  const bool tail = base + kKeyTile > D.len;
-  dma_k1(D, tile, tail, base, buf, 0);
-  dma_k1(D, tile, tail, base, buf, 1);
-  dma_k1(D, tile, tail, base, buf, 2);
-  dma_k1(D, tile, tail, base, buf, 3);
-  if (D.wave + 16 < kDmaK) dma_k1(D, tile, tail, base, buf, 4);
+  if (base + kKeyTile <= D.len) {
+    dma_k1(D, tile, false, base, buf, 0);
+    dma_k1(D, tile, false, base, buf, 1);
+    dma_k1(D, tile, false, base, buf, 2);
+    dma_k1(D, tile, false, base, buf, 3);
+    if (D.wave + 16 < kDmaK) dma_k1(D, tile, false, base, buf, 4);
+  } else {
+    dma_k1(D, tile, true, base, buf, 0);
+    dma_k1(D, tile, true, base, buf, 1);
+    dma_k1(D, tile, true, base, buf, 2);
+    dma_k1(D, tile, true, base, buf, 3);
+    if (D.wave + 16 < kDmaK) dma_k1(D, tile, true, base, buf, 4);
+  }
 }
 
 __device__ __forceinline__ void dma_v1(const Dma& D, const char* tile, u32x4* buf, int x) {
@@ -292,6 +305,12 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     ri.h = g * p.G + rr % p.G;
     ri.dst = (int64_t)(g - a.g0) * p.T * p.G + ri.t * p.G + (rr % p.G);
   }
+  // the tile's key range is wave-uniform: keep it in scalar registers
+  g = __builtin_amdgcn_readfirstlane(g);
+  s = __builtin_amdgcn_readfirstlane(s);
+  kbeg = uniform64(kbeg);
+  kend = uniform64(kend);
+  tmin = uniform64(tmin);
   const SeqInfo sq = a.seqs[s];
   const int64_t tok0 = sq.tok_start;
 
