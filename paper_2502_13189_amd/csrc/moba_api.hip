@@ -506,6 +506,8 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
     if (bp.off + kAlign <= limit) { nch = n; need = bp.off + kAlign; break; }
   }
   if (nch == 0) return MOBA_ERR_NO_MEMORY;
+  // as many chunks as the cap requires, of equal size (the last may be smaller)
+  nch = (int)ceil_div(p.Hkv, ceil_div(p.Hkv, nch));
   if ((st = ensure_workspace(dc, need)) != MOBA_OK) return st;
 
   Bump bp(dc->ws);
