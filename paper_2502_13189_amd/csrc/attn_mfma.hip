@@ -3,8 +3,10 @@
 // flash_attention_varlen calls; Sec. 2.2 "Current Block Attention") and dense
 // causal attention (Eq. 1), from one kernel template.
 //
-// Work-group = 4 waves = 128 query rows; wave w owns rows 32w..32w+31, one
-// query per lane column; two work-groups share a CU (two waves per SIMD).
+// Work-group = 8 waves = 256 query rows, one work-group per CU (two waves per
+// SIMD); wave w owns rows 32w..32w+31, one query per lane column.  Sharing
+// each K/V tile among 256 rows halves the LDS writes and DMA instructions per
+// row compared with 128-row work-groups.
 // Keys are consumed in tiles of 64.  LDS holds two K buffers and two V^T
 // buffers, filled straight from global memory by global_load_lds_dwordx4 (no
 // registers, no LDS store instructions).  Each such instruction writes 1 KiB
@@ -18,8 +20,7 @@
 //
 // Iteration i computes S(i) = K(i) . Q^T, its softmax and O += V(i) . P(i)
 // while the DMA fills the other K and V^T buffers with tile i+1; one barrier
-// per tile.  The two waves of a SIMD belong to different work-groups, so one
-// wave's softmax overlaps the other's MFMAs.
+// per tile.
 //
 // Per key tile and wave, on v_mfma_f32_32x32x16_bf16:
 //   S^T (keys x queries) = K . Q^T         2 halves x 8 k-steps
@@ -57,7 +58,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chun
 
 enum { kHist = 0, kCur = 1, kDense = 2 };
 
-constexpr int kRows = kTileRowsMfma;               // query rows per work-group (128)
+constexpr int kRows = kTileRowsMfma;               // query rows per work-group (256)
 constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // 16-byte chunks per V^T tile (1024)
 constexpr int kRowK = kHeadDim / 8 + 1;            // LDS K row: 16 chunks + 1 pad
 constexpr int kRowV = kKeyTile / 8 + 1;            // LDS V^T row: 8 chunks + 1 pad
@@ -91,8 +92,8 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
 }
 
 // Global sources of this thread's lane in the LDS DMA of a tile.  DMA
-// instruction j writes buffer chunks 64j .. 64j+63; wave w issues j = w + 4x
-// (x = 0..4, while j < kDmaK or kDmaV).  Lane L of instruction j fills chunk
+// instruction j writes buffer chunks 64j .. 64j+63; wave w issues j = w + 8x
+// (x = 0..2, while j < kDmaK or kDmaV).  Lane L of instruction j fills chunk
 // p = 64j + L: K row p / 17, chunk min(p % 17, 15); V^T row p / 9, chunk
 // min(p % 9, 7).  Addresses are a wave-uniform base plus a 32-bit per-lane
 // byte offset.
@@ -101,11 +102,11 @@ struct Dma {
   int64_t k_tile;     // bytes between consecutive key tiles (uniform)
   int64_t len;        // sequence length
   const char* klast;  // the sequence's last key row (uniform)
-  uint32_t koff[5];   // per-lane byte offset of the chunk within a tile
-  uint32_t kcol[5];   // per-lane byte offset of the chunk within its row
-  int krow[5];        // tile row of the lane's chunk
+  uint32_t koff[3];   // per-lane byte offset of the chunk within a tile
+  uint32_t kcol[3];   // per-lane byte offset of the chunk within its row
+  int krow[3];        // tile row of the lane's chunk
   const char* vbase;  // packed V^T tile 0 (uniform)
-  uint32_t voff[5];
+  uint32_t voff[3];
   int wave;           // wave-uniform
 };
 
@@ -114,7 +115,7 @@ __device__ __forceinline__ void dma_k1(const Dma& D, const char* tile, bool tail
   const char* src = tile + D.koff[x];
   // rows past the sequence end repeat its last key; they are always masked
   if (tail && base + D.krow[x] >= D.len) src = D.klast + D.kcol[x];
-  __builtin_amdgcn_global_load_lds(src, buf + 64 * (D.wave + 4 * x), 16, 0, 0);
+  __builtin_amdgcn_global_load_lds(src, buf + 64 * (D.wave + 8 * x), 16, 0, 0);
 }
 
 __device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
@@ -123,29 +124,23 @@ __device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
   if (base + kKeyTile <= D.len) {
     dma_k1(D, tile, false, base, buf, 0);
     dma_k1(D, tile, false, base, buf, 1);
-    dma_k1(D, tile, false, base, buf, 2);
-    dma_k1(D, tile, false, base, buf, 3);
-    if (D.wave + 16 < kDmaK) dma_k1(D, tile, false, base, buf, 4);
+    if (D.wave + 16 < kDmaK) dma_k1(D, tile, false, base, buf, 2);
   } else {
     dma_k1(D, tile, true, base, buf, 0);
     dma_k1(D, tile, true, base, buf, 1);
-    dma_k1(D, tile, true, base, buf, 2);
-    dma_k1(D, tile, true, base, buf, 3);
-    if (D.wave + 16 < kDmaK) dma_k1(D, tile, true, base, buf, 4);
+    if (D.wave + 16 < kDmaK) dma_k1(D, tile, true, base, buf, 2);
   }
 }
 
 __device__ __forceinline__ void dma_v1(const Dma& D, const char* tile, u32x4* buf, int x) {
-  __builtin_amdgcn_global_load_lds(tile + D.voff[x], buf + 64 * (D.wave + 4 * x), 16, 0, 0);
+  __builtin_amdgcn_global_load_lds(tile + D.voff[x], buf + 64 * (D.wave + 8 * x), 16, 0, 0);
 }
 
 __device__ __forceinline__ void dma_v(const Dma& D, int i, u32x4* buf) {
   const char* tile = D.vbase + (int64_t)i * (kChunksV * 16);
   dma_v1(D, tile, buf, 0);
   dma_v1(D, tile, buf, 1);
-  dma_v1(D, tile, buf, 2);
-  dma_v1(D, tile, buf, 3);
-  if (D.wave + 16 < kDmaV) dma_v1(D, tile, buf, 4);
+  if (D.wave + 16 < kDmaV) dma_v1(D, tile, buf, 2);
 }
 
 // Wait for this wave's LDS DMA (and everything else) before a barrier.
@@ -245,7 +240,7 @@ __device__ __forceinline__ void softmax(f32x16 (&s)[2], float& m, float& l, f32x
 }
 
 template <int MODE>
-__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p) {
+__global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p) {
   __shared__ u32x4 lds[kLdsChunks];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -338,13 +333,13 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
     D.len = sq.len;
     D.klast = D.kbase + (sq.len - 1) * kst;
 #pragma unroll
-    for (int x = 0; x < 5; x++) {
-      const int pk = 64 * (wv + 4 * x) + lane;
+    for (int x = 0; x < 3; x++) {
+      const int pk = 64 * (wv + 8 * x) + lane;
       const int row = min(pk / kRowK, kKeyTile - 1), c = min(pk % kRowK, kRowK - 2);
       D.krow[x] = row;
       D.kcol[x] = (uint32_t)(c * 16);
       D.koff[x] = (uint32_t)(row * kst) + D.kcol[x];
-      const int pv_ = 64 * (wv + 4 * x) + lane;
+      const int pv_ = 64 * (wv + 8 * x) + lane;
       const int vrow = min(pv_ / kRowV, kHeadDim - 1), vc = min(pv_ % kRowV, kRowV - 2);
       D.voff[x] = (uint32_t)(vrow * (kKeyTile * 2) + vc * 16);
     }
@@ -443,15 +438,15 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(AttnArgs a, Problem p
 hipError_t launch_attn_hist_bf16(const AttnArgs& a, const Problem& p, int64_t grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
   grid = (grid + 7) / 8 * 8;
-  attn_mfma_kernel<kHist><<<(unsigned)grid, 256, 0, st>>>(a, p);
+  attn_mfma_kernel<kHist><<<(unsigned)grid, 512, 0, st>>>(a, p);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_causal_bf16(bool dense, const AttnArgs& a, const Problem& p, hipStream_t st) {
   if (a.ntiles <= 0 || a.g1 <= a.g0) return hipSuccess;
   dim3 grid((unsigned)a.ntiles, a.g1 - a.g0);
-  if (dense) attn_mfma_kernel<kDense><<<grid, 256, 0, st>>>(a, p);
-  else attn_mfma_kernel<kCur><<<grid, 256, 0, st>>>(a, p);
+  if (dense) attn_mfma_kernel<kDense><<<grid, 512, 0, st>>>(a, p);
+  else attn_mfma_kernel<kCur><<<grid, 512, 0, st>>>(a, p);
   return hipGetLastError();
 }
 

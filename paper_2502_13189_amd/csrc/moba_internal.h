@@ -9,7 +9,7 @@ namespace moba {
 
 constexpr int kHeadDim = 128;     // D; every kernel is specialised for it
 constexpr int kKeyTile = 64;      // keys per LDS tile in the attention kernels
-constexpr int kTileRowsMfma = 128;  // query rows per bf16 (matrix-core) attention work-group
+constexpr int kTileRowsMfma = 256;  // query rows per bf16 (matrix-core) attention work-group
 constexpr int kTileRowsF32 = 128;   // query rows per fp32 attention work-group
 constexpr int kMaxGroup = 128;      // largest Hq / Hkv
 constexpr int kMaxBlocksPerSeq = 4096;  // limit of the routing kernels' LDS tables
