@@ -154,6 +154,21 @@ struct ReadOff {
   int vq;
 };
 
+// Operand reads run kPre MFMAs ahead of their use: the first kPre LDS reads,
+// then one MFMA and one read alternately, then the last kPre MFMAs (pinned
+// with scheduling groups, so the LDS latency hides behind the matrix core).
+constexpr int kPre = 6;
+
+__device__ __forceinline__ void pin_pipeline() {
+  __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
+#pragma unroll
+  for (int j = 0; j < 16 - kPre; j++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
+}
+
 // S^T: 16 MFMAs from the K buffer at kb.
 __device__ __forceinline__ void qk(f32x16 (&s)[2], const u32x4* kb, const ReadOff& ro,
                                    const bf16x8 (&qf)[8]) {
@@ -162,22 +177,24 @@ __device__ __forceinline__ void qk(f32x16 (&s)[2], const u32x4* kb, const ReadOf
 #pragma unroll
     for (int r = 0; r < 16; r++) s[th][r] = 0.0f;
   const u32x4* k = kb + ro.kq;
+  u32x4 op[16];
 #pragma unroll
-  for (int kk = 0; kk < 8; kk++)
+  for (int j = 0; j < 16; j++) op[j] = k[32 * kRowK * (j & 1) + 2 * (j >> 1)];
 #pragma unroll
-    for (int th = 0; th < 2; th++)
-      s[th] = mfma(as_bf16x8(k[32 * kRowK * th + 2 * kk]), qf[kk], s[th]);
+  for (int j = 0; j < 16; j++) s[j & 1] = mfma(as_bf16x8(op[j]), qf[j >> 1], s[j & 1]);
+  pin_pipeline();
 }
 
 // O^T += V^T . P^T: 16 MFMAs from the V^T buffer at vb.
 __device__ __forceinline__ void pv(f32x16 (&o)[4], const u32x4* vb, const ReadOff& ro,
                                    const bf16x8 (&pb)[4]) {
   const u32x4* v = vb + ro.vq;
+  u32x4 op[16];
 #pragma unroll
-  for (int st = 0; st < 4; st++)
+  for (int j = 0; j < 16; j++) op[j] = v[32 * kRowV * (j & 3) + 2 * (j >> 2)];
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++)
-      o[dt] = mfma(as_bf16x8(v[32 * kRowV * dt + 2 * st]), pb[st], o[dt]);
+  for (int j = 0; j < 16; j++) o[j & 3] = mfma(as_bf16x8(op[j]), pb[j >> 2], o[j & 3]);
+  pin_pipeline();
 }
 
 struct RowInfo {
