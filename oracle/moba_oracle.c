@@ -162,7 +162,9 @@ static int cmp_int(const void* a, const void* b) {
 /*
  * Gate (Eq. 5 and Eq. 6; Alg. 1 S = Q Kbar^T, causal mask, topk) for the
  * listed rows (row id r = t * Hq + h; rows == NULL means all T * Hq rows in
- * order).  For a query in local block c of its sequence:
+ * order).  q is [T, Hq, D], or with q_compact the listed rows' query vectors
+ * only, [nrows, D] in list order (for problems too large to copy whole).
+ * For a query in local block c of its sequence:
  *   - candidates are the past blocks j < c (future blocks get s = -inf and
  *     g = 0, and block c itself is forced on rather than scored);
  *   - the current block occupies one of the k places, so at most k - 1
@@ -175,9 +177,10 @@ static int cmp_int(const void* a, const void* b) {
 int moba_oracle_select(const void* q, int dtype, int64_t T, int Hq, int Hkv, int D,
                        const int32_t* cu, int S, int B, int topk, const double* kbar,
                        const int64_t* rows, int64_t nrows, int32_t* sel,
-                       double* scores, int64_t nmax) {
+                       double* scores, int64_t nmax, int q_compact) {
   if (check_common(T, Hq, Hkv, D, cu, S) != ORC_OK || B < 1 || topk < 1 || !kbar || !sel)
     return ORC_EARG;
+  if (q_compact && !rows) return ORC_EARG;
   if (!rows) nrows = T * Hq;
   int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (S + 1));
   if (!off) return ORC_ENOMEM;
@@ -197,6 +200,7 @@ int moba_oracle_select(const void* q, int dtype, int64_t T, int Hq, int Hkv, int
       int s = seq_of(cu, S, t);
       int64_t tau = t - cu[s];
       int c = (int)(tau / B);
+      int64_t qoff = q_compact ? i * D : (t * Hq + h) * D;
       if (c > cap) {
         free(cand);
         cap = c;
@@ -211,7 +215,7 @@ int moba_oracle_select(const void* q, int dtype, int64_t T, int Hq, int Hkv, int
       for (int j = 0; j < c; j++) {
         const double* kb = kbar + ((off[s] + j) * Hkv + g) * D;
         double acc = 0.0;
-        for (int d = 0; d < D; d++) acc += elem(q, dtype, (t * Hq + h) * D + d) * kb[d];
+        for (int d = 0; d < D; d++) acc += elem(q, dtype, qoff + d) * kb[d];
         cand[j].s = acc;
         cand[j].j = j;
         if (scores && j < nmax) scores[i * nmax + j] = acc;
@@ -232,16 +236,16 @@ int moba_oracle_select(const void* q, int dtype, int64_t T, int Hq, int Hkv, int
  * Softmax attention of one query row over an explicit key list (Eq. 2),
  * two-pass: max, then normalised weights.  out[D] and *lse in fp64.
  */
-static void attend_keys(const void* q, const void* k, const void* v, int dtype, int Hq,
-                        int Hkv, int D, int64_t t, int h, int g, const int64_t* keys,
-                        int64_t nk, double* z, double* out, double* lse) {
+static void attend_keys(const void* q, const void* k, const void* v, int dtype, int Hkv,
+                        int D, int64_t qoff, int g, const int64_t* keys, int64_t nk, double* z,
+                        double* out, double* lse) {
   double scale = 1.0 / sqrt((double)D);
   double m = -INFINITY;
   for (int64_t x = 0; x < nk; x++) {
     int64_t u = keys[x];
     double acc = 0.0;
     for (int d = 0; d < D; d++)
-      acc += elem(q, dtype, (t * Hq + h) * D + d) * elem(k, dtype, (u * Hkv + g) * D + d);
+      acc += elem(q, dtype, qoff + d) * elem(k, dtype, (u * Hkv + g) * D + d);
     z[x] = scale * acc;
     if (z[x] > m) m = z[x];
   }
@@ -262,13 +266,15 @@ static void attend_keys(const void* q, const void* k, const void* v, int dtype, 
  * padded), the keys are every token of each selected block j < c, plus the
  * tokens of the current block c up to and including the query itself (the
  * causal mask inside the current block).  Outputs out[nrows, D], lse[nrows].
+ * q as in moba_oracle_select (q_compact: the listed rows only).
  */
 int moba_oracle_attend(const void* q, const void* k, const void* v, int dtype, int64_t T,
                        int Hq, int Hkv, int D, const int32_t* cu, int S, int B, int topk,
                        const int32_t* sel, const int64_t* rows, int64_t nrows, double* out,
-                       double* lse) {
+                       double* lse, int q_compact) {
   if (check_common(T, Hq, Hkv, D, cu, S) != ORC_OK || B < 1 || topk < 1 || !sel || !out || !lse)
     return ORC_EARG;
+  if (q_compact && !rows) return ORC_EARG;
   if (!rows) nrows = T * Hq;
   int G = Hq / Hkv;
   int fail = 0;
@@ -305,7 +311,8 @@ int moba_oracle_attend(const void* q, const void* k, const void* v, int dtype, i
         int64_t u1 = (j == c) ? tau + 1 : ((j + 1) * B < L ? (j + 1) * B : L);
         for (int64_t u = u0; u < u1; u++) keys[nk++] = cu[s] + u;
       }
-      attend_keys(q, k, v, dtype, Hq, Hkv, D, t, h, g, keys, nk, z, out + i * D, lse + i);
+      int64_t qoff = q_compact ? i * D : (t * Hq + h) * D;
+      attend_keys(q, k, v, dtype, Hkv, D, qoff, g, keys, nk, z, out + i * D, lse + i);
     }
     free(keys);
     free(z);
@@ -343,7 +350,8 @@ int moba_oracle_dense(const void* q, const void* k, const void* v, int dtype, in
       }
       if (!keys) continue;
       for (int64_t x = 0; x < nk; x++) keys[x] = cu[s] + x;
-      attend_keys(q, k, v, dtype, Hq, Hkv, D, t, h, h / G, keys, nk, z, out + i * D, lse + i);
+      attend_keys(q, k, v, dtype, Hkv, D, (t * Hq + h) * D, h / G, keys, nk, z, out + i * D,
+                  lse + i);
     }
     free(keys);
     free(z);

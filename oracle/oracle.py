@@ -53,9 +53,9 @@ def _load():
         vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
         lib.moba_oracle_pool.argtypes = [vp, i32, i64, i32, i32, vp, i32, i32, vp, vp]
         lib.moba_oracle_select.argtypes = [vp, i32, i64, i32, i32, i32, vp, i32, i32, i32, vp,
-                                           vp, i64, vp, vp, i64]
+                                           vp, i64, vp, vp, i64, i32]
         lib.moba_oracle_attend.argtypes = [vp, vp, vp, i32, i64, i32, i32, i32, vp, i32, i32,
-                                           i32, vp, vp, i64, vp, vp]
+                                           i32, vp, vp, i64, vp, vp, i32]
         lib.moba_oracle_dense.argtypes = [vp, vp, vp, i32, i64, i32, i32, i32, vp, i32, vp,
                                           i64, vp, vp]
         lib.moba_oracle_num_blocks.argtypes = [vp, i32, i32]
@@ -137,9 +137,27 @@ def select(q: np.ndarray, kbar: np.ndarray, cu, block_size: int, topk: int, rows
     kbar = np.ascontiguousarray(kbar, dtype=np.float64)
     _check(_load().moba_oracle_select(q.ctypes.data, dt, T, Hq, Hkv, D, cu.ctypes.data,
                                       cu.size - 1, int(block_size), int(topk), kbar.ctypes.data,
-                                      _ptr(rows), nr, sel.ctypes.data, _ptr(sc), int(nmax)),
+                                      _ptr(rows), nr, sel.ctypes.data, _ptr(sc), int(nmax), 0),
            "select")
     return (sel, sc) if nmax > 0 else sel
+
+
+def select_rows(q_rows: np.ndarray, T: int, Hq: int, kbar: np.ndarray, cu, block_size: int,
+                topk: int, rows):
+    """select() for the listed rows given only their query vectors q_rows
+    [nrows, D] (in the order of rows) of a [T, Hq, D] problem."""
+    q, dt = _elems(q_rows)
+    D = q.shape[-1]
+    Hkv = kbar.shape[1]
+    cu = _cu(cu)
+    rows, nr = _rows(rows)
+    assert rows is not None and q.reshape(-1, D).shape[0] == nr
+    sel = np.empty((nr, topk), np.int32)
+    kbar = np.ascontiguousarray(kbar, dtype=np.float64)
+    _check(_load().moba_oracle_select(q.ctypes.data, dt, int(T), int(Hq), Hkv, D, cu.ctypes.data,
+                                      cu.size - 1, int(block_size), int(topk), kbar.ctypes.data,
+                                      _ptr(rows), nr, sel.ctypes.data, None, 0, 1), "select")
+    return sel
 
 
 def attend(q, k, v, cu, block_size: int, sel: np.ndarray, rows=None):
@@ -162,7 +180,29 @@ def attend(q, k, v, cu, block_size: int, sel: np.ndarray, rows=None):
     _check(_load().moba_oracle_attend(q.ctypes.data, k.ctypes.data, v.ctypes.data, dt, T, Hq,
                                       Hkv, D, cu.ctypes.data, cu.size - 1, int(block_size),
                                       sel.shape[1], sel.ctypes.data, _ptr(rows), nr,
-                                      out.ctypes.data, lse.ctypes.data), "attend")
+                                      out.ctypes.data, lse.ctypes.data, 0), "attend")
+    return out, lse
+
+
+def attend_rows(q_rows, T: int, Hq: int, k, v, cu, block_size: int, sel: np.ndarray, rows):
+    """attend() for the listed rows given only their query vectors q_rows
+    [nrows, D] (in the order of rows) of a [T, Hq, D] problem."""
+    q, dt = _elems(q_rows)
+    k, dtk = _elems(k)
+    v, dtv = _elems(v)
+    assert dt == dtk == dtv
+    D = q.shape[-1]
+    Hkv = k.shape[1]
+    cu = _cu(cu)
+    rows, nr = _rows(rows)
+    assert rows is not None and q.reshape(-1, D).shape[0] == nr
+    sel = np.ascontiguousarray(sel, dtype=np.int32).reshape(nr, -1)
+    out = np.empty((nr, D), np.float64)
+    lse = np.empty((nr,), np.float64)
+    _check(_load().moba_oracle_attend(q.ctypes.data, k.ctypes.data, v.ctypes.data, dt, int(T),
+                                      int(Hq), Hkv, D, cu.ctypes.data, cu.size - 1,
+                                      int(block_size), sel.shape[1], sel.ctypes.data, _ptr(rows),
+                                      nr, out.ctypes.data, lse.ctypes.data, 1), "attend")
     return out, lse
 
 

@@ -429,3 +429,20 @@ def test_tail_sparsity_matches_paper(case):
     nkeys = math.exp(lse[0])
     assert abs(nkeys - round(nkeys)) < 1e-6
     assert abs((1.0 - round(nkeys) / N) - case["sparsity"]) <= 5e-5
+
+
+def test_compact_query_rows_match_full_arrays():
+    """select_rows / attend_rows (only the listed rows' query vectors) give
+    bit-identical results to select / attend on the full query array."""
+    q, k, v, cu = inputs.make((700, 0, 333), 8, 2, 128, torch.bfloat16, 64, 0.5, 3)
+    qn, kn, vn = inputs.to_oracle(q), inputs.to_oracle(k), inputs.to_oracle(v)
+    cun = cu.numpy()
+    rows = np.array([0, 5, 100, 2000, 5555, 8000, 8263], dtype=np.int64)
+    kbar = oracle.pool(kn, cun, 64)
+    s_full = oracle.select(qn, kbar, cun, 64, 4, rows=rows)
+    q_rows = qn.reshape(-1, 128)[rows]
+    s_rows = oracle.select_rows(q_rows, q.shape[0], 8, kbar, cun, 64, 4, rows)
+    assert np.array_equal(s_full, s_rows)
+    o_full, l_full = oracle.attend(qn, kn, vn, cun, 64, s_full, rows=rows)
+    o_rows, l_rows = oracle.attend_rows(q_rows, q.shape[0], 8, kn, vn, cun, 64, s_rows, rows)
+    assert np.array_equal(o_full, o_rows) and np.array_equal(l_full, l_rows)
