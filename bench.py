@@ -1,6 +1,7 @@
 """Benchmark of the MoBA causal prefill forward on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--dense-steps N] [--no-cpu]
+    python bench.py --sweep fig2a|fig2b [--sweep-steps K] [--sweep-lengths L1,L2,..]
 
 One step = one moba_forward call over the whole workload (pool, gate, route,
 history and current-block attention, merge), inputs resident in HBM.  The
@@ -155,6 +156,52 @@ def _cpu_model():
     return "unknown"
 
 
+def run_sweep(args):
+    """Length-scaling sweep (Fig. 2a or 2b): one JSON line per length with the
+    forward time, attended TFLOP/s and, up to --sweep-dense-max tokens, the
+    dense causal time and measured speedup; beyond it the dense time is
+    extrapolated at the rate of the largest measured dense point and
+    labelled as such."""
+    dev = torch.device("cuda:0")
+    lengths = inputs.SWEEP_LENGTHS[args.sweep]
+    if args.sweep_lengths:
+        keep = {int(x) for x in args.sweep_lengths.split(",")}
+        lengths = [L for L in lengths if L in keep]
+    dense_rate = None  # FLOP per ms of the largest measured dense point
+    for L in lengths:
+        w = inputs.sweep_workload(args.sweep, L)
+        print("[bench] sweep %s L=%d" % (args.sweep, L), file=sys.stderr, flush=True)
+        q, k, v, cu = inputs.make_workload(w, device=dev)
+        out = torch.empty_like(q)
+        lse = torch.empty((w.hq, L), dtype=torch.float32, device=dev)
+        step = lambda: binding.forward(q, k, v, cu, w.block_size, w.topk, out=out, lse=lse)
+        ms = time_steps(step, args.sweep_steps, 1)
+        cur, hist, _ = attended_keys(w.seqlens, w.block_size, w.topk)
+        flop = 4.0 * w.d * w.hq * (cur + hist)
+        dflop = 4.0 * w.d * w.hq * dense_keys(w.seqlens)
+        dense_ms, dense_kind = None, None
+        if L <= args.sweep_dense_max:
+            dense_ms = time_steps(lambda: binding.dense_forward(q, k, v, cu, out=out, lse=lse), 1,
+                                  1 if L <= 262144 else 0)
+            dense_kind = "measured"
+            dense_rate = dflop / dense_ms
+        elif dense_rate:
+            dense_ms = dflop / dense_rate
+            dense_kind = "extrapolated at the largest measured dense rate"
+        tflops = flop / (ms * 1e-3) / 1e12
+        print(json.dumps({
+            "sweep": args.sweep, "workload": w.name, "tokens": L, "block_size": w.block_size,
+            "topk": w.topk, "q_heads": w.hq, "kv_heads": w.hkv, "steps": args.sweep_steps,
+            "ms": round(ms, 3), "attended_flop": flop, "tflops": round(tflops, 2),
+            "pct_bf16_peak": round(100.0 * tflops / BF16_PEAK_TFLOPS, 2),
+            "dense_flop": dflop, "flop_ratio": round(dflop / flop, 3),
+            "dense_ms": None if dense_ms is None else round(dense_ms, 2), "dense": dense_kind,
+            "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 3),
+        }), flush=True)
+        del q, k, v, out, lse
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -164,6 +211,12 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=1)
     ap.add_argument("--cpu-rows", type=int, default=12000)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sweep", choices=sorted(inputs.SWEEP_LENGTHS),
+                    help="length-scaling sweep instead of the headline line (one JSON line "
+                         "per length)")
+    ap.add_argument("--sweep-steps", type=int, default=2)
+    ap.add_argument("--sweep-lengths", default=None, help="comma-separated subset of lengths")
+    ap.add_argument("--sweep-dense-max", type=int, default=1 << 20)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -173,8 +226,11 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
 
-    w = inputs.WORKLOADS[args.workload]
     binding.load()
+    if args.sweep:
+        run_sweep(args)
+        return
+    w = inputs.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     print("[bench] generating %s" % w.name, file=sys.stderr, flush=True)
     q, k, v, cu = inputs.make_workload(w, device=dev)

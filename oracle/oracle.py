@@ -143,9 +143,10 @@ def select(q: np.ndarray, kbar: np.ndarray, cu, block_size: int, topk: int, rows
 
 
 def select_rows(q_rows: np.ndarray, T: int, Hq: int, kbar: np.ndarray, cu, block_size: int,
-                topk: int, rows):
+                topk: int, rows, nmax: int = 0):
     """select() for the listed rows given only their query vectors q_rows
-    [nrows, D] (in the order of rows) of a [T, Hq, D] problem."""
+    [nrows, D] (in the order of rows) of a [T, Hq, D] problem; with nmax > 0
+    also the scores, as in select()."""
     q, dt = _elems(q_rows)
     D = q.shape[-1]
     Hkv = kbar.shape[1]
@@ -153,11 +154,13 @@ def select_rows(q_rows: np.ndarray, T: int, Hq: int, kbar: np.ndarray, cu, block
     rows, nr = _rows(rows)
     assert rows is not None and q.reshape(-1, D).shape[0] == nr
     sel = np.empty((nr, topk), np.int32)
+    sc = np.empty((nr, nmax), np.float64) if nmax > 0 else None
     kbar = np.ascontiguousarray(kbar, dtype=np.float64)
     _check(_load().moba_oracle_select(q.ctypes.data, dt, int(T), int(Hq), Hkv, D, cu.ctypes.data,
                                       cu.size - 1, int(block_size), int(topk), kbar.ctypes.data,
-                                      _ptr(rows), nr, sel.ctypes.data, None, 0, 1), "select")
-    return sel
+                                      _ptr(rows), nr, sel.ctypes.data, _ptr(sc), int(nmax), 1),
+           "select")
+    return (sel, sc) if nmax > 0 else sel
 
 
 def attend(q, k, v, cu, block_size: int, sel: np.ndarray, rows=None):

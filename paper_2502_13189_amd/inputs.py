@@ -112,7 +112,72 @@ def make(seqlens, hq: int, hkv: int, d: int, dtype, block_size: int, key_offset_
     return q, k, v, cu_seqlens(seqlens)
 
 
+def make_chunked(seqlens, hq: int, hkv: int, d: int, dtype, block_size: int,
+                 key_offset_std: float = 0.0, seed: int = 0, device="cpu",
+                 chunk_tokens: int = 1 << 18):
+    """Like make(), for prefills too long to draw in fp32 at once: the block
+    offsets come first from a generator seeded with `seed`; then the tokens
+    are drawn in chunks of chunk_tokens, chunk c from a generator seeded with
+    seed * 1000003 + c + 1 (Q, K, V of the chunk in that order, fp32), and
+    each chunk is rounded to `dtype` as it is written.  Defines its own
+    workloads: the values differ from make() for the same seed."""
+    seqlens = tuple(int(x) for x in seqlens)
+    T = sum(seqlens)
+    dev = torch.device(device)
+    q = torch.empty((T, hq, d), device=dev, dtype=dtype)
+    k = torch.empty((T, hkv, d), device=dev, dtype=dtype)
+    v = torch.empty((T, hkv, d), device=dev, dtype=dtype)
+    ids, nblk = _block_ids(seqlens, block_size)
+    off = None
+    if key_offset_std > 0.0 and T > 0:
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(int(seed))
+        off = torch.randn((nblk, hkv, d), generator=gen, device=dev, dtype=torch.float32)
+        off.mul_(float(key_offset_std))
+    for c, t0 in enumerate(range(0, T, chunk_tokens)):
+        t1 = min(T, t0 + chunk_tokens)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(int(seed) * 1000003 + c + 1)
+        qc = torch.randn((t1 - t0, hq, d), generator=gen, device=dev, dtype=torch.float32)
+        kc = torch.randn((t1 - t0, hkv, d), generator=gen, device=dev, dtype=torch.float32)
+        vc = torch.randn((t1 - t0, hkv, d), generator=gen, device=dev, dtype=torch.float32)
+        if off is not None:
+            kc.add_(off[ids[t0:t1].to(dev)])
+        q[t0:t1].copy_(qc)
+        k[t0:t1].copy_(kc)
+        v[t0:t1].copy_(vc)
+        del qc, kc, vc
+    return q, k, v, cu_seqlens(seqlens)
+
+
+# Length-scaling sweeps (Fig. 2), 32 query / 8 kv heads, D = 128, bf16, key
+# offsets N(0, 0.5^2), chunked generation:
+#   fig2a: 8K .. 1M tokens at block size 4096 and top-12 (the 1M model's
+#          setting);
+#   fig2b: 8K .. 10M tokens with 64 blocks per sequence (B = L / 64) and
+#          top-3, i.e. a fixed tail sparsity of 1 - 3/64 = 95.31%.
+SWEEP_LENGTHS = {
+    "fig2a": [8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576],
+    "fig2b": [8192, 32768, 131072, 524288, 1048576, 2097152, 4194304, 8388608, 10485760],
+}
+
+
+def sweep_workload(kind: str, L: int) -> Workload:
+    if kind == "fig2a":
+        B, k = 4096, 12
+    elif kind == "fig2b":
+        B, k = L // 64, 3
+    else:
+        raise ValueError(kind)
+    seed = 100 + SWEEP_LENGTHS[kind].index(L) + (0 if kind == "fig2a" else 50)
+    return Workload("bf16_L%d_gqa32x8_B%d_k%d_%s" % (L, B, k, kind), (L,), 32, 8, 128, "bf16", B,
+                    k, 0.5, seed, "length sweep %s" % kind)
+
+
 def make_workload(w: Workload, device="cpu"):
+    if w.name.endswith("_fig2a") or w.name.endswith("_fig2b"):
+        return make_chunked(w.seqlens, w.hq, w.hkv, w.d, w.torch_dtype, w.block_size,
+                            w.key_offset_std, w.seed, device)
     return make(w.seqlens, w.hq, w.hkv, w.d, w.torch_dtype, w.block_size, w.key_offset_std,
                 w.seed, device)
 

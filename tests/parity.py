@@ -83,6 +83,41 @@ def check_selection(gpu_sel, rows, qn, kn, cu, B, topk, exact):
     return osel, bad
 
 
+def check_selection_rows(gpu_sel, rows, q_rows, T, Hq, kn, cu, B, topk, exact):
+    """check_selection() for problems too large to copy whole: q_rows holds
+    only the listed rows' query vectors [nrows, D] (list order)."""
+    cu = np.asarray(cu)
+    kbar, kabs = oracle.pool(kn, cu, B, with_abs=True)
+    osel = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows)
+    gsel = np.asarray(gpu_sel).reshape(len(rows), topk)
+    bad = np.nonzero((gsel != osel).any(axis=1))[0]
+    if exact:
+        assert bad.size == 0, "selection differs on %d rows, first rows %s" % (bad.size, rows[bad[:5]])
+        return osel, bad
+    if bad.size == 0:
+        return osel, bad
+    G = Hq // kn.shape[1]
+    nmax = int(max(osel.max(), gsel.max())) + 1
+    _, sc = oracle.select_rows(q_rows[bad], T, Hq, kbar, cu, B, topk, rows[bad], nmax=nmax)
+    boff = block_offsets(cu, B)
+    qf = np.abs(_widen(np.asarray(q_rows).reshape(len(rows), -1)))
+    for n, i in enumerate(bad):
+        r = int(rows[i])
+        t, h = r // Hq, r % Hq
+        g = h // G
+        s = int(seq_of_tokens(cu, t))
+        o_set = set(int(x) for x in osel[i] if x >= 0)
+        g_set = set(int(x) for x in gsel[i] if x >= 0)
+        assert len(o_set) == len(g_set) and max(o_set) == max(g_set), (r, o_set, g_set)
+        for jg in g_set - o_set:
+            for jo in o_set - g_set:
+                tau = TAU_SCALE * (qf[i] @ kabs[boff[s] + jg, g] + qf[i] @ kabs[boff[s] + jo, g])
+                gap = sc[n, jo] - sc[n, jg]
+                assert gap <= tau, ("row %d: GPU kept block %d over block %d, score gap %.3e > "
+                                    "tolerance %.3e" % (r, jg, jo, gap, tau))
+    return osel, bad
+
+
 def _widen(x):
     if x.dtype == np.uint16:
         return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
