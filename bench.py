@@ -1,7 +1,7 @@
 """Benchmark of the MoBA causal prefill forward on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--dense-steps N] [--no-cpu]
-    python bench.py --sweep fig2a|fig2b [--sweep-steps K] [--sweep-lengths L1,L2,..]
+    python bench.py --sweep fig2a|fig2b|gran [--sweep-steps K] [--sweep-lengths L1,L2,..]
 
 One step = one moba_forward call over the whole workload (pool, gate, route,
 history and current-block attention, merge), inputs resident in HBM.  The
@@ -157,20 +157,20 @@ def _cpu_model():
 
 
 def run_sweep(args):
-    """Length-scaling sweep (Fig. 2a or 2b): one JSON line per length with the
-    forward time, attended TFLOP/s and, up to --sweep-dense-max tokens, the
-    dense causal time and measured speedup; beyond it the dense time is
-    extrapolated at the rate of the largest measured dense point and
-    labelled as such."""
+    """A sweep (Fig. 2a or 2b lengths, or the block-granularity points): one
+    JSON line per point with the forward time, attended TFLOP/s and, up to
+    --sweep-dense-max tokens, the dense causal time and measured speedup;
+    beyond it the dense time is extrapolated at the rate of the largest
+    measured dense point and labelled as such."""
     dev = torch.device("cuda:0")
-    lengths = inputs.SWEEP_LENGTHS[args.sweep]
+    points = inputs.sweep_workloads(args.sweep)
     if args.sweep_lengths:
         keep = {int(x) for x in args.sweep_lengths.split(",")}
-        lengths = [L for L in lengths if L in keep]
+        points = [w for w in points if w.seqlens[0] in keep]
     dense_rate = None  # FLOP per ms of the largest measured dense point
-    for L in lengths:
-        w = inputs.sweep_workload(args.sweep, L)
-        print("[bench] sweep %s L=%d" % (args.sweep, L), file=sys.stderr, flush=True)
+    for w in points:
+        L = w.seqlens[0]
+        print("[bench] sweep %s %s" % (args.sweep, w.name), file=sys.stderr, flush=True)
         q, k, v, cu = inputs.make_workload(w, device=dev)
         out = torch.empty_like(q)
         lse = torch.empty((w.hq, L), dtype=torch.float32, device=dev)
@@ -211,7 +211,7 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=1)
     ap.add_argument("--cpu-rows", type=int, default=12000)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--sweep", choices=sorted(inputs.SWEEP_LENGTHS),
+    ap.add_argument("--sweep", choices=sorted(inputs.SWEEP_POINTS),
                     help="length-scaling sweep instead of the headline line (one JSON line "
                          "per length)")
     ap.add_argument("--sweep-steps", type=int, default=2)

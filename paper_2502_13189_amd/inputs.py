@@ -150,32 +150,43 @@ def make_chunked(seqlens, hq: int, hkv: int, d: int, dtype, block_size: int,
     return q, k, v, cu_seqlens(seqlens)
 
 
-# Length-scaling sweeps (Fig. 2), 32 query / 8 kv heads, D = 128, bf16, key
-# offsets N(0, 0.5^2), chunked generation:
+# Sweeps, 32 query / 8 kv heads, D = 128, bf16, key offsets N(0, 0.5^2),
+# chunked generation; points are (tokens, block size, top-k):
 #   fig2a: 8K .. 1M tokens at block size 4096 and top-12 (the 1M model's
-#          setting);
+#          setting, Fig. 2a);
 #   fig2b: 8K .. 10M tokens with 64 blocks per sequence (B = L / 64) and
-#          top-3, i.e. a fixed tail sparsity of 1 - 3/64 = 95.31%.
-SWEEP_LENGTHS = {
-    "fig2a": [8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576],
-    "fig2b": [8192, 32768, 131072, 524288, 1048576, 2097152, 4194304, 8388608, 10485760],
+#          top-3, a fixed tail sparsity of 1 - 3/64 = 95.31% (Fig. 2b);
+#   gran:  32K tokens at a fixed tail sparsity of 75% with finer and finer
+#          blocks, (B, k) = (4096, 2) .. (256, 32) (the block-granularity
+#          ablation of Sec. 3.1).
+SWEEP_POINTS = {
+    "fig2a": [(L, 4096, 12) for L in (8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576)],
+    "fig2b": [(L, L // 64, 3) for L in (8192, 32768, 131072, 524288, 1048576, 2097152, 4194304,
+                                          8388608, 10485760)],
+    "gran": [(32768, 4096, 2), (32768, 2048, 4), (32768, 1024, 8), (32768, 512, 16),
+             (32768, 256, 32)],
 }
 
 
-def sweep_workload(kind: str, L: int) -> Workload:
-    if kind == "fig2a":
-        B, k = 4096, 12
-    elif kind == "fig2b":
-        B, k = L // 64, 3
-    else:
-        raise ValueError(kind)
-    seed = 100 + SWEEP_LENGTHS[kind].index(L) + (0 if kind == "fig2a" else 50)
-    return Workload("bf16_L%d_gqa32x8_B%d_k%d_%s" % (L, B, k, kind), (L,), 32, 8, 128, "bf16", B,
-                    k, 0.5, seed, "length sweep %s" % kind)
+def sweep_workload(kind: str, L: int, B: int = None, k: int = None) -> Workload:
+    """The sweep point of `kind` with L tokens (and, for gran, block size B)."""
+    pts = SWEEP_POINTS[kind]
+    idx = [i for i, (l, b, kk) in enumerate(pts) if l == L and (B is None or b == B)]
+    if not idx:
+        raise ValueError((kind, L, B))
+    i = idx[0]
+    L, B, k = pts[i]
+    seed = 100 + i + {"fig2a": 0, "fig2b": 50, "gran": 80}[kind]
+    return Workload("bf16_L%d_gqa32x8_B%d_k%d_%s" % (L, B, k, kind), (L,), 32, 8, 128, "bf16", B, k,
+                    0.5, seed, "sweep %s" % kind)
+
+
+def sweep_workloads(kind: str):
+    return [sweep_workload(kind, L, B) for (L, B, _) in SWEEP_POINTS[kind]]
 
 
 def make_workload(w: Workload, device="cpu"):
-    if w.name.endswith("_fig2a") or w.name.endswith("_fig2b"):
+    if w.name.rsplit("_", 1)[-1] in SWEEP_POINTS:
         return make_chunked(w.seqlens, w.hq, w.hkv, w.d, w.torch_dtype, w.block_size,
                             w.key_offset_std, w.seed, device)
     return make(w.seqlens, w.hq, w.hkv, w.d, w.torch_dtype, w.block_size, w.key_offset_std,

@@ -1,7 +1,8 @@
-"""Parity along the length-scaling sweeps (Fig. 2a: block size 4096, top-12,
-8K to 1M tokens; Fig. 2b: 64 blocks per sequence, top-3, 8K to 10M tokens;
+"""Parity along the sweeps (Fig. 2a: block size 4096, top-12, 8K to 1M
+tokens; Fig. 2b: 64 blocks per sequence, top-3, 8K to 10M tokens; block
+granularity: 32K tokens at 75% sparsity, (B, k) = (4096, 2) .. (256, 32);
 32 query / 8 kv heads, bf16), in the launch configuration the sweep times
-(one moba_forward call per length).
+(one moba_forward call per point).
 
 Per length: the selection invariants on every row (on the GPU, token chunk by
 token chunk); the tie-aware selection and the outputs on a sample of rows
@@ -24,9 +25,10 @@ import parity
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
-CASES = [("fig2a", L) for L in (8192, 32768, 131072, 524288)] + \
-        [("fig2b", L) for L in (8192, 131072, 1048576, 2097152)]
-LARGE = [("fig2b", L) for L in (4194304, 8388608, 10485760)]
+CASES = [("fig2a", L, 4096) for L in (8192, 32768, 131072, 524288)] + \
+        [("fig2b", L, L // 64) for L in (8192, 131072, 1048576, 2097152)] + \
+        [("gran", 32768, B) for B in (4096, 2048, 1024, 512, 256)]
+LARGE = [("fig2b", L, L // 64) for L in (4194304, 8388608, 10485760)]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -69,8 +71,8 @@ def selection_invariants_chunked(sel, B, topk, chunk=1 << 18):
         assert bool(((s == -1) | ~(idx > nh[..., None])).all())
 
 
-def run_sweep_point(kind, L):
-    w = inputs.sweep_workload(kind, L)
+def run_sweep_point(kind, L, B):
+    w = inputs.sweep_workload(kind, L, B)
     print("[sweep] %s: generating" % w.name, flush=True)
     q, k, v, cu = inputs.make_workload(w, device=DEV)
     print("[sweep] %s: forward and selection on the GPU" % w.name, flush=True)
@@ -100,13 +102,13 @@ def run_sweep_point(kind, L):
           % (w.name, len(rows), len(bad), mx, mean, lmx))
 
 
-@pytest.mark.parametrize("kind,L", CASES, ids=["%s_L%d" % c for c in CASES])
-def test_sweep_parity(kind, L):
-    run_sweep_point(kind, L)
+@pytest.mark.parametrize("kind,L,B", CASES, ids=["%s_L%d_B%d" % c for c in CASES])
+def test_sweep_parity(kind, L, B):
+    run_sweep_point(kind, L, B)
 
 
 @pytest.mark.skipif(os.environ.get("MOBA_LARGE_SWEEP") != "1",
                     reason="multi-million-token sweep points run with MOBA_LARGE_SWEEP=1")
-@pytest.mark.parametrize("kind,L", LARGE, ids=["%s_L%d" % c for c in LARGE])
-def test_sweep_parity_large(kind, L):
-    run_sweep_point(kind, L)
+@pytest.mark.parametrize("kind,L,B", LARGE, ids=["%s_L%d_B%d" % c for c in LARGE])
+def test_sweep_parity_large(kind, L, B):
+    run_sweep_point(kind, L, B)
