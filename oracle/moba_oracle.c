@@ -20,6 +20,8 @@
  *   attend  : softmax over the union of the selected blocks,         (Eq. 2 and Eq. 4)
  *             causal inside the current block                        (Sec. 2.2, "Current Block Attention")
  *   dense   : causal softmax attention over the whole prefix         (Eq. 1)
+ *   backward: gradients of attend w.r.t. q, k, v for a fixed         (chain rule through Eq. 2;
+ *             selection (the hard gate passes no gradient)            Eq. 3 and Eq. 5 are 0/1)
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *   - logit scale 1/sqrt(d) in the attention softmax (Eq. 1/2 print none; it
@@ -37,7 +39,9 @@
  * Parity of every function here is pinned by the CPU test suite (dense
  * equivalence at top-k >= #blocks, per-block causal attention at top-k = 1,
  * brute-force subset enumeration, constructed ties, invariances, the paper's
- * tail-sparsity figures).
+ * tail-sparsity figures; for the backward: fp64 autograd of causal attention
+ * in the dense and top-1 special cases, finite differences of attend, a closed
+ * form, and the sum identities of softmax-attention gradients).
  */
 #include <math.h>
 #include <stdint.h>
@@ -317,6 +321,171 @@ int moba_oracle_attend(const void* q, const void* k, const void* v, int dtype, i
     free(keys);
     free(z);
   }
+  return fail ? ORC_EARG : ORC_OK;
+}
+
+/*
+ * Gradients of MoBA attention given a block selection: the chain rule
+ * through Eq. 2 over the key set of Eq. 4.  The gate is a hard 0/1 choice
+ * (Eq. 3 and Eq. 5), so no gradient flows into the block keys or the gate
+ * scores; only the attention over the selected keys is differentiated.
+ *
+ * For each listed row (t, h) with key set U (as in moba_oracle_attend),
+ * logits z_u = <q, k_u> / sqrt(D), weights p_u = exp(z_u) / sum_w exp(z_w),
+ * output o = sum_u p_u v_u, and upstream gradient go = dout[t, h]:
+ *   dp_u = <go, v_u>                      (gradient of o w.r.t. p_u)
+ *   dz_u = p_u (dp_u - sum_w p_w dp_w)    (softmax Jacobian)
+ *   dq   = sum_u dz_u k_u / sqrt(D)
+ *   dk_u += dz_u q / sqrt(D)
+ *   dv_u += p_u go
+ * q and dout are [T, Hq, D], or with q_compact the listed rows only,
+ * [nrows, D] in list order.  dq [nrows, D] (nullable).  dk and dv (nullable,
+ * both or neither) receive the listed rows' contributions to the keys of
+ * tokens kv_lo <= u < kv_hi, as [(kv_hi - kv_lo), Hkv, D]; the contributions
+ * to a kv-head sum over the query heads of its group.  Each thread
+ * accumulates into private dk/dv arrays, added up in thread order at the end.
+ */
+static void backward_row(const void* q, const void* k, const void* v, const void* dout,
+                         int dtype, int Hkv, int D, int64_t qoff, int g, const int64_t* keys,
+                         int64_t nk, double* z, double* dpv, double* dq, int64_t kv_lo,
+                         int64_t kv_hi, double* dk, double* dv) {
+  double scale = 1.0 / sqrt((double)D);
+  double m = -INFINITY;
+  for (int64_t x = 0; x < nk; x++) {
+    int64_t u = keys[x];
+    double acc = 0.0;
+    for (int d = 0; d < D; d++)
+      acc += elem(q, dtype, qoff + d) * elem(k, dtype, (u * Hkv + g) * D + d);
+    z[x] = scale * acc;
+    if (z[x] > m) m = z[x];
+  }
+  double l = 0.0;
+  for (int64_t x = 0; x < nk; x++) l += exp(z[x] - m);
+  /* z[x] becomes p_u, dpv[x] becomes dp_u; then sum_w p_w dp_w */
+  double pdp = 0.0;
+  for (int64_t x = 0; x < nk; x++) {
+    int64_t u = keys[x];
+    z[x] = exp(z[x] - m) / l;
+    double acc = 0.0;
+    for (int d = 0; d < D; d++)
+      acc += elem(dout, dtype, qoff + d) * elem(v, dtype, (u * Hkv + g) * D + d);
+    dpv[x] = acc;
+    pdp += z[x] * acc;
+  }
+  if (dq)
+    for (int d = 0; d < D; d++) dq[d] = 0.0;
+  for (int64_t x = 0; x < nk; x++) {
+    int64_t u = keys[x];
+    double dz = z[x] * (dpv[x] - pdp);
+    if (dq)
+      for (int d = 0; d < D; d++) dq[d] += dz * scale * elem(k, dtype, (u * Hkv + g) * D + d);
+    if (dk && u >= kv_lo && u < kv_hi) {
+      double* dkr = dk + ((u - kv_lo) * Hkv + g) * D;
+      double* dvr = dv + ((u - kv_lo) * Hkv + g) * D;
+      for (int d = 0; d < D; d++) {
+        dkr[d] += dz * scale * elem(q, dtype, qoff + d);
+        dvr[d] += z[x] * elem(dout, dtype, qoff + d);
+      }
+    }
+  }
+}
+
+int moba_oracle_attend_backward(const void* q, const void* k, const void* v, const void* dout,
+                                int dtype, int64_t T, int Hq, int Hkv, int D, const int32_t* cu,
+                                int S, int B, int topk, const int32_t* sel, const int64_t* rows,
+                                int64_t nrows, int q_compact, double* dq, int64_t kv_lo,
+                                int64_t kv_hi, double* dk, double* dv) {
+  if (check_common(T, Hq, Hkv, D, cu, S) != ORC_OK || B < 1 || topk < 1 || !sel || !dout)
+    return ORC_EARG;
+  if (q_compact && !rows) return ORC_EARG;
+  if ((dk == NULL) != (dv == NULL)) return ORC_EARG;
+  if (dk && (kv_lo < 0 || kv_hi > T || kv_lo > kv_hi)) return ORC_EARG;
+  if (!rows) nrows = T * Hq;
+  int G = Hq / Hkv;
+  int64_t nkv = dk ? (kv_hi - kv_lo) * Hkv * D : 0;
+  if (dk) {
+    memset(dk, 0, sizeof(double) * (size_t)nkv);
+    memset(dv, 0, sizeof(double) * (size_t)nkv);
+  }
+  int nthr = 1;
+#ifdef _OPENMP
+  nthr = omp_get_max_threads();
+#endif
+  double** pdk = (double**)calloc((size_t)nthr, sizeof(double*));
+  double** pdv = (double**)calloc((size_t)nthr, sizeof(double*));
+  if (!pdk || !pdv) { free(pdk); free(pdv); return ORC_ENOMEM; }
+  int fail = 0;
+#pragma omp parallel num_threads(nthr)
+  {
+    int me = 0;
+#ifdef _OPENMP
+    me = omp_get_thread_num();
+#endif
+    double* mydk = NULL;
+    double* mydv = NULL;
+    if (dk) {
+      mydk = (double*)calloc((size_t)nkv > 0 ? (size_t)nkv : 1, sizeof(double));
+      mydv = (double*)calloc((size_t)nkv > 0 ? (size_t)nkv : 1, sizeof(double));
+      if (!mydk || !mydv) fail = 1;
+    }
+    pdk[me] = mydk;
+    pdv[me] = mydv;
+    int64_t cap = 0;
+    int64_t* keys = NULL;
+    double* z = NULL;
+    double* dpv = NULL;
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t i = 0; i < nrows; i++) {
+      if (dk && (!mydk || !mydv)) continue;
+      int64_t r = rows ? rows[i] : i;
+      int64_t t = r / Hq;
+      int h = (int)(r % Hq);
+      int g = h / G;
+      int s = seq_of(cu, S, t);
+      int64_t L = (int64_t)cu[s + 1] - cu[s];
+      int64_t tau = t - cu[s];
+      int64_t c = tau / B;
+      int64_t need = (int64_t)topk * B;
+      if (need > cap) {
+        free(keys); free(z); free(dpv);
+        cap = need;
+        keys = (int64_t*)malloc(sizeof(int64_t) * cap);
+        z = (double*)malloc(sizeof(double) * cap);
+        dpv = (double*)malloc(sizeof(double) * cap);
+        if (!keys || !z || !dpv) {
+          fail = 1; cap = 0; free(keys); free(z); free(dpv); keys = NULL; z = NULL; dpv = NULL;
+        }
+      }
+      if (!keys) continue;
+      int64_t nk = 0;
+      for (int x = 0; x < topk; x++) {
+        int64_t j = sel[i * topk + x];
+        if (j < 0) continue;
+        if (j > c) { fail = 1; continue; } /* future block: never valid */
+        int64_t u0 = j * B;
+        int64_t u1 = (j == c) ? tau + 1 : ((j + 1) * B < L ? (j + 1) * B : L);
+        for (int64_t u = u0; u < u1; u++) keys[nk++] = cu[s] + u;
+      }
+      int64_t qoff = q_compact ? i * D : (t * Hq + h) * D;
+      backward_row(q, k, v, dout, dtype, Hkv, D, qoff, g, keys, nk, z, dpv,
+                   dq ? dq + i * D : NULL, kv_lo, kv_hi, mydk, mydv);
+    }
+    free(keys);
+    free(z);
+    free(dpv);
+  }
+  if (dk && !fail) {
+    for (int th = 0; th < nthr; th++) {
+      if (!pdk[th]) continue;
+      for (int64_t x = 0; x < nkv; x++) {
+        dk[x] += pdk[th][x];
+        dv[x] += pdv[th][x];
+      }
+    }
+  }
+  for (int th = 0; th < nthr; th++) { free(pdk[th]); free(pdv[th]); }
+  free(pdk);
+  free(pdv);
   return fail ? ORC_EARG : ORC_OK;
 }
 

@@ -18,6 +18,8 @@ Functions and the passages they follow (Method section of the paper):
              (Eq. 2, Eq. 4)
   dense   -- causal softmax attention (Eq. 1)
   forward -- pool, select, attend
+  attend_backward -- gradients of attend w.r.t. q, k, v for a fixed selection
+             (chain rule through Eq. 2; the hard gate of Eq. 3/5 passes none)
 """
 from __future__ import annotations
 
@@ -56,6 +58,9 @@ def _load():
                                            vp, i64, vp, vp, i64, i32]
         lib.moba_oracle_attend.argtypes = [vp, vp, vp, i32, i64, i32, i32, i32, vp, i32, i32,
                                            i32, vp, vp, i64, vp, vp, i32]
+        lib.moba_oracle_attend_backward.argtypes = [vp, vp, vp, vp, i32, i64, i32, i32, i32,
+                                                    vp, i32, i32, i32, vp, vp, i64, i32, vp,
+                                                    i64, i64, vp, vp]
         lib.moba_oracle_dense.argtypes = [vp, vp, vp, i32, i64, i32, i32, i32, vp, i32, vp,
                                           i64, vp, vp]
         lib.moba_oracle_num_blocks.argtypes = [vp, i32, i32]
@@ -207,6 +212,50 @@ def attend_rows(q_rows, T: int, Hq: int, k, v, cu, block_size: int, sel: np.ndar
                                       int(block_size), sel.shape[1], sel.ctypes.data, _ptr(rows),
                                       nr, out.ctypes.data, lse.ctypes.data, 1), "attend")
     return out, lse
+
+
+def attend_backward(q, k, v, dout, cu, block_size: int, sel: np.ndarray, rows=None,
+                    shape=None, want_dq: bool = True, kv_window=None):
+    """Gradients of attend() for a fixed selection sel [nrows, topk].
+
+    Returns (dq, dk, dv): dq [nrows, D] fp64 (None unless want_dq); dk, dv
+    [(hi - lo), Hkv, D] fp64 over the token window kv_window = (lo, hi)
+    (None: no dk/dv; "all": every token), holding the listed rows'
+    contributions.  With shape = (T, Hq), q and dout hold the listed rows'
+    vectors only, [nrows, D] in list order."""
+    q, dt = _elems(q)
+    k, dtk = _elems(k)
+    v, dtv = _elems(v)
+    dout, dto = _elems(dout)
+    assert dt == dtk == dtv == dto
+    D = q.shape[-1]
+    Hkv = k.shape[1]
+    compact = shape is not None
+    if compact:
+        T, Hq = int(shape[0]), int(shape[1])
+    else:
+        T, Hq = q.shape[0], q.shape[1]
+    cu = _cu(cu)
+    rows, nr = _rows(rows)
+    n = T * Hq if rows is None else nr
+    if compact:
+        assert rows is not None and q.reshape(-1, D).shape[0] == nr
+        assert dout.reshape(-1, D).shape[0] == nr
+    else:
+        assert dout.shape == q.shape
+    sel = np.ascontiguousarray(sel, dtype=np.int32).reshape(n, -1)
+    dq = np.empty((n, D), np.float64) if want_dq else None
+    lo, hi = 0, 0
+    dk = dv = None
+    if kv_window is not None:
+        lo, hi = (0, T) if kv_window == "all" else (int(kv_window[0]), int(kv_window[1]))
+        dk = np.empty((hi - lo, Hkv, D), np.float64)
+        dv = np.empty((hi - lo, Hkv, D), np.float64)
+    _check(_load().moba_oracle_attend_backward(
+        q.ctypes.data, k.ctypes.data, v.ctypes.data, dout.ctypes.data, dt, T, Hq, Hkv, D,
+        cu.ctypes.data, cu.size - 1, int(block_size), sel.shape[1], sel.ctypes.data, _ptr(rows),
+        nr, 1 if compact else 0, _ptr(dq), lo, hi, _ptr(dk), _ptr(dv)), "attend_backward")
+    return dq, dk, dv
 
 
 def dense(q, k, v, cu, rows=None):
