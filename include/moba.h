@@ -104,6 +104,30 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
                          moba_tensor* out, moba_tensor* lse, hipStream_t stream);
 
 /*
+ * MoBA backward: gradients of moba_forward's output w.r.t. q, k and v.  The
+ * gate (Eq. 3 and Eq. 5) is a hard 0/1 choice and passes no gradient, so
+ * these are the gradients of softmax attention (Eq. 2) over the key set of
+ * Eq. 4 that the forward selected.
+ *
+ * q, k, v, cu_seqlens, block_size, topk: exactly as passed to moba_forward;
+ *   the selection is recomputed from them and equals the forward's.
+ * out [T, Hq, D], lse [Hq, T]: moba_forward's results for these inputs.
+ * dout [T, Hq, D]: gradient of the loss w.r.t. out.
+ * dq [T, Hq, D], dk, dv [T, Hkv, D]: outputs, overwritten; dk and dv of a
+ *   kv-head sum over the query heads of its group.
+ * bf16 only: f32 inputs return MOBA_ERR_DTYPE.  Layout rules as for
+ * moba_forward (last dim contiguous, 16-byte aligned rows, any token/head
+ * stride).  Products accumulate in fp32; the softmax weights P and the score
+ * gradients dS are rounded to bf16 for the second matrix-core products;
+ * Delta = <dout, out> per row uses the bf16 out.  Deterministic: no atomics,
+ * fixed summation order.
+ */
+moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                          const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                          const moba_tensor* out, const moba_tensor* lse, const moba_tensor* dout,
+                          moba_tensor* dq, moba_tensor* dk, moba_tensor* dv, hipStream_t stream);
+
+/*
  * Dense causal attention (Eq. 1 with a causal mask and scale 1/sqrt(D)):
  * every query attends to every key of its sequence up to and including
  * itself.  Same tensor conventions as moba_forward.

@@ -344,11 +344,19 @@ int moba_oracle_attend(const void* q, const void* k, const void* v, int dtype, i
  * tokens kv_lo <= u < kv_hi, as [(kv_hi - kv_lo), Hkv, D]; the contributions
  * to a kv-head sum over the query heads of its group.  Each thread
  * accumulates into private dk/dv arrays, added up in thread order at the end.
+ *
+ * cq, ck, cv (nullable; ck and cv need dk) receive, in the layouts of dq, dk
+ * and dv, the sums of absolute terms that bound a rounded evaluation (used
+ * only by the tests' tolerances), with d_row = sum over dims |go| |o|:
+ *   cq = sum_u (|dz_u| + p_u d_row) |k_u| / sqrt(D)
+ *   ck_u += (|dz_u| + p_u d_row) |q| / sqrt(D)
+ *   cv_u += p_u |go|
  */
 static void backward_row(const void* q, const void* k, const void* v, const void* dout,
                          int dtype, int Hkv, int D, int64_t qoff, int g, const int64_t* keys,
                          int64_t nk, double* z, double* dpv, double* dq, int64_t kv_lo,
-                         int64_t kv_hi, double* dk, double* dv) {
+                         int64_t kv_hi, double* dk, double* dv, double* cq, double* ck,
+                         double* cv) {
   double scale = 1.0 / sqrt((double)D);
   double m = -INFINITY;
   for (int64_t x = 0; x < nk; x++) {
@@ -372,19 +380,40 @@ static void backward_row(const void* q, const void* k, const void* v, const void
     dpv[x] = acc;
     pdp += z[x] * acc;
   }
+  /* d_row = sum over dims of |go| |o|, o = sum_u p_u v_u (bounds only) */
+  double drow = 0.0;
+  if (cq || ck)
+    for (int d = 0; d < D; d++) {
+      double o = 0.0;
+      for (int64_t x = 0; x < nk; x++) o += z[x] * elem(v, dtype, (keys[x] * Hkv + g) * D + d);
+      drow += fabs(elem(dout, dtype, qoff + d)) * fabs(o);
+    }
   if (dq)
     for (int d = 0; d < D; d++) dq[d] = 0.0;
+  if (cq)
+    for (int d = 0; d < D; d++) cq[d] = 0.0;
   for (int64_t x = 0; x < nk; x++) {
     int64_t u = keys[x];
     double dz = z[x] * (dpv[x] - pdp);
+    double az = fabs(dz) + z[x] * drow;
     if (dq)
       for (int d = 0; d < D; d++) dq[d] += dz * scale * elem(k, dtype, (u * Hkv + g) * D + d);
+    if (cq)
+      for (int d = 0; d < D; d++) cq[d] += az * scale * fabs(elem(k, dtype, (u * Hkv + g) * D + d));
     if (dk && u >= kv_lo && u < kv_hi) {
       double* dkr = dk + ((u - kv_lo) * Hkv + g) * D;
       double* dvr = dv + ((u - kv_lo) * Hkv + g) * D;
       for (int d = 0; d < D; d++) {
         dkr[d] += dz * scale * elem(q, dtype, qoff + d);
         dvr[d] += z[x] * elem(dout, dtype, qoff + d);
+      }
+      if (ck) {
+        double* ckr = ck + ((u - kv_lo) * Hkv + g) * D;
+        double* cvr = cv + ((u - kv_lo) * Hkv + g) * D;
+        for (int d = 0; d < D; d++) {
+          ckr[d] += az * scale * fabs(elem(q, dtype, qoff + d));
+          cvr[d] += z[x] * fabs(elem(dout, dtype, qoff + d));
+        }
       }
     }
   }
@@ -394,26 +423,28 @@ int moba_oracle_attend_backward(const void* q, const void* k, const void* v, con
                                 int dtype, int64_t T, int Hq, int Hkv, int D, const int32_t* cu,
                                 int S, int B, int topk, const int32_t* sel, const int64_t* rows,
                                 int64_t nrows, int q_compact, double* dq, int64_t kv_lo,
-                                int64_t kv_hi, double* dk, double* dv) {
+                                int64_t kv_hi, double* dk, double* dv, double* cq, double* ck,
+                                double* cv) {
   if (check_common(T, Hq, Hkv, D, cu, S) != ORC_OK || B < 1 || topk < 1 || !sel || !dout)
     return ORC_EARG;
   if (q_compact && !rows) return ORC_EARG;
   if ((dk == NULL) != (dv == NULL)) return ORC_EARG;
+  if ((ck == NULL) != (cv == NULL) || (ck && !dk)) return ORC_EARG;
   if (dk && (kv_lo < 0 || kv_hi > T || kv_lo > kv_hi)) return ORC_EARG;
   if (!rows) nrows = T * Hq;
   int G = Hq / Hkv;
   int64_t nkv = dk ? (kv_hi - kv_lo) * Hkv * D : 0;
-  if (dk) {
-    memset(dk, 0, sizeof(double) * (size_t)nkv);
-    memset(dv, 0, sizeof(double) * (size_t)nkv);
-  }
+  int nacc = ck ? 4 : 2; /* dk, dv (, ck, cv) */
+  double* outs[4] = {dk, dv, ck, cv};
+  if (dk)
+    for (int a = 0; a < nacc; a++) memset(outs[a], 0, sizeof(double) * (size_t)nkv);
   int nthr = 1;
 #ifdef _OPENMP
   nthr = omp_get_max_threads();
 #endif
-  double** pdk = (double**)calloc((size_t)nthr, sizeof(double*));
-  double** pdv = (double**)calloc((size_t)nthr, sizeof(double*));
-  if (!pdk || !pdv) { free(pdk); free(pdv); return ORC_ENOMEM; }
+  /* private accumulators: priv[th * 4 + a] */
+  double** priv = (double**)calloc((size_t)nthr * 4, sizeof(double*));
+  if (!priv) return ORC_ENOMEM;
   int fail = 0;
 #pragma omp parallel num_threads(nthr)
   {
@@ -421,22 +452,22 @@ int moba_oracle_attend_backward(const void* q, const void* k, const void* v, con
 #ifdef _OPENMP
     me = omp_get_thread_num();
 #endif
-    double* mydk = NULL;
-    double* mydv = NULL;
-    if (dk) {
-      mydk = (double*)calloc((size_t)nkv > 0 ? (size_t)nkv : 1, sizeof(double));
-      mydv = (double*)calloc((size_t)nkv > 0 ? (size_t)nkv : 1, sizeof(double));
-      if (!mydk || !mydv) fail = 1;
-    }
-    pdk[me] = mydk;
-    pdv[me] = mydv;
+    double* mine[4] = {NULL, NULL, NULL, NULL};
+    int ok = 1;
+    if (dk)
+      for (int a = 0; a < nacc; a++) {
+        mine[a] = (double*)calloc((size_t)nkv > 0 ? (size_t)nkv : 1, sizeof(double));
+        if (!mine[a]) ok = 0;
+      }
+    if (!ok) fail = 1;
+    for (int a = 0; a < 4; a++) priv[me * 4 + a] = mine[a];
     int64_t cap = 0;
     int64_t* keys = NULL;
     double* z = NULL;
     double* dpv = NULL;
 #pragma omp for schedule(dynamic, 16)
     for (int64_t i = 0; i < nrows; i++) {
-      if (dk && (!mydk || !mydv)) continue;
+      if (!ok) continue;
       int64_t r = rows ? rows[i] : i;
       int64_t t = r / Hq;
       int h = (int)(r % Hq);
@@ -468,24 +499,22 @@ int moba_oracle_attend_backward(const void* q, const void* k, const void* v, con
       }
       int64_t qoff = q_compact ? i * D : (t * Hq + h) * D;
       backward_row(q, k, v, dout, dtype, Hkv, D, qoff, g, keys, nk, z, dpv,
-                   dq ? dq + i * D : NULL, kv_lo, kv_hi, mydk, mydv);
+                   dq ? dq + i * D : NULL, kv_lo, kv_hi, mine[0], mine[1],
+                   cq ? cq + i * D : NULL, mine[2], mine[3]);
     }
     free(keys);
     free(z);
     free(dpv);
   }
-  if (dk && !fail) {
-    for (int th = 0; th < nthr; th++) {
-      if (!pdk[th]) continue;
-      for (int64_t x = 0; x < nkv; x++) {
-        dk[x] += pdk[th][x];
-        dv[x] += pdv[th][x];
+  if (dk && !fail)
+    for (int th = 0; th < nthr; th++)
+      for (int a = 0; a < nacc; a++) {
+        const double* src = priv[th * 4 + a];
+        if (!src) continue;
+        for (int64_t x = 0; x < nkv; x++) outs[a][x] += src[x];
       }
-    }
-  }
-  for (int th = 0; th < nthr; th++) { free(pdk[th]); free(pdv[th]); }
-  free(pdk);
-  free(pdv);
+  for (int x = 0; x < nthr * 4; x++) free(priv[x]);
+  free(priv);
   return fail ? ORC_EARG : ORC_OK;
 }
 

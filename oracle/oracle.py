@@ -60,7 +60,7 @@ def _load():
                                            i32, vp, vp, i64, vp, vp, i32]
         lib.moba_oracle_attend_backward.argtypes = [vp, vp, vp, vp, i32, i64, i32, i32, i32,
                                                     vp, i32, i32, i32, vp, vp, i64, i32, vp,
-                                                    i64, i64, vp, vp]
+                                                    i64, i64, vp, vp, vp, vp, vp]
         lib.moba_oracle_dense.argtypes = [vp, vp, vp, i32, i64, i32, i32, i32, vp, i32, vp,
                                           i64, vp, vp]
         lib.moba_oracle_num_blocks.argtypes = [vp, i32, i32]
@@ -215,14 +215,16 @@ def attend_rows(q_rows, T: int, Hq: int, k, v, cu, block_size: int, sel: np.ndar
 
 
 def attend_backward(q, k, v, dout, cu, block_size: int, sel: np.ndarray, rows=None,
-                    shape=None, want_dq: bool = True, kv_window=None):
+                    shape=None, want_dq: bool = True, kv_window=None, with_bounds: bool = False):
     """Gradients of attend() for a fixed selection sel [nrows, topk].
 
     Returns (dq, dk, dv): dq [nrows, D] fp64 (None unless want_dq); dk, dv
     [(hi - lo), Hkv, D] fp64 over the token window kv_window = (lo, hi)
     (None: no dk/dv; "all": every token), holding the listed rows'
     contributions.  With shape = (T, Hq), q and dout hold the listed rows'
-    vectors only, [nrows, D] in list order."""
+    vectors only, [nrows, D] in list order.  With with_bounds, returns
+    (dq, dk, dv, cq, ck, cv): the sums of absolute terms, in the same
+    layouts, that the tests' rounding tolerances scale with."""
     q, dt = _elems(q)
     k, dtk = _elems(k)
     v, dtv = _elems(v)
@@ -246,15 +248,22 @@ def attend_backward(q, k, v, dout, cu, block_size: int, sel: np.ndarray, rows=No
     sel = np.ascontiguousarray(sel, dtype=np.int32).reshape(n, -1)
     dq = np.empty((n, D), np.float64) if want_dq else None
     lo, hi = 0, 0
-    dk = dv = None
+    dk = dv = ck = cv = None
     if kv_window is not None:
         lo, hi = (0, T) if kv_window == "all" else (int(kv_window[0]), int(kv_window[1]))
         dk = np.empty((hi - lo, Hkv, D), np.float64)
         dv = np.empty((hi - lo, Hkv, D), np.float64)
+        if with_bounds:
+            ck = np.empty((hi - lo, Hkv, D), np.float64)
+            cv = np.empty((hi - lo, Hkv, D), np.float64)
+    cq = np.empty((n, D), np.float64) if (with_bounds and want_dq) else None
     _check(_load().moba_oracle_attend_backward(
         q.ctypes.data, k.ctypes.data, v.ctypes.data, dout.ctypes.data, dt, T, Hq, Hkv, D,
         cu.ctypes.data, cu.size - 1, int(block_size), sel.shape[1], sel.ctypes.data, _ptr(rows),
-        nr, 1 if compact else 0, _ptr(dq), lo, hi, _ptr(dk), _ptr(dv)), "attend_backward")
+        nr, 1 if compact else 0, _ptr(dq), lo, hi, _ptr(dk), _ptr(dv), _ptr(cq), _ptr(ck),
+        _ptr(cv)), "attend_backward")
+    if with_bounds:
+        return dq, dk, dv, cq, ck, cv
     return dq, dk, dv
 
 

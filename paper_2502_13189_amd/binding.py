@@ -59,6 +59,7 @@ def load() -> ctypes.CDLL:
     vp, i32 = ctypes.c_void_p, ctypes.c_int32
     sig = {
         "moba_forward": [P, P, P, P, i32, i32, P, P, vp],
+        "moba_backward": [P, P, P, P, i32, i32, P, P, P, P, P, P, vp],
         "moba_dense_forward": [P, P, P, P, P, P, vp],
         "moba_pool": [P, P, i32, P, vp],
         "moba_select": [P, P, P, i32, i32, P, P, vp],
@@ -138,6 +139,27 @@ def forward(q, k, v, cu_seqlens, block_size: int, topk: int, out=None, lse=None,
     _check("moba_forward", lib.moba_forward(_ref(dq), _ref(dk), _ref(dv), _ref(dc), int(block_size),
                                             int(topk), _ref(do), _ref(dl), _stream(q, stream)))
     return out, lse
+
+
+def backward(q, k, v, cu_seqlens, block_size: int, topk: int, out, lse, dout, dq=None, dk=None,
+             dv=None, stream=None):
+    """Gradients of forward() w.r.t. q, k, v (bf16).  out and lse are forward()'s
+    results for the same inputs; dout [T, Hq, 128] is the gradient w.r.t. out.
+    Returns (dq [T, Hq, 128], dk [T, Hkv, 128], dv [T, Hkv, 128])."""
+    lib = load()
+    cu = _cu(cu_seqlens)
+    if dq is None:
+        dq = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if dk is None:
+        dk = torch.empty_like(k, memory_format=torch.contiguous_format)
+    if dv is None:
+        dv = torch.empty_like(v, memory_format=torch.contiguous_format)
+    d = [describe(t) for t in (q, k, v, cu, out, lse, dout, dq, dk, dv)]
+    _check("moba_backward", lib.moba_backward(_ref(d[0]), _ref(d[1]), _ref(d[2]), _ref(d[3]),
+                                              int(block_size), int(topk), _ref(d[4]), _ref(d[5]),
+                                              _ref(d[6]), _ref(d[7]), _ref(d[8]), _ref(d[9]),
+                                              _stream(q, stream)))
+    return dq, dk, dv
 
 
 def dense_forward(q, k, v, cu_seqlens, out=None, lse=None, stream=None):

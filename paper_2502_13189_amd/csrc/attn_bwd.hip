@@ -1,0 +1,664 @@
+// Backward of MoBA attention on the gfx950 matrix cores: the gradients w.r.t.
+// q, k and v for the selection the forward made.  The gate is a hard 0/1
+// choice (Eq. 3 and Eq. 5) and passes no gradient, so this is the chain rule
+// through Eq. 2 over the key set of Eq. 4.  With the forward's lse per row
+// and Delta = <dO, O> per row (O the forward's output):
+//   P = exp(z - lse), z = <q, k> / sqrt(D);   dP = <dO, v>;   dS = P (dP - Delta)
+//   dQ = sum over keys of dS k / sqrt(D)
+//   dK = sum over rows of dS q / sqrt(D),     dV = sum over rows of P dO
+//
+// Kernels, in launch order:
+//   delta  LD[h, t] = (lse * log2 e, Delta), 16 lanes per row.
+//   rec    (t, h, LD[h, t]) of every routed history entry, in routing order,
+//          so that the key-side kernel gets a row's facts with one load.
+//   dq     query side, on the forward's tiles.  A history tile (256 routed
+//          rows of one (kv-head, block) bin) loops over the block's 64-key
+//          tiles and writes each row's dQ for that selection slot in fp32; a
+//          current-block tile covers the causal keys of its block, adds the
+//          row's history partials in slot order and writes dQ.  Per key
+//          tile and wave: S^T = K . Q^T and dP^T = V . dO^T (K and V
+//          row-major from LDS, Q^T and dO^T operands in registers), then
+//          dQ^T += K^T . dS^T from the packed K^T tile: 48 MFMAs.
+//   dkdv   key side: a work-group owns 256 keys of one block and kv-head
+//          (wave w: 32 keys, with K, V, dK^T and dV^T in registers) and
+//          loops over every row that attends them, 64 rows at a time: the
+//          bin's routed history rows, then the block's own rows (causal).
+//          The rows' Q and dO arrive by LDS DMA, gathered row by row, and are
+//          transposed once per chunk inside LDS.  Per 32-row subtile and
+//          wave: S = Q . K^T, dP = dO . V^T, then dV^T += dO^T . P and
+//          dK^T += Q^T . dS: 32 MFMAs.  Each key has one owner, so dK and dV
+//          need neither atomics nor a merge.
+// P and dS enter the second products as bf16; every product accumulates in
+// fp32.
+#include "bwd_internal.h"
+#include "mfma_tile.h"
+
+#include <limits.h>
+#include <math.h>
+
+namespace moba {
+namespace {
+
+enum { kHist = 0, kCur = 1 };
+
+constexpr int kRows = kTileRowsMfma;  // query rows per dQ work-group (256)
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Per-lane DMA sources of one 64-key tile set: lane chunk p = 64j + L of DMA
+// instruction j holds row p / 17, chunk min(p % 17, 15) of a row-major tile
+// and row p / 9, chunk min(p % 9, 7) of a packed tile.
+__device__ __forceinline__ void init_dma(Dma& D, int wave, int lane, const char* base, int64_t st_bytes,
+                                         int64_t len, const char* packed) {
+  D.wave = wave;
+  D.kbase = base;
+  D.k_tile = kKeyTile * st_bytes;
+  D.len = len;
+  D.klast = base + (len - 1) * st_bytes;
+#pragma unroll
+  for (int x = 0; x < 3; x++) {
+    const int pk = 64 * (wave + 8 * x) + lane;
+    const int row = min(pk / kRowK, kKeyTile - 1), c = min(pk % kRowK, kRowK - 2);
+    D.krow[x] = row;
+    D.kcol[x] = (uint32_t)(c * 16);
+    D.koff[x] = (uint32_t)(row * st_bytes) + D.kcol[x];
+    const int vrow = min(pk / kRowV, kHeadDim - 1), vc = min(pk % kRowV, kRowV - 2);
+    D.voff[x] = (uint32_t)(vrow * (kKeyTile * 2) + vc * 16);
+  }
+  D.vbase = packed;
+}
+
+// ============================================================ delta, rec
+__global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a, Problem p) {
+  const int64_t r = (int64_t)blockIdx.x * 16 + threadIdx.x / 16;  // r = t * Hq + h
+  const int l16 = threadIdx.x % 16;
+  if (r >= p.T * p.Hq) return;  // the 16 lanes of a row leave together
+  const int64_t t = r / p.Hq;
+  const int h = (int)(r % p.Hq);
+  const uint4 ou = *reinterpret_cast<const uint4*>(static_cast<const __hip_bfloat16*>(a.o) +
+                                                   t * a.o_st + (int64_t)h * a.o_sh + 8 * l16);
+  const uint4 du = *reinterpret_cast<const uint4*>(static_cast<const __hip_bfloat16*>(a.dout) +
+                                                   t * a.do_st + (int64_t)h * a.do_sh + 8 * l16);
+  const uint32_t ow[4] = {ou.x, ou.y, ou.z, ou.w}, dw[4] = {du.x, du.y, du.z, du.w};
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    acc = fmaf(__uint_as_float(ow[i] << 16), __uint_as_float(dw[i] << 16), acc);
+    acc = fmaf(__uint_as_float(ow[i] & 0xffff0000u), __uint_as_float(dw[i] & 0xffff0000u), acc);
+  }
+#pragma unroll
+  for (int m = 8; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
+  if (l16 == 0) {
+    const int64_t i = (int64_t)h * p.T + t;
+    a.ld[i] = make_float2(a.lse[i] * kLog2e, acc);
+  }
+}
+
+__global__ __launch_bounds__(256) void bwd_rec_kernel(BwdArgs a, Problem p) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= p.hist_entries) return;
+  const uint64_t kh = (uint64_t)(p.topk - 1);
+  const uint64_t TG = (uint64_t)p.T * p.G;
+  const uint64_t r = (uint64_t)a.entries[e] / kh;
+  const int g = (int)(r / TG);
+  const uint64_t rem = r - (uint64_t)g * TG;
+  const int64_t t = (int64_t)(rem / p.G);
+  const int h = g * p.G + (int)(rem % p.G);
+  const float2 ld = a.ld[(int64_t)h * p.T + t];
+  a.rec[e] = make_int4((int)t, h, __float_as_int(ld.x), __float_as_int(ld.y));
+}
+
+// ================================================================ dQ
+// dS^T of a 64-key tile from S^T and dP^T, as bf16 operands db[2*th + s2]
+// (keys 32*th + 16*s2 .. +15, the order of the packed K^T tile).
+__device__ __forceinline__ void grad_scores(f32x16 (&s)[2], const f32x16 (&dp)[2], bf16x8 (&db)[4],
+                                            bool edge, int lo, int hi, float c2, float lse2,
+                                            float dlt) {
+  if (edge) mask_keys(s, lo, hi);
+#pragma unroll
+  for (int th = 0; th < 2; th++)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; s2++) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const int i0 = 8 * s2 + 2 * e, i1 = i0 + 1;
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[th][i0], c2, -lse2));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[th][i1], c2, -lse2));
+        w[e] = pack_bf16(p0 * (dp[th][i0] - dlt), p1 * (dp[th][i1] - dlt));
+      }
+      db[2 * th + s2] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+    }
+}
+
+constexpr int kDqStage = 2 * kBufK + kBufV;  // K, V (row-major), K^T (packed)
+
+template <int MODE>
+__global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
+  __shared__ u32x4 lds[2 * kDqStage];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int qc = lane & 31, hh = lane >> 5;
+
+  // ------------------------------------------------------------ tile setup
+  int g, s;
+  int64_t kbeg, kend, tmin;
+  RowInfo ri;
+  const int rloc = wave * 32 + qc;
+  if constexpr (MODE == kHist) {
+    const int64_t nb = p.nblk_total;
+    const int64_t tbeg = a.bin_tile_start[a.g0 * nb];
+    const int64_t tend = a.bin_tile_start[a.g1 * nb];
+    // tiles of one bin share its K/V block: a contiguous run of tiles per XCD
+    const int64_t per = gridDim.x / 8;
+    const int64_t tile = tbeg + (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (tile >= tend) return;
+    int64_t lo = a.g0 * nb, hi = a.g1 * nb - 1;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (a.bin_tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    const int64_t bin = lo;
+    g = (int)(bin / nb);
+    const int b = (int)(bin % nb);
+    const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kRows;
+    const int n = (int)min((int64_t)kRows, a.bin_start[bin] + a.bin_count[bin] - e0);
+    s = find_seq(a.seqs, p.S, b, [](const SeqInfo& x) { return x.blk_off; });
+    const SeqInfo sq = a.seqs[s];
+    kbeg = (int64_t)sq.tok_start + (int64_t)(b - sq.blk_off) * p.B;
+    kend = kbeg + p.B;
+    tmin = kend;
+    const uint64_t kh = (uint64_t)(p.topk - 1);
+    const uint64_t TG = (uint64_t)p.T * p.G;
+    const uint64_t ev = a.entries[e0 + min(rloc, n - 1)];
+    const uint64_t rem = ev / kh - (uint64_t)g * TG;
+    const bool ok = rem < TG;
+    ri.valid = rloc < n && ok;
+    ri.t = ok ? (int64_t)(rem / p.G) : kbeg;
+    ri.h = g * p.G + (ok ? (int)(rem % p.G) : 0);
+    ri.dst = (int64_t)(ev - (uint64_t)a.g0 * TG * kh);
+  } else {
+    const CausalTile ct = a.tiles[blockIdx.x];
+    if (ct.t1 <= ct.t0) return;  // padding of the tile list
+    g = a.g0 + blockIdx.y;
+    s = ct.s;
+    kbeg = ct.kbeg;
+    kend = ct.t1;
+    tmin = ct.t0;
+    const int nrow = (ct.t1 - ct.t0) * p.G;
+    ri.valid = rloc < nrow;
+    const int rr = ri.valid ? rloc : 0;
+    ri.t = ct.t0 + rr / p.G;
+    ri.h = g * p.G + rr % p.G;
+    ri.dst = (int64_t)(g - a.g0) * p.T * p.G + ri.t * p.G + (rr % p.G);
+  }
+  g = __builtin_amdgcn_readfirstlane(g);
+  s = __builtin_amdgcn_readfirstlane(s);
+  kbeg = uniform64(kbeg);
+  kend = uniform64(kend);
+  tmin = uniform64(tmin);
+  const SeqInfo sq = a.seqs[s];
+  const int64_t tok0 = sq.tok_start;
+
+  // ------------------------------------------- Q^T, dO^T operands, lse, Delta
+  bf16x8 qf[8], df[8];
+  {
+    const __hip_bfloat16* qrow = static_cast<const __hip_bfloat16*>(a.q) + ri.t * a.q_st +
+                                 (int64_t)ri.h * a.q_sh + 8 * hh;
+    const __hip_bfloat16* drow = static_cast<const __hip_bfloat16*>(a.dout) + ri.t * a.do_st +
+                                 (int64_t)ri.h * a.do_sh + 8 * hh;
+#pragma unroll
+    for (int kk = 0; kk < 8; kk++) {
+      qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 16 * kk));
+      df[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(drow + 16 * kk));
+    }
+  }
+  const float2 ld = a.ld[(int64_t)ri.h * p.T + ri.t];
+
+  // ------------------------------------------------------------ key tiles
+  const int64_t rb = kbeg - tok0, re = kend - tok0;
+  const int i0 = (int)(rb / kKeyTile), i1 = (int)((re + kKeyTile - 1) / kKeyTile);
+  Dma DK, DV;  // DK: K row-major and the packed K^T; DV: V row-major
+  {
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const char* kb = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.k) +
+                                                   (int64_t)g * a.k_sh) + tok0 * (a.k_st * 2);
+    const char* vb = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.v) +
+                                                   (int64_t)g * a.v_sh) + tok0 * (a.v_st * 2);
+    const char* ktb = reinterpret_cast<const char*>(
+        a.kt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) * (kKeyTile * kHeadDim));
+    init_dma(DK, wv, lane, kb, a.k_st * 2, sq.len, ktb);
+    init_dma(DV, wv, lane, vb, a.v_st * 2, sq.len, nullptr);
+  }
+  ReadOff ro;
+  ro.kq = qc * kRowK + hh;
+  ro.vq = qc * kRowV + hh;
+  const float c2 = a.scale_log2;
+  f32x16 acc[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+    for (int r = 0; r < 16; r++) acc[dt][r] = 0.0f;
+
+  // stage x: K at lds + x*kDqStage, V at + kBufK, K^T at + 2*kBufK
+  dma_k(DK, i0, lds);
+  dma_k(DV, i0, lds + kBufK);
+  dma_v(DK, i0, lds + 2 * kBufK);
+  dma_wait();
+  __syncthreads();
+
+  for (int i = i0; i < i1; i++) {
+    const int cur = (i - i0) & 1;
+    u32x4* st = lds + cur * kDqStage;
+    if (i + 1 < i1) {
+      u32x4* nx = lds + (cur ^ 1) * kDqStage;
+      dma_k(DK, i + 1, nx);
+      dma_k(DV, i + 1, nx + kBufK);
+      dma_v(DK, i + 1, nx + 2 * kBufK);
+    }
+    f32x16 sc[2], dp[2];
+    qk(sc, st, ro, qf);
+    qk(dp, st + kBufK, ro, df);
+    const int64_t u0 = tok0 + (int64_t)i * kKeyTile;
+    const bool edge = u0 < kbeg || u0 + kKeyTile > kend || (MODE != kHist && u0 + kKeyTile - 1 > tmin);
+    int lo = 0, hi = kKeyTile;
+    if (edge) {
+      lo = (int)max((int64_t)0, kbeg - u0) - 4 * hh;
+      const int64_t lim = min((int64_t)kKeyTile, kend - u0);
+      hi = (int)(MODE == kHist ? lim : min(lim, ri.t + 1 - u0)) - 4 * hh;
+    }
+    bf16x8 db[4];
+    grad_scores(sc, dp, db, edge, lo, hi, c2, ld.x, ld.y);
+    pv(acc, st + 2 * kBufK, ro, db);
+    dma_wait();
+    __syncthreads();
+  }
+
+  // -------------------------------------------------------------- epilogue
+  if (!ri.valid) return;
+  const float scl = a.scale;
+  if constexpr (MODE == kHist) {
+    float* dst = a.dq_part + ri.dst * kHeadDim;
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; r4++)
+        *reinterpret_cast<float4*>(dst + 32 * dt + 8 * r4 + 4 * hh) =
+            make_float4(acc[dt][4 * r4] * scl, acc[dt][4 * r4 + 1] * scl,
+                        acc[dt][4 * r4 + 2] * scl, acc[dt][4 * r4 + 3] * scl);
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) acc[dt][r] *= scl;
+    // history slots of this row, in slot order
+    const int kh = p.topk - 1;
+    const int nh = (int)min((int64_t)kh, (ri.t - tok0) / p.B);
+    const float* part = a.dq_part + ri.dst * kh * kHeadDim;
+    for (int x = 0; x < nh; x++) {
+#pragma unroll
+      for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; r4++) {
+          const float4 f =
+              *reinterpret_cast<const float4*>(part + x * kHeadDim + 32 * dt + 8 * r4 + 4 * hh);
+          acc[dt][4 * r4] += f.x;
+          acc[dt][4 * r4 + 1] += f.y;
+          acc[dt][4 * r4 + 2] += f.z;
+          acc[dt][4 * r4 + 3] += f.w;
+        }
+    }
+    __hip_bfloat16* drow =
+        static_cast<__hip_bfloat16*>(a.dq) + ri.t * a.dq_st + (int64_t)ri.h * a.dq_sh;
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; r4++) {
+        uint2 w;
+        w.x = pack_bf16(acc[dt][4 * r4], acc[dt][4 * r4 + 1]);
+        w.y = pack_bf16(acc[dt][4 * r4 + 2], acc[dt][4 * r4 + 3]);
+        *reinterpret_cast<uint2*>(drow + 32 * dt + 8 * r4 + 4 * hh) = w;
+      }
+  }
+}
+
+// ============================================================== dK, dV
+constexpr int kChunk = 64;                       // rows per chunk
+constexpr int kRowT = kChunk / 8 + 1;            // transposed row (one dim): 8 chunks + 1 pad
+constexpr int kBufR = kChunk * kRowK;            // row-major Q or dO chunk (1088)
+constexpr int kBufT = kHeadDim * kRowT;          // transposed Q or dO chunk (1152)
+constexpr int kDmaR = kBufR / 64;                // DMA instructions per row-major chunk (17)
+constexpr int kDkdvLds = 4 * kBufR + 2 * kBufT;  // Q, dO row-major x2, Q^T, dO^T: 104 KiB
+constexpr int kSlots = 3;                        // row tables in flight
+
+// Position p (0..63) of a packed row order holds row perm(p) of the chunk
+// (the key order of the packed K^T / V^T tiles, applied to rows).
+__device__ __forceinline__ int packed_row(int p) {
+  const int grp = p & ~15, w = p & 15;
+  return grp + 8 * ((w & 7) >> 2) + 4 * (w >> 3) + (w & 3);
+}
+
+struct __align__(16) RowTab {
+  int t[kSlots][kChunk];
+  int h[kSlots][kChunk];
+  int kmax[kSlots][kChunk];   // last key the row may attend (causal rows), -1 for padding
+  float lse2[kSlots][kChunk];
+  float dlt[kSlots][kChunk];
+};
+
+// What one lane of wave 0 fetches for one row of a chunk.
+struct RowFetch {
+  int4 rec;
+  float2 ld;
+  int t, h, kind;  // kind 0: routed history row, 1: row of the block itself, 2: padding
+};
+
+struct RowList {
+  int64_t nhist, bstart, nrows;
+  int k0, nct, g;
+};
+
+__device__ __forceinline__ RowFetch row_fetch(const BwdArgs& a, const Problem& p, const RowList& L,
+                                              int ci, int lane) {
+  RowFetch f;
+  const int64_t x = (int64_t)ci * kChunk + lane;
+  f.t = L.k0;
+  f.h = L.g * p.G;
+  if (x < L.nhist) {
+    f.kind = 0;
+    f.rec = a.rec[L.bstart + x];
+  } else if (x < L.nrows) {
+    f.kind = 1;
+    const int y = (int)(x - L.nhist);
+    const int hl = y / L.nct;
+    f.t = L.k0 + (y - hl * L.nct);
+    f.h = L.g * p.G + hl;
+    f.ld = a.ld[(int64_t)f.h * p.T + f.t];
+  } else {
+    f.kind = 2;
+  }
+  return f;
+}
+
+__device__ __forceinline__ void row_store(RowTab& R, int slot, int lane, const RowFetch& f) {
+  int t = f.t, h = f.h, km = -1;
+  float l2 = INFINITY, dl = 0.0f;
+  if (f.kind == 0) {
+    t = f.rec.x;
+    h = f.rec.y;
+    l2 = __int_as_float(f.rec.z);
+    dl = __int_as_float(f.rec.w);
+    km = INT_MAX;
+  } else if (f.kind == 1) {
+    l2 = f.ld.x;
+    dl = f.ld.y;
+    km = t;
+  }
+  R.t[slot][lane] = t;
+  R.h[slot][lane] = h;
+  R.kmax[slot][lane] = km;
+  R.lse2[slot][lane] = l2;
+  R.dlt[slot][lane] = dl;
+}
+
+// bf16 pair (element e of chunk a, element e of chunk b) as one 32-bit word.
+__device__ __forceinline__ uint32_t pair16(const u32x4& x, const u32x4& y, int e) {
+  const uint32_t wx = x[e >> 1], wy = y[e >> 1];
+  return (e & 1) ? ((wx >> 16) | (wy & 0xffff0000u)) : ((wx & 0xffffu) | (wy << 16));
+}
+
+__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
+  __shared__ u32x4 lds[kDkdvLds];
+  __shared__ RowTab R;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int qc = lane & 31, hh = lane >> 5;
+
+  // work-group -> (kv-head, key tile): each XCD takes a contiguous run (the
+  // key tiles of one bin read the same rows), early blocks (longest row
+  // lists) first
+  const int64_t total = a.nktiles * p.Hkv;
+  const int64_t per = gridDim.x / 8;
+  const int64_t wi = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (wi >= total) return;
+  RowList L;
+  L.g = (int)(wi / a.nktiles);
+  const KeyTile kt = a.ktiles[wi % a.nktiles];
+  L.k0 = kt.k0;
+  L.nct = kt.bend - kt.k0;
+  L.nhist = 0;
+  L.bstart = 0;
+  if (a.bin_count) {
+    const int64_t bin = (int64_t)L.g * p.nblk_total + kt.b;
+    L.nhist = a.bin_count[bin];
+    L.bstart = a.bin_start[bin];
+  }
+  L.nhist = uniform64(L.nhist);
+  L.bstart = uniform64(L.bstart);
+  L.nrows = L.nhist + (int64_t)L.nct * p.G;
+  const int nch = (int)((L.nrows + kChunk - 1) / kChunk);
+
+  // this wave's 32 keys: K and V as the B operands of S = Q K^T, dP = dO V^T
+  const int kw0 = kt.k0 + 32 * wave;
+  const bool wave_live = kw0 < kt.k1;
+  const bool wave_full = kw0 + 32 <= kt.k1;
+  const int key = kw0 + qc;
+  const int kld = min(key, kt.k1 - 1);
+  bf16x8 kf[8], vf[8];
+  {
+    const __hip_bfloat16* kr = static_cast<const __hip_bfloat16*>(a.k) + (int64_t)kld * a.k_st +
+                               (int64_t)L.g * a.k_sh + 8 * hh;
+    const __hip_bfloat16* vr = static_cast<const __hip_bfloat16*>(a.v) + (int64_t)kld * a.v_st +
+                               (int64_t)L.g * a.v_sh + 8 * hh;
+#pragma unroll
+    for (int kk = 0; kk < 8; kk++) {
+      kf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(kr + 16 * kk));
+      vf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(vr + 16 * kk));
+    }
+  }
+
+  // per-lane DMA rows and chunk offsets (instruction j = wave + 8x)
+  int drow[3];
+  uint32_t dcol[3];
+#pragma unroll
+  for (int x = 0; x < 3; x++) {
+    const int pk = 64 * (wave + 8 * x) + lane;
+    drow[x] = min(pk / kRowK, kChunk - 1);
+    dcol[x] = (uint32_t)(min(pk % kRowK, kRowK - 2) * 16);
+  }
+  const char* qb = static_cast<const char*>(a.q);
+  const char* db = static_cast<const char*>(a.dout);
+  auto dma_rows = [&](int slot, u32x4* qbuf, u32x4* dbuf) {
+#pragma unroll
+    for (int x = 0; x < 3; x++) {
+      if (wave + 8 * x < kDmaR) {
+        const int64_t t = R.t[slot][drow[x]], h = R.h[slot][drow[x]];
+        __builtin_amdgcn_global_load_lds(qb + (t * a.q_st + h * a.q_sh) * 2 + dcol[x],
+                                         qbuf + 64 * (wave + 8 * x), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(db + (t * a.do_st + h * a.do_sh) * 2 + dcol[x],
+                                         dbuf + 64 * (wave + 8 * x), 16, 0, 0);
+      }
+    }
+  };
+  u32x4* qt = lds + 4 * kBufR;
+  u32x4* dtr = qt + kBufT;
+  // Q^T / dO^T of a landed chunk: thread -> (row pair at packed positions
+  // 2pp, 2pp+1; 8-dim chunk c); one 32-bit LDS word per dim.
+  auto transpose = [&](const u32x4* qbuf, const u32x4* dbuf) {
+    const int pp = tid & 31, c = tid >> 5;
+    const int r = packed_row(2 * pp);
+    const u32x4 q0 = qbuf[r * kRowK + c], q1 = qbuf[(r + 1) * kRowK + c];
+    const u32x4 d0 = dbuf[r * kRowK + c], d1 = dbuf[(r + 1) * kRowK + c];
+    uint32_t* q32 = reinterpret_cast<uint32_t*>(qt);
+    uint32_t* d32 = reinterpret_cast<uint32_t*>(dtr);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      q32[(8 * c + e) * (4 * kRowT) + pp] = pair16(q0, q1, e);
+      d32[(8 * c + e) * (4 * kRowT) + pp] = pair16(d0, d1, e);
+    }
+  };
+
+  f32x16 dka[4], dva[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      dka[dt][r] = 0.0f;
+      dva[dt][r] = 0.0f;
+    }
+  const float c2 = a.scale_log2;
+
+  // prologue: row tables of chunks 0 and 1, chunk 0 landed and transposed
+  if (wave == 0) {
+    row_store(R, 0, lane, row_fetch(a, p, L, 0, lane));
+    if (nch > 1) row_store(R, 1, lane, row_fetch(a, p, L, 1, lane));
+  }
+  __syncthreads();
+  dma_rows(0, lds, lds + 2 * kBufR);
+  dma_wait();
+  __syncthreads();
+  transpose(lds, lds + 2 * kBufR);
+  __syncthreads();
+
+  for (int i = 0; i < nch; i++) {
+    const int cur = i & 1;
+    RowFetch nf;
+    const bool fetch = wave == 0 && i + 2 < nch;
+    if (fetch) nf = row_fetch(a, p, L, i + 2, lane);
+    if (i + 1 < nch) dma_rows((i + 1) % kSlots, lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
+
+    if (wave_live) {
+      const u32x4* qr = lds + cur * kBufR;
+      const u32x4* dr = lds + 2 * kBufR + cur * kBufR;
+      const int slot = i % kSlots;
+      const bool edge = (int64_t)(i + 1) * kChunk > L.nhist || !wave_full;
+#pragma unroll 1
+      for (int st = 0; st < 2; st++) {
+        f32x16 sv, dpv;
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          sv[r] = 0.0f;
+          dpv[r] = 0.0f;
+        }
+        const u32x4* qa = qr + (32 * st + qc) * kRowK + hh;
+        const u32x4* da = dr + (32 * st + qc) * kRowK + hh;
+#pragma unroll
+        for (int kk = 0; kk < 8; kk++) sv = mfma(as_bf16x8(qa[2 * kk]), kf[kk], sv);
+#pragma unroll
+        for (int kk = 0; kk < 8; kk++) dpv = mfma(as_bf16x8(da[2 * kk]), vf[kk], dpv);
+        // this lane's rows: 32*st + 8*r4 + 4*hh + (0..3)
+        bf16x8 pb[2], sb[2];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; s2++) {
+          uint32_t wp[4], ws[4];
+#pragma unroll
+          for (int h2 = 0; h2 < 2; h2++) {
+            const int r4 = 2 * s2 + h2;
+            const int row0 = 32 * st + 8 * r4 + 4 * hh;
+            const float4 l2 = *reinterpret_cast<const float4*>(&R.lse2[slot][row0]);
+            const float4 dl = *reinterpret_cast<const float4*>(&R.dlt[slot][row0]);
+            const float lv[4] = {l2.x, l2.y, l2.z, l2.w};
+            const float dv[4] = {dl.x, dl.y, dl.z, dl.w};
+            float pr[4], ds[4];
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+              const int idx = 4 * r4 + c;
+              pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[idx], c2, -lv[c]));
+            }
+            if (edge) {
+              const int4 km = *reinterpret_cast<const int4*>(&R.kmax[slot][row0]);
+              const int kv[4] = {km.x, km.y, km.z, km.w};
+#pragma unroll
+              for (int c = 0; c < 4; c++) pr[c] = (key <= kv[c] && key < kt.k1) ? pr[c] : 0.0f;
+            }
+#pragma unroll
+            for (int c = 0; c < 4; c++) ds[c] = pr[c] * (dpv[4 * r4 + c] - dv[c]);
+            wp[2 * h2] = pack_bf16(pr[0], pr[1]);
+            wp[2 * h2 + 1] = pack_bf16(pr[2], pr[3]);
+            ws[2 * h2] = pack_bf16(ds[0], ds[1]);
+            ws[2 * h2 + 1] = pack_bf16(ds[2], ds[3]);
+          }
+          pb[s2] = as_bf16x8(u32x4{wp[0], wp[1], wp[2], wp[3]});
+          sb[s2] = as_bf16x8(u32x4{ws[0], ws[1], ws[2], ws[3]});
+        }
+        // dV^T += dO^T . P and dK^T += Q^T . dS over this subtile's 32 rows
+        const u32x4* dta = dtr + qc * kRowT + 4 * st + hh;
+        const u32x4* qta = qt + qc * kRowT + 4 * st + hh;
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; s2++)
+            dva[dt] = mfma(as_bf16x8(dta[32 * kRowT * dt + 2 * s2]), pb[s2], dva[dt]);
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; s2++)
+            dka[dt] = mfma(as_bf16x8(qta[32 * kRowT * dt + 2 * s2]), sb[s2], dka[dt]);
+      }
+    }
+    dma_wait();
+    __syncthreads();
+    if (i + 1 < nch) transpose(lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
+    if (fetch) row_store(R, (i + 2) % kSlots, lane, nf);
+    __syncthreads();
+  }
+
+  // -------------------------------------------------------------- epilogue
+  if (!wave_live || key >= kt.k1) return;
+  const float scl = a.scale;
+  __hip_bfloat16* dkr =
+      static_cast<__hip_bfloat16*>(a.dk) + (int64_t)key * a.dk_st + (int64_t)L.g * a.dk_sh;
+  __hip_bfloat16* dvr =
+      static_cast<__hip_bfloat16*>(a.dv) + (int64_t)key * a.dv_st + (int64_t)L.g * a.dv_sh;
+#pragma unroll
+  for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; r4++) {
+      const int d = 32 * dt + 8 * r4 + 4 * hh;
+      uint2 w;
+      w.x = pack_bf16(dka[dt][4 * r4] * scl, dka[dt][4 * r4 + 1] * scl);
+      w.y = pack_bf16(dka[dt][4 * r4 + 2] * scl, dka[dt][4 * r4 + 3] * scl);
+      *reinterpret_cast<uint2*>(dkr + d) = w;
+      w.x = pack_bf16(dva[dt][4 * r4], dva[dt][4 * r4 + 1]);
+      w.y = pack_bf16(dva[dt][4 * r4 + 2], dva[dt][4 * r4 + 3]);
+      *reinterpret_cast<uint2*>(dvr + d) = w;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_delta(const BwdArgs& a, const Problem& p, hipStream_t st) {
+  const int64_t rows = p.T * p.Hq;
+  if (rows <= 0) return hipSuccess;
+  bwd_delta_kernel<<<(unsigned)((rows + 15) / 16), 256, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_rec(const BwdArgs& a, const Problem& p, hipStream_t st) {
+  if (p.hist_entries <= 0 || p.topk <= 1) return hipSuccess;
+  bwd_rec_kernel<<<(unsigned)((p.hist_entries + 255) / 256), 256, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_hist(const BwdArgs& a, const Problem& p, int64_t grid, hipStream_t st) {
+  if (grid <= 0) return hipSuccess;
+  grid = (grid + 7) / 8 * 8;
+  bwd_dq_kernel<kHist><<<(unsigned)grid, 512, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_cur(const BwdArgs& a, const Problem& p, hipStream_t st) {
+  if (a.ntiles <= 0 || a.g1 <= a.g0) return hipSuccess;
+  dim3 grid((unsigned)a.ntiles, a.g1 - a.g0);
+  bwd_dq_kernel<kCur><<<grid, 512, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dkdv(const BwdArgs& a, const Problem& p, hipStream_t st) {
+  const int64_t total = a.nktiles * p.Hkv;
+  if (total <= 0) return hipSuccess;
+  const int64_t grid = (total + 7) / 8 * 8;
+  bwd_dkdv_kernel<<<(unsigned)grid, 512, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+}  // namespace moba

@@ -43,182 +43,22 @@
 // natural-log lse in fp32; current-block and dense tiles write the normalised
 // result to the output and its lse (the merge kernel then folds the history
 // partials into the current-block result).
-#include "moba_internal.h"
+#include "mfma_tile.h"
 
 #include <math.h>
 
 namespace moba {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
-
 enum { kHist = 0, kCur = 1, kDense = 2 };
 
 constexpr int kRows = kTileRowsMfma;               // query rows per work-group (256)
-constexpr int kChunksV = kHeadDim * kKeyTile / 8;  // 16-byte chunks per V^T tile (1024)
-constexpr int kRowK = kHeadDim / 8 + 1;            // LDS K row: 16 chunks + 1 pad
-constexpr int kRowV = kKeyTile / 8 + 1;            // LDS V^T row: 8 chunks + 1 pad
-constexpr int kBufK = kKeyTile * kRowK;            // 1088 chunks
-constexpr int kBufV = kHeadDim * kRowV;            // 1152 chunks
-constexpr int kDmaK = kBufK / 64;                  // DMA instructions per K tile (17)
-constexpr int kDmaV = kBufV / 64;                  // DMA instructions per V^T tile (18)
-constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 70 KiB
-static_assert(kBufK % 64 == 0 && kBufV % 64 == 0, "DMA windows cover whole buffers");
+constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 70 KiB: two K and two V^T buffers
 constexpr float kRescaleSlack = 8.0f;              // exp2 units
 constexpr float kLn2 = 0.69314718055994531f;
 
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
-
-// Two fp32 values to a packed bf16 pair, round-to-nearest-even.
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  const f32x2 v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
-
-__device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
-
-__device__ __forceinline__ int64_t uniform64(int64_t v) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-// Global sources of this thread's lane in the LDS DMA of a tile.  DMA
-// instruction j writes buffer chunks 64j .. 64j+63; wave w issues j = w + 8x
-// (x = 0..2, while j < kDmaK or kDmaV).  Lane L of instruction j fills chunk
-// p = 64j + L: K row p / 17, chunk min(p % 17, 15); V^T row p / 9, chunk
-// min(p % 9, 7).  Addresses are a wave-uniform base plus a 32-bit per-lane
-// byte offset.
-struct Dma {
-  const char* kbase;  // K of this kv-head at the sequence start (uniform)
-  int64_t k_tile;     // bytes between consecutive key tiles (uniform)
-  int64_t len;        // sequence length
-  const char* klast;  // the sequence's last key row (uniform)
-  uint32_t koff[3];   // per-lane byte offset of the chunk within a tile
-  uint32_t kcol[3];   // per-lane byte offset of the chunk within its row
-  int krow[3];        // tile row of the lane's chunk
-  const char* vbase;  // packed V^T tile 0 (uniform)
-  uint32_t voff[3];
-  int wave;           // wave-uniform
-};
-
-__device__ __forceinline__ void dma_k1(const Dma& D, const char* tile, bool tail, int64_t base,
-                                       u32x4* buf, int x) {
-  const char* src = tile + D.koff[x];
-  // rows past the sequence end repeat its last key; they are always masked
-  if (tail && base + D.krow[x] >= D.len) src = D.klast + D.kcol[x];
-  __builtin_amdgcn_global_load_lds(src, buf + 64 * (D.wave + 8 * x), 16, 0, 0);
-}
-
-__device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
-  const int64_t base = (int64_t)i * kKeyTile;
-  const char* tile = D.kbase + (int64_t)i * D.k_tile;
-  if (base + kKeyTile <= D.len) {
-    dma_k1(D, tile, false, base, buf, 0);
-    dma_k1(D, tile, false, base, buf, 1);
-    if (D.wave + 16 < kDmaK) dma_k1(D, tile, false, base, buf, 2);
-  } else {
-    dma_k1(D, tile, true, base, buf, 0);
-    dma_k1(D, tile, true, base, buf, 1);
-    if (D.wave + 16 < kDmaK) dma_k1(D, tile, true, base, buf, 2);
-  }
-}
-
-__device__ __forceinline__ void dma_v1(const Dma& D, const char* tile, u32x4* buf, int x) {
-  __builtin_amdgcn_global_load_lds(tile + D.voff[x], buf + 64 * (D.wave + 8 * x), 16, 0, 0);
-}
-
-__device__ __forceinline__ void dma_v(const Dma& D, int i, u32x4* buf) {
-  const char* tile = D.vbase + (int64_t)i * (kChunksV * 16);
-  dma_v1(D, tile, buf, 0);
-  dma_v1(D, tile, buf, 1);
-  if (D.wave + 16 < kDmaV) dma_v1(D, tile, buf, 2);
-}
-
-// Wait for this wave's LDS DMA (and everything else) before a barrier.
-__device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0); }
-
-// Lane read bases (chunks) into a K and a V^T buffer: K row 32*th + qc,
-// chunk 2kk + hh is kq + 32*kRowK*th + 2kk; V^T row 32*dt + qc, chunk
-// 2st + hh is vq + 32*kRowV*dt + 2st.
-struct ReadOff {
-  int kq;
-  int vq;
-};
-
-// Operand reads run kPre MFMAs ahead of their use: the first kPre LDS reads,
-// then one MFMA and one read alternately, then the last kPre MFMAs (pinned
-// with scheduling groups, so the LDS latency hides behind the matrix core).
-constexpr int kPre = 6;
-
-__device__ __forceinline__ void pin_pipeline() {
-  __builtin_amdgcn_sched_group_barrier(0x100, kPre, 0);
-#pragma unroll
-  for (int j = 0; j < 16 - kPre; j++) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
-}
-
-// S^T: 16 MFMAs from the K buffer at kb.
-__device__ __forceinline__ void qk(f32x16 (&s)[2], const u32x4* kb, const ReadOff& ro,
-                                   const bf16x8 (&qf)[8]) {
-#pragma unroll
-  for (int th = 0; th < 2; th++)
-#pragma unroll
-    for (int r = 0; r < 16; r++) s[th][r] = 0.0f;
-  const u32x4* k = kb + ro.kq;
-  u32x4 op[16];
-#pragma unroll
-  for (int j = 0; j < 16; j++) op[j] = k[32 * kRowK * (j & 1) + 2 * (j >> 1)];
-#pragma unroll
-  for (int j = 0; j < 16; j++) s[j & 1] = mfma(as_bf16x8(op[j]), qf[j >> 1], s[j & 1]);
-  pin_pipeline();
-}
-
-// O^T += V^T . P^T: 16 MFMAs from the V^T buffer at vb.
-__device__ __forceinline__ void pv(f32x16 (&o)[4], const u32x4* vb, const ReadOff& ro,
-                                   const bf16x8 (&pb)[4]) {
-  const u32x4* v = vb + ro.vq;
-  u32x4 op[16];
-#pragma unroll
-  for (int j = 0; j < 16; j++) op[j] = v[32 * kRowV * (j & 3) + 2 * (j >> 2)];
-#pragma unroll
-  for (int j = 0; j < 16; j++) o[j & 3] = mfma(as_bf16x8(op[j]), pb[j >> 2], o[j & 3]);
-  pin_pipeline();
-}
-
-struct RowInfo {
-  int64_t t;
-  int h;
-  bool valid;
-  int64_t dst;  // partial index (history) or chunk-relative row (current block)
-};
-
 // Masking and online softmax of S(i); the weights leave as bf16 P^T operands
 // pb[2*th + s2] (keys 32*th + 16*s2 .. +15).
-// On edge tiles only keys k of the tile with lo <= k < hi are kept; lo and
-// hi come relative to this lane's key offset 4*hh, so each element compares
-// a compile-time constant with a lane value.
-__device__ __forceinline__ void mask_keys(f32x16 (&s)[2], int lo, int hi) {
-#pragma unroll
-  for (int th = 0; th < 2; th++)
-#pragma unroll
-    for (int r = 0; r < 16; r++) {
-      const int k = 32 * th + 8 * (r >> 2) + (r & 3);
-      s[th][r] = (k >= lo && k < hi) ? s[th][r] : -INFINITY;
-    }
-}
-
 template <int MODE>
 __device__ __forceinline__ void softmax(f32x16 (&s)[2], float& m, float& l, f32x16 (&o)[4],
                                         bf16x8 (&pb)[4], bool edge, int lo, int hi, float c2) {

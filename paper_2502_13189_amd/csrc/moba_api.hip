@@ -12,6 +12,7 @@
 // partials: bf16 on the bf16 path, fp32 on the fp32 path) is what the
 // workspace cap limits.
 #include "moba.h"
+#include "bwd_internal.h"
 #include "moba_internal.h"
 
 #include <algorithm>
@@ -175,6 +176,7 @@ struct Plan {
   Problem p{};
   std::vector<SeqInfo> seqs;
   std::vector<CausalTile> tiles;
+  std::vector<KeyTile> ktiles;  // key tiles of the dK/dV kernel (kTilesCur plans)
   int64_t hist_per_head = 0;  // history selections of one query head, summed over tokens
 };
 
@@ -234,6 +236,7 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
   p.hist_entries = hist * Hq;
 
   pl->tiles.clear();
+  pl->ktiles.clear();
   if (mode == kTilesNone) return;
   const int tt = std::max(1, tile_rows / p.G);  // tokens per causal tile
   if (mode == kTilesCur) {
@@ -274,6 +277,19 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
     for (size_t k = 0; k < n; k++)
       for (int x = 0; x < kXcd; x++)
         pl->tiles.push_back(k < lists[x].size() ? lists[x][k] : CausalTile{0, 0, 0, 0});
+    // dK/dV key tiles: local block 0 of every sequence first (early blocks
+    // collect the longest routed row lists), then block 1, ...
+    for (int j = 0; j < nbmax; j++)
+      for (int s = 0; s < S; s++) {
+        const int64_t L = (int64_t)cu[s + 1] - cu[s];
+        const int64_t b0 = (int64_t)j * B;
+        if (b0 >= L) continue;
+        const int64_t b1 = std::min(L, b0 + B);
+        for (int64_t k0 = b0; k0 < b1; k0 += kKeysPerDkdv)
+          pl->ktiles.push_back(KeyTile{pl->seqs[s].blk_off + j, (int32_t)(cu[s] + k0),
+                                       (int32_t)(cu[s] + std::min(b1, k0 + kKeysPerDkdv)),
+                                       (int32_t)(cu[s] + b1)});
+      }
     return;
   }
   for (int s = 0; s < S; s++) {
@@ -334,14 +350,16 @@ moba_status ensure_workspace(DevCache* dc, size_t bytes) {
 // because kernels of earlier calls may still read the old tables.
 moba_status get_plan(DevCache* dc, const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk,
                      TileMode mode, int tile_rows, const Plan** out, const SeqInfo** d_seqs,
-                     const CausalTile** d_tiles) {
+                     const CausalTile** d_tiles, const KeyTile** d_ktiles = nullptr) {
   std::vector<int64_t> key = {Hq, Hkv, B, topk, mode, tile_rows, (int64_t)cu.size()};
   key.insert(key.end(), cu.begin(), cu.end());
   if (key != dc->tab_key || !dc->tab) {
     Plan pl;
     build_plan(cu, Hq, Hkv, B, topk, mode, tile_rows, &pl);
     const size_t sb = pl.seqs.size() * sizeof(SeqInfo);
-    const size_t need = ((sb + kAlign - 1) / kAlign) * kAlign + pl.tiles.size() * sizeof(CausalTile) + kAlign;
+    const size_t tb = pl.tiles.size() * sizeof(CausalTile);
+    const size_t need = ((sb + kAlign - 1) / kAlign) * kAlign + ((tb + kAlign - 1) / kAlign) * kAlign +
+                        pl.ktiles.size() * sizeof(KeyTile) + kAlign;
     if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
     if (need > dc->tab_bytes) {
       if (dc->tab) (void)hipFree(dc->tab);
@@ -362,14 +380,23 @@ moba_status get_plan(DevCache* dc, const std::vector<int32_t>& cu, int Hq, int H
         hipMemcpy(base + toff, pl.tiles.data(), pl.tiles.size() * sizeof(CausalTile),
                   hipMemcpyHostToDevice) != hipSuccess)
       return MOBA_ERR_HIP;
+    const size_t koff = toff + ((tb + kAlign - 1) / kAlign) * kAlign;
+    if (!pl.ktiles.empty() &&
+        hipMemcpy(base + koff, pl.ktiles.data(), pl.ktiles.size() * sizeof(KeyTile),
+                  hipMemcpyHostToDevice) != hipSuccess)
+      return MOBA_ERR_HIP;
     dc->plan = std::move(pl);
     dc->tab_key = std::move(key);
   }
   const size_t sb = dc->plan.seqs.size() * sizeof(SeqInfo);
+  const size_t tb = dc->plan.tiles.size() * sizeof(CausalTile);
+  const size_t toff = ((sb + kAlign - 1) / kAlign) * kAlign;
   *out = &dc->plan;
   *d_seqs = static_cast<const SeqInfo*>(dc->tab);
-  *d_tiles = reinterpret_cast<const CausalTile*>(static_cast<char*>(dc->tab) +
-                                                 ((sb + kAlign - 1) / kAlign) * kAlign);
+  *d_tiles = reinterpret_cast<const CausalTile*>(static_cast<char*>(dc->tab) + toff);
+  if (d_ktiles)
+    *d_ktiles = reinterpret_cast<const KeyTile*>(static_cast<char*>(dc->tab) + toff +
+                                                 ((tb + kAlign - 1) / kAlign) * kAlign);
   return MOBA_OK;
 }
 
@@ -561,6 +588,151 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
       Phase ph("attn_cur_merge", stream);
       MOBA_LAUNCH(launch_attn_causal_f32(false, a, p, stream));
     }
+  }
+  return MOBA_OK;
+}
+
+moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                          const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                          const moba_tensor* out, const moba_tensor* lse, const moba_tensor* dout,
+                          moba_tensor* dq, moba_tensor* dk, moba_tensor* dv, hipStream_t stream) {
+  Inputs in;
+  View vo, vdo, vdq, vdk, vdv;
+  moba_status st = check_inputs(q, k, v, cu_seqlens, out, lse, &in, &vo);
+  if (st != MOBA_OK) return st;
+  if (!in.bf16) return MOBA_ERR_DTYPE;
+  if (missing(dout) || missing(dq) || missing(dk) || missing(dv)) return MOBA_ERR_NULL;
+  if ((st = check_3d(dout, MOBA_BF16, &vdo)) != MOBA_OK) return st;
+  if ((st = check_3d(dq, MOBA_BF16, &vdq)) != MOBA_OK) return st;
+  if ((st = check_3d(dk, MOBA_BF16, &vdk)) != MOBA_OK) return st;
+  if ((st = check_3d(dv, MOBA_BF16, &vdv)) != MOBA_OK) return st;
+  if (dout->shape[0] != in.T || dq->shape[0] != in.T || dk->shape[0] != in.T ||
+      dv->shape[0] != in.T)
+    return MOBA_ERR_SHAPE;
+  if (vdo.H != in.Hq || vdq.H != in.Hq || vdk.H != in.Hkv || vdv.H != in.Hkv) return MOBA_ERR_SHAPE;
+  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (topk < 1) return MOBA_ERR_TOPK;
+  if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
+  if (in.T == 0) return MOBA_OK;
+
+  int64_t nbmax = 0;
+  for (size_t s = 0; s + 1 < in.cu.size(); s++)
+    nbmax = std::max<int64_t>(nbmax, ceil_div((int64_t)in.cu[s + 1] - in.cu[s], block_size));
+  if (nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
+  const int kk = (int)std::min<int64_t>(topk, nbmax);
+  if (kk - 1 > 63 && kk - 1 < nbmax - 1) return MOBA_ERR_UNSUPPORTED;
+  if ((uint64_t)in.T * in.Hq * (uint64_t)std::max(kk - 1, 1) >= (uint64_t(1) << 32))
+    return MOBA_ERR_UNSUPPORTED;
+
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  const KeyTile* d_ktiles;
+  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur, kTileRowsMfma, &pl,
+                     &d_seqs, &d_tiles, &d_ktiles)) != MOBA_OK)
+    return st;
+  const Problem& p = pl->p;
+  const int64_t kh = kk - 1;
+  const int64_t TG = p.T * p.G;
+  const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;
+  const bool routed = kh > 0 && p.hist_entries > 0;
+
+  struct Bufs {
+    float* kbar; __hip_bfloat16* kt; int32_t* sel; RouteBuffers rb; float2* ld; int4* rec;
+    float* dq_part;
+  };
+  auto layout = [&](int nch, Bump* bp, Bufs* b) {
+    b->kbar = bp->take<float>((int64_t)p.nblk_total * p.Hkv * kHeadDim);
+    b->kt = bp->take<__hip_bfloat16>((int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim);
+    b->sel = bp->take<int32_t>(p.T * p.Hq * kk);
+    b->rb.hist = bp->take<int32_t>((int64_t)p.Hkv * p.hist_words);
+    b->rb.bin_count = bp->take<int32_t>(nbins);
+    b->rb.bin_start = bp->take<int64_t>(nbins + 1);
+    b->rb.bin_tile_start = bp->take<int32_t>(nbins + 1);
+    b->rb.entries = bp->take<uint32_t>(p.hist_entries);
+    b->ld = bp->take<float2>(p.T * p.Hq);
+    b->rec = bp->take<int4>(routed ? p.hist_entries : 0);
+    b->dq_part = bp->take<float>(routed ? (int64_t)nch * TG * kh * kHeadDim : 0);
+  };
+  const size_t limit = workspace_limit();
+  int nch = 0;
+  size_t need = 0;
+  for (int n = p.Hkv; n >= 1; n--) {
+    Bump bp(nullptr);
+    Bufs b{};
+    layout(n, &bp, &b);
+    if (bp.off + kAlign <= limit) { nch = n; need = bp.off + kAlign; break; }
+  }
+  if (nch == 0) return MOBA_ERR_NO_MEMORY;
+  nch = (int)ceil_div(p.Hkv, ceil_div(p.Hkv, nch));
+  if ((st = ensure_workspace(dc, need)) != MOBA_OK) return st;
+  Bump bp(dc->ws);
+  Bufs b{};
+  layout(nch, &bp, &b);
+
+  BwdArgs a{};
+  a.q = in.q.data; a.q_st = in.q.st; a.q_sh = in.q.sh;
+  a.k = in.k.data; a.k_st = in.k.st; a.k_sh = in.k.sh;
+  a.v = in.v.data; a.v_st = in.v.st; a.v_sh = in.v.sh;
+  a.o = vo.data; a.o_st = vo.st; a.o_sh = vo.sh;
+  a.dout = vdo.data; a.do_st = vdo.st; a.do_sh = vdo.sh;
+  a.lse = static_cast<const float*>(lse->data);
+  a.dq = vdq.data; a.dq_st = vdq.st; a.dq_sh = vdq.sh;
+  a.dk = vdk.data; a.dk_st = vdk.st; a.dk_sh = vdk.sh;
+  a.dv = vdv.data; a.dv_st = vdv.st; a.dv_sh = vdv.sh;
+  a.kt = b.kt;
+  a.seqs = d_seqs;
+  if (routed) {
+    a.bin_tile_start = b.rb.bin_tile_start;
+    a.bin_start = b.rb.bin_start;
+    a.bin_count = b.rb.bin_count;
+    a.entries = b.rb.entries;
+  }
+  a.ld = b.ld;
+  a.rec = b.rec;
+  a.dq_part = b.dq_part;
+  a.tiles = d_tiles;
+  a.ntiles = (int64_t)pl->tiles.size();
+  a.ktiles = d_ktiles;
+  a.nktiles = (int64_t)pl->ktiles.size();
+  a.scale = (float)(1.0 / std::sqrt((double)kHeadDim));
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)kHeadDim));
+
+  // the forward's selection and routing, recomputed
+  { Phase ph("pool", stream);
+    MOBA_LAUNCH(launch_pool(in.k.data, true, in.k.st, in.k.sh, d_seqs, p, b.kbar, stream)); }
+  { Phase ph("kt_pack", stream);
+    MOBA_LAUNCH(launch_vt_pack(static_cast<const __hip_bfloat16*>(in.k.data), in.k.st, in.k.sh,
+                               d_seqs, p, b.kt, stream)); }
+  { Phase ph("gate", stream);
+    MOBA_LAUNCH(launch_gate(in.q.data, true, in.q.st, in.q.sh, b.kbar, d_seqs, p, b.sel, nullptr, 0,
+                            stream)); }
+  if (routed) {
+    Phase ph("route", stream);
+    MOBA_LAUNCH(launch_route(b.sel, d_seqs, p, b.rb, stream));
+  }
+  { Phase ph("bwd_delta", stream);
+    MOBA_LAUNCH(launch_bwd_delta(a, p, stream)); }
+  if (routed) {
+    Phase ph("bwd_rec", stream);
+    MOBA_LAUNCH(launch_bwd_rec(a, p, stream));
+  }
+  { Phase ph("bwd_dkdv", stream);
+    MOBA_LAUNCH(launch_bwd_dkdv(a, p, stream)); }
+  for (int g0 = 0; g0 < p.Hkv; g0 += nch) {
+    a.g0 = g0;
+    a.g1 = std::min(p.Hkv, g0 + nch);
+    const int64_t e_chunk = pl->hist_per_head * p.G * (a.g1 - a.g0);
+    if (routed && e_chunk > 0) {
+      const int64_t grid = ceil_div(e_chunk, kTileRowsMfma) + (int64_t)(a.g1 - a.g0) * p.nblk_total;
+      Phase ph("bwd_dq_hist", stream);
+      MOBA_LAUNCH(launch_bwd_dq_hist(a, p, grid, stream));
+    }
+    Phase ph("bwd_dq_cur", stream);
+    MOBA_LAUNCH(launch_bwd_dq_cur(a, p, stream));
   }
   return MOBA_OK;
 }

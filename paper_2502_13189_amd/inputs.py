@@ -150,6 +150,23 @@ def make_chunked(seqlens, hq: int, hkv: int, d: int, dtype, block_size: int,
     return q, k, v, cu_seqlens(seqlens)
 
 
+def make_dout(shape, dtype, seed: int = 0, device="cpu", chunk_tokens: int = 1 << 18):
+    """Upstream gradient dL/d(out) for the backward pass: entries i.i.d.
+    N(0, 1), drawn in fp32 in chunks of chunk_tokens rows of `shape` =
+    (T, Hq, D), chunk c from a generator seeded with seed * 7919 + c + 17, and
+    rounded once to `dtype`."""
+    T = int(shape[0])
+    dev = torch.device(device)
+    out = torch.empty(tuple(shape), device=dev, dtype=dtype)
+    for c, t0 in enumerate(range(0, T, chunk_tokens)):
+        t1 = min(T, t0 + chunk_tokens)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(int(seed) * 7919 + c + 17)
+        out[t0:t1].copy_(torch.randn((t1 - t0,) + tuple(shape[1:]), generator=gen, device=dev,
+                                     dtype=torch.float32))
+    return out
+
+
 # Sweeps, 32 query / 8 kv heads, D = 128, bf16, key offsets N(0, 0.5^2),
 # chunked generation; points are (tokens, block size, top-k):
 #   fig2a: 8K .. 1M tokens at block size 4096 and top-12 (the 1M model's

@@ -184,3 +184,56 @@ def dense_parity(q, k, v, cu, rows=None, dtype="bf16"):
     gout, glse = gather_rows(out, lse, rows)
     mx, mean, lmx = compare_outputs(gout, glse, oout, olse, dtype, "dense")
     return {"rows": len(rows), "max_abs": mx, "mean_abs": mean, "lse_max_abs": lmx}
+
+
+# Backward tolerances (bf16).  bf16 rounding has unit roundoff u = 2^-8.  The
+# kernels round each P and dS term to bf16 once (<= u relative), use Delta =
+# <dO, O> with the forward's bf16 O (whose error stays within ~3u per element
+# after the partial rounding and the merge), accumulate in fp32 (negligible
+# here) and round the result once (<= u).  So every gradient element obeys
+#   |err| <= 3u (|ref| + c),
+# c the oracle's sum of absolute terms (cq, ck, cv of attend_backward); the
+# elementwise bound below is 4u.  It is a worst case; a systematic error (a
+# dropped block, a wrong mask) shows in the mean instead, bounded by
+# BWD_MEAN_REL of the mean |ref| (the random-walk rounding error observed is
+# about u / 2 of it).
+BWD_ELEM_U = 4.0 * 2.0 ** -8
+BWD_MEAN_REL = 2.0 ** -7
+
+
+def moba_backward_parity(q, k, v, cu, B, topk, dout, exact_sel=False):
+    """Run forward + backward on the GPU and the oracle's fp64 gradients on the
+    selection the GPU made (oracle selection; tie-explained rows take the GPU's
+    order, as in moba_parity).  Asserts the backward tolerances and returns,
+    per gradient, (max of |err| / (|ref| + c), mean |err| / mean |ref|)."""
+    cu_t = cu if isinstance(cu, torch.Tensor) else torch.tensor(cu, dtype=torch.int32)
+    out, lse = binding.forward(q, k, v, cu_t, B, topk)
+    dq, dk, dv = binding.backward(q, k, v, cu_t, B, topk, out, lse, dout)
+    gsel = binding.select(q, k, cu_t, B, topk)
+    torch.cuda.synchronize()
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    rows = np.arange(T * Hq, dtype=np.int64)
+    qn, kn, vn = host_inputs(q, k, v)
+    dn = inputs.to_oracle(dout)
+    cun = cu_t.numpy()
+    gs = gsel.view(T * Hq, topk).cpu().numpy()
+    osel, bad = check_selection(gs, rows, qn, kn, cun, B, topk, exact_sel)
+    use_sel = osel.copy()
+    use_sel[bad] = gs[bad]
+    odq, odk, odv, cq, ck, cv = oracle.attend_backward(qn, kn, vn, dn, cun, B, use_sel,
+                                                       kv_window="all", with_bounds=True)
+    res = {"tie_rows": int(bad.size)}
+    for name, g, ref, c in (("dq", dq, odq, cq), ("dk", dk, odk, ck), ("dv", dv, odv, cv)):
+        g = g.float().cpu().numpy().astype(np.float64).reshape(ref.shape)
+        assert np.isfinite(g).all(), "%s has non-finite values" % name
+        err = np.abs(g - ref)
+        ratio = err / (np.abs(ref) + c + 1e-30)
+        worst = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
+        mean_rel = float(err.mean() / max(np.abs(ref).mean(), 1e-30))
+        res[name] = (float(ratio.max()), mean_rel)
+        assert ratio.max() <= BWD_ELEM_U, ("%s element %s: |err| %.3e > %.3g (|ref| + c) with ref "
+                                           "%.3e, c %.3e" % (name, worst, err[worst], BWD_ELEM_U,
+                                                             ref[worst], c[worst]))
+        assert mean_rel <= BWD_MEAN_REL, "%s mean |err| %.3e of mean |ref|" % (name, mean_rel)
+    return res

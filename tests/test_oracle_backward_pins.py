@@ -238,3 +238,37 @@ def test_backward_scale_is_inverse_sqrt_d():
     np.testing.assert_allclose(dq[1], want, rtol=0, atol=1e-14)
     np.testing.assert_allclose(dq[0], 0.0, atol=0)  # token 0 has zero upstream gradient
     np.testing.assert_allclose(dv[:, 0], np.outer([p0, p1], g), rtol=0, atol=1e-14)
+
+
+def test_backward_bound_sums():
+    """The absolute-term sums behind the backward tolerances: each bounds its
+    gradient (triangle inequality), and for a dense tiny problem they equal
+    the sums written out from softmax weights computed here with torch."""
+    qn, kn, vn, dn, cu = rand_case((9,), 2, 1, 4, 3, seed=35)
+    T, Hq, D = qn.shape
+    kbar = oracle.pool(kn, cu, 3)
+    sel = oracle.select(qn, kbar, cu, 3, 3)  # 3 blocks of 3: every causal key
+    dq, dk, dv, cq, ck, cv = oracle.attend_backward(qn, kn, vn, dn, cu, 3, sel, kv_window="all",
+                                                    with_bounds=True)
+    assert np.all(cq >= np.abs(dq) - 1e-15)
+    assert np.all(ck >= np.abs(dk) - 1e-15) and np.all(cv >= np.abs(dv) - 1e-15)
+    q, k, v, g = (_f64(x) for x in (qn, kn, vn, dn))
+    s = 1.0 / math.sqrt(D)
+    want_cq = torch.zeros(T, Hq, D, dtype=torch.float64)
+    want_ck = torch.zeros(T, 1, D, dtype=torch.float64)
+    want_cv = torch.zeros(T, 1, D, dtype=torch.float64)
+    for t in range(T):
+        for h in range(Hq):
+            kk, vv = k[: t + 1, 0], v[: t + 1, 0]
+            p = torch.softmax(kk @ q[t, h] * s, dim=0)
+            o = p @ vv
+            dp = vv @ g[t, h]
+            dz = p * (dp - (p * dp).sum())
+            drow = (g[t, h].abs() * o.abs()).sum()
+            az = dz.abs() + p * drow
+            want_cq[t, h] = s * (az[:, None] * kk.abs()).sum(0)
+            want_ck[: t + 1, 0] += s * az[:, None] * q[t, h].abs()[None, :]
+            want_cv[: t + 1, 0] += p[:, None] * g[t, h].abs()[None, :]
+    np.testing.assert_allclose(cq.reshape(T, Hq, D), want_cq.numpy(), rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(ck, want_ck.numpy(), rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(cv, want_cv.numpy(), rtol=1e-12, atol=1e-15)
