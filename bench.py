@@ -2,6 +2,7 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--dense-steps N] [--no-cpu]
     python bench.py --sweep fig2a|fig2b|gran [--sweep-steps K] [--sweep-lengths L1,L2,..]
+    python bench.py --backward [--steps K] [--warmup W] [--workload NAME]
 
 One step = one moba_forward call over the whole workload (pool, gate, route,
 history and current-block attention, merge), inputs resident in HBM.  The
@@ -202,6 +203,66 @@ def run_sweep(args):
         torch.cuda.empty_cache()
 
 
+def run_backward(args):
+    """The backward pass (moba_backward) on the workload: one JSON line with
+    its time and rates.  Algorithmic FLOPs count the five products of the
+    attention backward (S recomputed, dP, dV, dK, dQ: 10*D per attended
+    query-key pair, 2.5x the forward's); the kernels execute seven (S and dP
+    are computed on both the query and the key side)."""
+    w = inputs.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    print("[bench] generating %s" % w.name, file=sys.stderr, flush=True)
+    q, k, v, cu = inputs.make_workload(w, device=dev)
+    dout = inputs.make_dout(q.shape, q.dtype, w.seed, device=dev)
+    out, lse = binding.forward(q, k, v, cu, w.block_size, w.topk)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    torch.cuda.synchronize()
+
+    def step():
+        binding.backward(q, k, v, cu, w.block_size, w.topk, out, lse, dout, dq=dq, dk=dk, dv=dv)
+
+    print("[bench] backward warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("[bench] backward timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    binding.profile_read()
+    binding.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    binding.profile_enable(False)
+    phases = binding.profile_read()
+    cur, hist, _ = attended_keys(w.seqlens, w.block_size, w.topk)
+    pairs = w.hq * (cur + hist)
+    flop = 10.0 * w.d * pairs
+    tflops = flop / (ms * 1e-3) / 1e12
+
+    def kernel_rate(name, kflop):
+        """Executed TFLOP/s of a phase: kflop per step over its time per step."""
+        n, t = phases.get(name, (0, 0.0))
+        return None if not n else round(kflop / (t / args.steps * 1e-3) / 1e12, 2)
+
+    # executed products per kernel: dq history 3 (S, dP, dQ) over history
+    # pairs; dq current 3 over current-block pairs; dkdv 4 (S, dP, dV, dK)
+    # over all pairs
+    rates = {
+        "bwd_dq_hist": kernel_rate("bwd_dq_hist", 6.0 * w.d * w.hq * hist),
+        "bwd_dq_cur": kernel_rate("bwd_dq_cur", 6.0 * w.d * w.hq * cur),
+        "bwd_dkdv": kernel_rate("bwd_dkdv", 8.0 * w.d * pairs),
+    }
+    print(json.dumps({
+        "mode": "backward", "workload": w.name, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 3), "algorithmic_flop": flop, "tflops": round(tflops, 2),
+        "pct_bf16_peak": round(100.0 * tflops / BF16_PEAK_TFLOPS, 2), "dtype": "bf16",
+        "data": "synthetic",
+        "phases_ms_per_step": {n: round(t / args.steps, 3) for n, (c, t) in phases.items()},
+        "executed_tflops_per_kernel": rates,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,6 +278,8 @@ def main():
     ap.add_argument("--sweep-steps", type=int, default=2)
     ap.add_argument("--sweep-lengths", default=None, help="comma-separated subset of lengths")
     ap.add_argument("--sweep-dense-max", type=int, default=1 << 20)
+    ap.add_argument("--backward", action="store_true",
+                    help="time moba_backward on the workload instead (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -229,6 +292,9 @@ def main():
     binding.load()
     if args.sweep:
         run_sweep(args)
+        return
+    if args.backward:
+        run_backward(args)
         return
     w = inputs.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")

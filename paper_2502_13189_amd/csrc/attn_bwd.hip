@@ -19,12 +19,14 @@
 //          tile and wave: S^T = K . Q^T and dP^T = V . dO^T (K and V
 //          row-major from LDS, Q^T and dO^T operands in registers), then
 //          dQ^T += K^T . dS^T from the packed K^T tile: 48 MFMAs.
-//   dkdv   key side: a work-group owns 256 keys of one block and kv-head
+//   dkdv   key side: a work-group (4 waves, one per SIMD, so each wave may
+//          hold 512 registers) owns 128 keys of one block and kv-head
 //          (wave w: 32 keys, with K, V, dK^T and dV^T in registers) and
 //          loops over every row that attends them, 64 rows at a time: the
 //          bin's routed history rows, then the block's own rows (causal).
-//          The rows' Q and dO arrive by LDS DMA, gathered row by row, and are
-//          transposed once per chunk inside LDS.  Per 32-row subtile and
+//          The rows' Q and dO arrive by LDS DMA, gathered row by row, into a
+//          swizzled row-major layout that also serves the transposed
+//          operands (ds_read_b64_tr_b16).  Per 32-row subtile and
 //          wave: S = Q . K^T, dP = dO . V^T, then dV^T += dO^T . P and
 //          dK^T += Q^T . dS: 32 MFMAs.  Each key has one owner, so dK and dV
 //          need neither atomics nor a merge.
@@ -108,26 +110,79 @@ __global__ __launch_bounds__(256) void bwd_rec_kernel(BwdArgs a, Problem p) {
 }
 
 // ================================================================ dQ
-// dS^T of a 64-key tile from S^T and dP^T, as bf16 operands db[2*th + s2]
-// (keys 32*th + 16*s2 .. +15, the order of the packed K^T tile).
-__device__ __forceinline__ void grad_scores(f32x16 (&s)[2], const f32x16 (&dp)[2], bf16x8 (&db)[4],
-                                            bool edge, int lo, int hi, float c2, float lse2,
-                                            float dlt) {
-  if (edge) mask_keys(s, lo, hi);
+// S^T and dP^T of keys 32*th .. 32*th+31 of a 64-key tile: 8 k-steps each
+// from the row-major K and V buffers, the two accumulation chains
+// interleaved, operand reads kPre MFMAs ahead.
+__device__ __forceinline__ void sdp_half(f32x16& s, f32x16& dp, const u32x4* kb, const u32x4* vb,
+                                         const ReadOff& ro, int th, const bf16x8 (&qf)[8],
+                                         const bf16x8 (&df)[8]) {
 #pragma unroll
-  for (int th = 0; th < 2; th++)
+  for (int r = 0; r < 16; r++) {
+    s[r] = 0.0f;
+    dp[r] = 0.0f;
+  }
+  const u32x4* k = kb + ro.kq + 32 * kRowK * th;
+  const u32x4* v = vb + ro.kq + 32 * kRowK * th;
+  u32x4 op[16];
 #pragma unroll
-    for (int s2 = 0; s2 < 2; s2++) {
-      uint32_t w[4];
+  for (int j = 0; j < 16; j++) op[j] = (j & 1) ? v[2 * (j >> 1)] : k[2 * (j >> 1)];
 #pragma unroll
-      for (int e = 0; e < 4; e++) {
-        const int i0 = 8 * s2 + 2 * e, i1 = i0 + 1;
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[th][i0], c2, -lse2));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[th][i1], c2, -lse2));
-        w[e] = pack_bf16(p0 * (dp[th][i0] - dlt), p1 * (dp[th][i1] - dlt));
+  for (int j = 0; j < 16; j++) {
+    if (j & 1) dp = mfma(as_bf16x8(op[j]), df[j >> 1], dp);
+    else s = mfma(as_bf16x8(op[j]), qf[j >> 1], s);
+  }
+  pin_pipeline();
+}
+
+// dS^T = P^T (dP^T - Delta), P^T = exp2(S^T c2 - lse2), for keys 32*th ..
+// 32*th+31 of the tile, as the bf16 operands db[2*th + s2] (keys 32*th +
+// 16*s2 .. +15, the key order of the packed K^T tile).  On edge tiles only
+// keys lo <= k < hi (relative to this lane's key offset 4*hh) are kept.
+__device__ __forceinline__ void grad_half(const f32x16& s, const f32x16& dp, bf16x8 (&db)[4], int th,
+                                          bool edge, int lo, int hi, float c2, float lse2,
+                                          float dlt) {
+#pragma unroll
+  for (int s2 = 0; s2 < 2; s2++) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+      float d[2];
+#pragma unroll
+      for (int u = 0; u < 2; u++) {
+        const int i = 8 * s2 + 2 * e + u;
+        const int kk = 32 * th + 8 * (i >> 2) + (i & 3);
+        float p = __builtin_amdgcn_exp2f(fmaf(s[i], c2, -lse2));
+        if (edge) p = (kk >= lo && kk < hi) ? p : 0.0f;
+        d[u] = p * (dp[i] - dlt);
       }
-      db[2 * th + s2] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+      w[e] = pack_bf16(d[0], d[1]);
     }
+    db[2 * th + s2] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+  }
+}
+
+// Row-major V tiles for the DMA: the wave-uniform part; the per-lane
+// offsets are recomputed from K's rows and columns (V may have its own
+// token stride).
+struct VDma {
+  const char* base;
+  const char* last;
+  int64_t tile;
+  uint32_t st;  // token stride in bytes
+};
+
+__device__ __forceinline__ void dma_vrow(const Dma& D, const VDma& V, int i, u32x4* buf) {
+  const int64_t base = (int64_t)i * kKeyTile;
+  const char* tile = V.base + (int64_t)i * V.tile;
+  const bool tail = base + kKeyTile > D.len;
+#pragma unroll
+  for (int x = 0; x < 3; x++) {
+    if (x < 2 || D.wave + 16 < kDmaK) {
+      const char* src = tile + (D.krow[x] * V.st + D.kcol[x]);
+      if (tail && base + D.krow[x] >= D.len) src = V.last + D.kcol[x];
+      __builtin_amdgcn_global_load_lds(src, buf + 64 * (D.wave + 8 * x), 16, 0, 0);
+    }
+  }
 }
 
 constexpr int kDqStage = 2 * kBufK + kBufV;  // K, V (row-major), K^T (packed)
@@ -217,17 +272,20 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
   // ------------------------------------------------------------ key tiles
   const int64_t rb = kbeg - tok0, re = kend - tok0;
   const int i0 = (int)(rb / kKeyTile), i1 = (int)((re + kKeyTile - 1) / kKeyTile);
-  Dma DK, DV;  // DK: K row-major and the packed K^T; DV: V row-major
+  Dma DK;  // K row-major and the packed K^T
+  VDma DV;  // V row-major
   {
     const int wv = __builtin_amdgcn_readfirstlane(wave);
     const char* kb = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.k) +
                                                    (int64_t)g * a.k_sh) + tok0 * (a.k_st * 2);
-    const char* vb = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.v) +
-                                                   (int64_t)g * a.v_sh) + tok0 * (a.v_st * 2);
     const char* ktb = reinterpret_cast<const char*>(
         a.kt + ((int64_t)g * p.vt_tiles + sq.vt_tile_off) * (kKeyTile * kHeadDim));
     init_dma(DK, wv, lane, kb, a.k_st * 2, sq.len, ktb);
-    init_dma(DV, wv, lane, vb, a.v_st * 2, sq.len, nullptr);
+    DV.st = (uint32_t)(a.v_st * 2);
+    DV.base = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.v) +
+                                            (int64_t)g * a.v_sh) + tok0 * (a.v_st * 2);
+    DV.last = DV.base + (sq.len - 1) * (a.v_st * 2);
+    DV.tile = kKeyTile * (a.v_st * 2);
   }
   ReadOff ro;
   ro.kq = qc * kRowK + hh;
@@ -241,7 +299,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
 
   // stage x: K at lds + x*kDqStage, V at + kBufK, K^T at + 2*kBufK
   dma_k(DK, i0, lds);
-  dma_k(DV, i0, lds + kBufK);
+  dma_vrow(DK, DV, i0, lds + kBufK);
   dma_v(DK, i0, lds + 2 * kBufK);
   dma_wait();
   __syncthreads();
@@ -252,12 +310,9 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
     if (i + 1 < i1) {
       u32x4* nx = lds + (cur ^ 1) * kDqStage;
       dma_k(DK, i + 1, nx);
-      dma_k(DV, i + 1, nx + kBufK);
+      dma_vrow(DK, DV, i + 1, nx + kBufK);
       dma_v(DK, i + 1, nx + 2 * kBufK);
     }
-    f32x16 sc[2], dp[2];
-    qk(sc, st, ro, qf);
-    qk(dp, st + kBufK, ro, df);
     const int64_t u0 = tok0 + (int64_t)i * kKeyTile;
     const bool edge = u0 < kbeg || u0 + kKeyTile > kend || (MODE != kHist && u0 + kKeyTile - 1 > tmin);
     int lo = 0, hi = kKeyTile;
@@ -267,7 +322,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
       hi = (int)(MODE == kHist ? lim : min(lim, ri.t + 1 - u0)) - 4 * hh;
     }
     bf16x8 db[4];
-    grad_scores(sc, dp, db, edge, lo, hi, c2, ld.x, ld.y);
+#pragma unroll
+    for (int th = 0; th < 2; th++) {
+      f32x16 sh, dh;
+      sdp_half(sh, dh, st, st + kBufK, ro, th, qf, df);
+      grad_half(sh, dh, db, th, edge, lo, hi, c2, ld.x, ld.y);
+    }
     pv(acc, st + 2 * kBufK, ro, db);
     dma_wait();
     __syncthreads();
@@ -322,19 +382,40 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
 }
 
 // ============================================================== dK, dV
-constexpr int kChunk = 64;                       // rows per chunk
-constexpr int kRowT = kChunk / 8 + 1;            // transposed row (one dim): 8 chunks + 1 pad
-constexpr int kBufR = kChunk * kRowK;            // row-major Q or dO chunk (1088)
-constexpr int kBufT = kHeadDim * kRowT;          // transposed Q or dO chunk (1152)
-constexpr int kDmaR = kBufR / 64;                // DMA instructions per row-major chunk (17)
-constexpr int kDkdvLds = 4 * kBufR + 2 * kBufT;  // Q, dO row-major x2, Q^T, dO^T: 104 KiB
-constexpr int kSlots = 3;                        // row tables in flight
+constexpr int kChunk = 64;          // rows per chunk
+constexpr int kBufR = kChunk * 16;  // one row-major Q or dO chunk: 64 rows x 16 16-byte chunks
+constexpr int kDmaR = kBufR / 64;   // DMA instructions per chunk and tensor (16)
+constexpr int kSlots = 3;           // row tables in flight
 
-// Position p (0..63) of a packed row order holds row perm(p) of the chunk
-// (the key order of the packed K^T / V^T tiles, applied to rows).
-__device__ __forceinline__ int packed_row(int p) {
-  const int grp = p & ~15, w = p & 15;
-  return grp + 8 * ((w & 7) >> 2) + 4 * (w >> 3) + (w & 3);
+// Swizzled row-major chunk: the logical 16-byte chunk c of row r is stored
+// at r*16 + (c ^ swz(r)), swz(r) = 4*(r % 4) + (r / 4) % 4.  Both reads of
+// the buffer are then free of LDS bank conflicts:
+//  - operand reads of S = Q K^T and dP = dO V^T: 16 lanes on 16 consecutive
+//    rows at one logical chunk (swz takes 16 distinct values there);
+//  - transposed reads (ds_read_b64_tr_b16) for dV^T += dO^T P and
+//    dK^T += Q^T dS: per 32 lanes, 4 consecutive rows (starting at a multiple
+//    of 4) by the 4 logical chunks of 32 dims; the rows' swz differ in bits
+//    2-3, so their 64-byte windows are disjoint.
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives element
+// i % 4 of the 8-byte pieces addressed by lanes 4e + i / 4 (e = 0..3).  If
+// lane j of the group addresses row r0 + j/4 at dims d0 + 4 (j % 4), lane i
+// receives dims d0 + i of rows r0 .. r0+3: four consecutive rows of one
+// dimension, the transposed operand.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ s16x4 tr_read(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+}
+
+// A operand [dims x rows] of one k = 16 step from a swizzled chunk buffer:
+// rows r0 .. r0+3 and r0+8 .. r0+11 (the packed row order of the P and dS
+// operands), one dimension per lane.
+__device__ __forceinline__ bf16x8 tr_operand(const char* p0, const char* p1) {
+  const s16x4 lo = tr_read(p0), hi = tr_read(p1);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 struct __align__(16) RowTab {
@@ -400,15 +481,10 @@ __device__ __forceinline__ void row_store(RowTab& R, int slot, int lane, const R
   R.dlt[slot][lane] = dl;
 }
 
-// bf16 pair (element e of chunk a, element e of chunk b) as one 32-bit word.
-__device__ __forceinline__ uint32_t pair16(const u32x4& x, const u32x4& y, int e) {
-  const uint32_t wx = x[e >> 1], wy = y[e >> 1];
-  return (e & 1) ? ((wx >> 16) | (wy & 0xffff0000u)) : ((wx & 0xffffu) | (wy << 16));
-}
-
-__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
-  __shared__ u32x4 lds[kDkdvLds];
+__global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
+  __shared__ u32x4 lds[4 * kBufR];  // Q chunk x2, dO chunk x2
   __shared__ RowTab R;
+  constexpr int kW = kDkdvWaves;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
@@ -456,46 +532,52 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) 
     }
   }
 
-  // per-lane DMA rows and chunk offsets (instruction j = wave + 8x)
-  int drow[3];
-  uint32_t dcol[3];
+  // DMA: instruction j = wave + 4x writes buffer chunks 64j .. 64j+63; lane L
+  // fills row 4j + L/16, stored chunk L % 16, i.e. logical chunk
+  // (L % 16) ^ swz(row)
+  constexpr int kDx = kDmaR / kW;
+  static_assert(kDmaR % kW == 0, "whole DMA instructions per wave");
+  int drow[kDx];
+  uint32_t dcol[kDx];
 #pragma unroll
-  for (int x = 0; x < 3; x++) {
-    const int pk = 64 * (wave + 8 * x) + lane;
-    drow[x] = min(pk / kRowK, kChunk - 1);
-    dcol[x] = (uint32_t)(min(pk % kRowK, kRowK - 2) * 16);
+  for (int x = 0; x < kDx; x++) {
+    drow[x] = 4 * (wave + kW * x) + (lane >> 4);
+    dcol[x] = (uint32_t)((((lane & 15) ^ swz(drow[x]))) * 16);
   }
   const char* qb = static_cast<const char*>(a.q);
   const char* db = static_cast<const char*>(a.dout);
   auto dma_rows = [&](int slot, u32x4* qbuf, u32x4* dbuf) {
 #pragma unroll
-    for (int x = 0; x < 3; x++) {
-      if (wave + 8 * x < kDmaR) {
-        const int64_t t = R.t[slot][drow[x]], h = R.h[slot][drow[x]];
-        __builtin_amdgcn_global_load_lds(qb + (t * a.q_st + h * a.q_sh) * 2 + dcol[x],
-                                         qbuf + 64 * (wave + 8 * x), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(db + (t * a.do_st + h * a.do_sh) * 2 + dcol[x],
-                                         dbuf + 64 * (wave + 8 * x), 16, 0, 0);
-      }
+    for (int x = 0; x < kDx; x++) {
+      const int64_t t = R.t[slot][drow[x]], h = R.h[slot][drow[x]];
+      __builtin_amdgcn_global_load_lds(qb + (t * a.q_st + h * a.q_sh) * 2 + dcol[x],
+                                       qbuf + 64 * (wave + kW * x), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(db + (t * a.do_st + h * a.do_sh) * 2 + dcol[x],
+                                       dbuf + 64 * (wave + kW * x), 16, 0, 0);
     }
   };
-  u32x4* qt = lds + 4 * kBufR;
-  u32x4* dtr = qt + kBufT;
-  // Q^T / dO^T of a landed chunk: thread -> (row pair at packed positions
-  // 2pp, 2pp+1; 8-dim chunk c); one 32-bit LDS word per dim.
-  auto transpose = [&](const u32x4* qbuf, const u32x4* dbuf) {
-    const int pp = tid & 31, c = tid >> 5;
-    const int r = packed_row(2 * pp);
-    const u32x4 q0 = qbuf[r * kRowK + c], q1 = qbuf[(r + 1) * kRowK + c];
-    const u32x4 d0 = dbuf[r * kRowK + c], d1 = dbuf[(r + 1) * kRowK + c];
-    uint32_t* q32 = reinterpret_cast<uint32_t*>(qt);
-    uint32_t* d32 = reinterpret_cast<uint32_t*>(dtr);
+
+  // per-lane byte offsets into a chunk buffer
+  //  S / dP operands: row qc (+32 st), logical chunk 2kk + hh
+  uint32_t offa[8];
+  {
+    const int sq = swz(qc);
 #pragma unroll
-    for (int e = 0; e < 8; e++) {
-      q32[(8 * c + e) * (4 * kRowT) + pp] = pair16(q0, q1, e);
-      d32[(8 * c + e) * (4 * kRowT) + pp] = pair16(d0, d1, e);
-    }
-  };
+    for (int kk = 0; kk < 8; kk++) offa[kk] = (uint32_t)(qc * 256 + (((2 * kk + hh) ^ sq) * 16));
+  }
+  //  transposed operands: group lane i = qc % 16 addresses row
+  //  r0 + i/4 (r0 = 32 st + 16 s2 + 4 hh + 8 x) at dims 32 dt + 16 (qc/16) + 4 (i%4)
+  uint32_t offt[2][4];
+  {
+    const int i = qc & 15, trow = i >> 2;
+    const int cl = 2 * (qc >> 4) + ((i & 3) >> 1);
+#pragma unroll
+    for (int x = 0; x < 2; x++)
+#pragma unroll
+      for (int dt = 0; dt < 4; dt++)
+        offt[x][dt] = (uint32_t)((4 * hh + trow + 8 * x) * 256 +
+                                 (4 * (dt ^ trow) + (cl ^ (hh + 2 * x))) * 16 + 8 * (i & 1));
+  }
 
   f32x16 dka[4], dva[4];
 #pragma unroll
@@ -507,7 +589,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) 
     }
   const float c2 = a.scale_log2;
 
-  // prologue: row tables of chunks 0 and 1, chunk 0 landed and transposed
+  // prologue: row tables of chunks 0 and 1, chunk 0 landed
   if (wave == 0) {
     row_store(R, 0, lane, row_fetch(a, p, L, 0, lane));
     if (nch > 1) row_store(R, 1, lane, row_fetch(a, p, L, 1, lane));
@@ -516,22 +598,21 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) 
   dma_rows(0, lds, lds + 2 * kBufR);
   dma_wait();
   __syncthreads();
-  transpose(lds, lds + 2 * kBufR);
-  __syncthreads();
 
   for (int i = 0; i < nch; i++) {
     const int cur = i & 1;
     RowFetch nf;
     const bool fetch = wave == 0 && i + 2 < nch;
     if (fetch) nf = row_fetch(a, p, L, i + 2, lane);
-    if (i + 1 < nch) dma_rows((i + 1) % kSlots, lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
+    if (i + 1 < nch)
+      dma_rows((i + 1) % kSlots, lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
 
     if (wave_live) {
-      const u32x4* qr = lds + cur * kBufR;
-      const u32x4* dr = lds + 2 * kBufR + cur * kBufR;
+      const char* qr = reinterpret_cast<const char*>(lds + cur * kBufR);
+      const char* dr = reinterpret_cast<const char*>(lds + 2 * kBufR + cur * kBufR);
       const int slot = i % kSlots;
       const bool edge = (int64_t)(i + 1) * kChunk > L.nhist || !wave_full;
-#pragma unroll 1
+#pragma unroll
       for (int st = 0; st < 2; st++) {
         f32x16 sv, dpv;
 #pragma unroll
@@ -539,12 +620,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) 
           sv[r] = 0.0f;
           dpv[r] = 0.0f;
         }
-        const u32x4* qa = qr + (32 * st + qc) * kRowK + hh;
-        const u32x4* da = dr + (32 * st + qc) * kRowK + hh;
 #pragma unroll
-        for (int kk = 0; kk < 8; kk++) sv = mfma(as_bf16x8(qa[2 * kk]), kf[kk], sv);
-#pragma unroll
-        for (int kk = 0; kk < 8; kk++) dpv = mfma(as_bf16x8(da[2 * kk]), vf[kk], dpv);
+        for (int kk = 0; kk < 8; kk++) {
+          sv = mfma(as_bf16x8(*reinterpret_cast<const u32x4*>(qr + 8192 * st + offa[kk])), kf[kk], sv);
+          dpv = mfma(as_bf16x8(*reinterpret_cast<const u32x4*>(dr + 8192 * st + offa[kk])), vf[kk], dpv);
+        }
         // this lane's rows: 32*st + 8*r4 + 4*hh + (0..3)
         bf16x8 pb[2], sb[2];
 #pragma unroll
@@ -560,10 +640,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) 
             const float dv[4] = {dl.x, dl.y, dl.z, dl.w};
             float pr[4], ds[4];
 #pragma unroll
-            for (int c = 0; c < 4; c++) {
-              const int idx = 4 * r4 + c;
-              pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[idx], c2, -lv[c]));
-            }
+            for (int c = 0; c < 4; c++) pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[4 * r4 + c], c2, -lv[c]));
             if (edge) {
               const int4 km = *reinterpret_cast<const int4*>(&R.kmax[slot][row0]);
               const int kv[4] = {km.x, km.y, km.z, km.w};
@@ -581,23 +658,19 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) 
           sb[s2] = as_bf16x8(u32x4{ws[0], ws[1], ws[2], ws[3]});
         }
         // dV^T += dO^T . P and dK^T += Q^T . dS over this subtile's 32 rows
-        const u32x4* dta = dtr + qc * kRowT + 4 * st + hh;
-        const u32x4* qta = qt + qc * kRowT + 4 * st + hh;
 #pragma unroll
-        for (int dt = 0; dt < 4; dt++)
+        for (int s2 = 0; s2 < 2; s2++)
 #pragma unroll
-          for (int s2 = 0; s2 < 2; s2++)
-            dva[dt] = mfma(as_bf16x8(dta[32 * kRowT * dt + 2 * s2]), pb[s2], dva[dt]);
-#pragma unroll
-        for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-          for (int s2 = 0; s2 < 2; s2++)
-            dka[dt] = mfma(as_bf16x8(qta[32 * kRowT * dt + 2 * s2]), sb[s2], dka[dt]);
+          for (int dt = 0; dt < 4; dt++) {
+            const int rb = (32 * st + 16 * s2) * 256;
+            const bf16x8 ad = tr_operand(dr + rb + offt[0][dt], dr + rb + offt[1][dt]);
+            const bf16x8 aq = tr_operand(qr + rb + offt[0][dt], qr + rb + offt[1][dt]);
+            dva[dt] = mfma(ad, pb[s2], dva[dt]);
+            dka[dt] = mfma(aq, sb[s2], dka[dt]);
+          }
       }
     }
     dma_wait();
-    __syncthreads();
-    if (i + 1 < nch) transpose(lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
     if (fetch) row_store(R, (i + 2) % kSlots, lane, nf);
     __syncthreads();
   }
@@ -657,7 +730,7 @@ hipError_t launch_bwd_dkdv(const BwdArgs& a, const Problem& p, hipStream_t st) {
   const int64_t total = a.nktiles * p.Hkv;
   if (total <= 0) return hipSuccess;
   const int64_t grid = (total + 7) / 8 * 8;
-  bwd_dkdv_kernel<<<(unsigned)grid, 512, 0, st>>>(a, p);
+  bwd_dkdv_kernel<<<(unsigned)grid, 64 * kDkdvWaves, 0, st>>>(a, p);
   return hipGetLastError();
 }
 

@@ -6,7 +6,8 @@
 
 namespace moba {
 
-constexpr int kKeysPerDkdv = 256;  // keys per dK/dV work-group (8 waves x 32)
+constexpr int kDkdvWaves = 4;                 // waves per dK/dV work-group (one per SIMD)
+constexpr int kKeysPerDkdv = 32 * kDkdvWaves;  // keys per dK/dV work-group
 
 // Keys [k0, k1) of global block b; the block's tokens end at bend.  One dK/dV
 // work-group per key tile and kv-head.
