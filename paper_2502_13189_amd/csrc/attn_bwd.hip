@@ -410,12 +410,15 @@ __device__ __forceinline__ s16x4 tr_read(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
 }
 
-// A operand [dims x rows] of one k = 16 step from a swizzled chunk buffer:
-// rows r0 .. r0+3 and r0+8 .. r0+11 (the packed row order of the P and dS
-// operands), one dimension per lane.
-__device__ __forceinline__ bf16x8 tr_operand(const char* p0, const char* p1) {
-  const s16x4 lo = tr_read(p0), hi = tr_read(p1);
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+// As pin_pipeline() for MFMAs whose operand takes two LDS reads.
+__device__ __forceinline__ void pin_pipeline_tr() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPre, 0);
+#pragma unroll
+  for (int j = 0; j < 16 - kPre; j++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
 }
 
 struct __align__(16) RowTab {
@@ -479,6 +482,94 @@ __device__ __forceinline__ void row_store(RowTab& R, int slot, int lane, const R
   R.kmax[slot][lane] = km;
   R.lse2[slot][lane] = l2;
   R.dlt[slot][lane] = dl;
+}
+
+// One 64-row chunk of the dK/dV kernel for this wave's 32 keys: per 32-row
+// subtile, S = Q K^T and dP = dO V^T, then P, dS, and dV^T += dO^T P,
+// dK^T += Q^T dS.  EDGE chunks hold rows that may not attend every key
+// (causal rows of the block itself, padding) or keys past the tile end.
+template <bool EDGE>
+__device__ __forceinline__ void dkdv_chunk(const char* qr, const char* dr, const RowTab& R, int slot,
+                                           const uint32_t (&offa)[8], const uint32_t (&offt)[2][4],
+                                           const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
+                                           f32x16 (&dka)[4], f32x16 (&dva)[4], int key, int k1,
+                                           float c2, int hh) {
+#pragma unroll 1
+  for (int st = 0; st < 2; st++) {
+    f32x16 sv, dpv;
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      sv[r] = 0.0f;
+      dpv[r] = 0.0f;
+    }
+    {
+      // 16 operand reads, kPre MFMAs ahead of their use
+      u32x4 op[16];
+#pragma unroll
+      for (int j = 0; j < 16; j++)
+        op[j] = *reinterpret_cast<const u32x4*>(((j & 1) ? dr : qr) + 8192 * st + offa[j >> 1]);
+#pragma unroll
+      for (int j = 0; j < 16; j++) {
+        if (j & 1) dpv = mfma(as_bf16x8(op[j]), vf[j >> 1], dpv);
+        else sv = mfma(as_bf16x8(op[j]), kf[j >> 1], sv);
+      }
+      pin_pipeline();
+    }
+    // this lane's rows: 32*st + 8*r4 + 4*hh + (0..3)
+    bf16x8 pb[2], sb[2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; s2++) {
+      uint32_t wp[4], ws[4];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; h2++) {
+        const int r4 = 2 * s2 + h2;
+        const int row0 = 32 * st + 8 * r4 + 4 * hh;
+        const float4 l2 = *reinterpret_cast<const float4*>(&R.lse2[slot][row0]);
+        const float4 dl = *reinterpret_cast<const float4*>(&R.dlt[slot][row0]);
+        const float lv[4] = {l2.x, l2.y, l2.z, l2.w};
+        const float dv[4] = {dl.x, dl.y, dl.z, dl.w};
+        float pr[4], ds[4];
+#pragma unroll
+        for (int c = 0; c < 4; c++) pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[4 * r4 + c], c2, -lv[c]));
+        if (EDGE) {
+          const int4 km = *reinterpret_cast<const int4*>(&R.kmax[slot][row0]);
+          const int kv[4] = {km.x, km.y, km.z, km.w};
+#pragma unroll
+          for (int c = 0; c < 4; c++) pr[c] = (key <= kv[c] && key < k1) ? pr[c] : 0.0f;
+        }
+#pragma unroll
+        for (int c = 0; c < 4; c++) ds[c] = pr[c] * (dpv[4 * r4 + c] - dv[c]);
+        wp[2 * h2] = pack_bf16(pr[0], pr[1]);
+        wp[2 * h2 + 1] = pack_bf16(pr[2], pr[3]);
+        ws[2 * h2] = pack_bf16(ds[0], ds[1]);
+        ws[2 * h2 + 1] = pack_bf16(ds[2], ds[3]);
+      }
+      pb[s2] = as_bf16x8(u32x4{wp[0], wp[1], wp[2], wp[3]});
+      sb[s2] = as_bf16x8(u32x4{ws[0], ws[1], ws[2], ws[3]});
+    }
+    // dV^T += dO^T . P and dK^T += Q^T . dS over this subtile's 32 rows
+    {
+      // 16 operands of two transposed reads each, kPre MFMAs ahead;
+      // j = 2 * (4 * s2 + dt) + (0: dV from dO^T, 1: dK from Q^T)
+      s16x4 tl[16], th[16];
+#pragma unroll
+      for (int j = 0; j < 16; j++) {
+        const int s2 = j >> 3, dt = (j >> 1) & 3;
+        const char* b = ((j & 1) ? qr : dr) + (32 * st + 16 * s2) * 256;
+        tl[j] = tr_read(b + offt[0][dt]);
+        th[j] = tr_read(b + offt[1][dt]);
+      }
+#pragma unroll
+      for (int j = 0; j < 16; j++) {
+        const int s2 = j >> 3, dt = (j >> 1) & 3;
+        const bf16x8 opj =
+            __builtin_bit_cast(bf16x8, __builtin_shufflevector(tl[j], th[j], 0, 1, 2, 3, 4, 5, 6, 7));
+        if (j & 1) dka[dt] = mfma(opj, sb[s2], dka[dt]);
+        else dva[dt] = mfma(opj, pb[s2], dva[dt]);
+      }
+      pin_pipeline_tr();
+    }
+  }
 }
 
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
@@ -611,64 +702,10 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
       const char* qr = reinterpret_cast<const char*>(lds + cur * kBufR);
       const char* dr = reinterpret_cast<const char*>(lds + 2 * kBufR + cur * kBufR);
       const int slot = i % kSlots;
-      const bool edge = (int64_t)(i + 1) * kChunk > L.nhist || !wave_full;
-#pragma unroll
-      for (int st = 0; st < 2; st++) {
-        f32x16 sv, dpv;
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-          sv[r] = 0.0f;
-          dpv[r] = 0.0f;
-        }
-#pragma unroll
-        for (int kk = 0; kk < 8; kk++) {
-          sv = mfma(as_bf16x8(*reinterpret_cast<const u32x4*>(qr + 8192 * st + offa[kk])), kf[kk], sv);
-          dpv = mfma(as_bf16x8(*reinterpret_cast<const u32x4*>(dr + 8192 * st + offa[kk])), vf[kk], dpv);
-        }
-        // this lane's rows: 32*st + 8*r4 + 4*hh + (0..3)
-        bf16x8 pb[2], sb[2];
-#pragma unroll
-        for (int s2 = 0; s2 < 2; s2++) {
-          uint32_t wp[4], ws[4];
-#pragma unroll
-          for (int h2 = 0; h2 < 2; h2++) {
-            const int r4 = 2 * s2 + h2;
-            const int row0 = 32 * st + 8 * r4 + 4 * hh;
-            const float4 l2 = *reinterpret_cast<const float4*>(&R.lse2[slot][row0]);
-            const float4 dl = *reinterpret_cast<const float4*>(&R.dlt[slot][row0]);
-            const float lv[4] = {l2.x, l2.y, l2.z, l2.w};
-            const float dv[4] = {dl.x, dl.y, dl.z, dl.w};
-            float pr[4], ds[4];
-#pragma unroll
-            for (int c = 0; c < 4; c++) pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[4 * r4 + c], c2, -lv[c]));
-            if (edge) {
-              const int4 km = *reinterpret_cast<const int4*>(&R.kmax[slot][row0]);
-              const int kv[4] = {km.x, km.y, km.z, km.w};
-#pragma unroll
-              for (int c = 0; c < 4; c++) pr[c] = (key <= kv[c] && key < kt.k1) ? pr[c] : 0.0f;
-            }
-#pragma unroll
-            for (int c = 0; c < 4; c++) ds[c] = pr[c] * (dpv[4 * r4 + c] - dv[c]);
-            wp[2 * h2] = pack_bf16(pr[0], pr[1]);
-            wp[2 * h2 + 1] = pack_bf16(pr[2], pr[3]);
-            ws[2 * h2] = pack_bf16(ds[0], ds[1]);
-            ws[2 * h2 + 1] = pack_bf16(ds[2], ds[3]);
-          }
-          pb[s2] = as_bf16x8(u32x4{wp[0], wp[1], wp[2], wp[3]});
-          sb[s2] = as_bf16x8(u32x4{ws[0], ws[1], ws[2], ws[3]});
-        }
-        // dV^T += dO^T . P and dK^T += Q^T . dS over this subtile's 32 rows
-#pragma unroll
-        for (int s2 = 0; s2 < 2; s2++)
-#pragma unroll
-          for (int dt = 0; dt < 4; dt++) {
-            const int rb = (32 * st + 16 * s2) * 256;
-            const bf16x8 ad = tr_operand(dr + rb + offt[0][dt], dr + rb + offt[1][dt]);
-            const bf16x8 aq = tr_operand(qr + rb + offt[0][dt], qr + rb + offt[1][dt]);
-            dva[dt] = mfma(ad, pb[s2], dva[dt]);
-            dka[dt] = mfma(aq, sb[s2], dka[dt]);
-          }
-      }
+      if ((int64_t)(i + 1) * kChunk > L.nhist || !wave_full)
+        dkdv_chunk<true>(qr, dr, R, slot, offa, offt, kf, vf, dka, dva, key, kt.k1, c2, hh);
+      else
+        dkdv_chunk<false>(qr, dr, R, slot, offa, offt, kf, vf, dka, dva, key, kt.k1, c2, hh);
     }
     dma_wait();
     if (fetch) row_store(R, (i + 2) % kSlots, lane, nf);
