@@ -42,7 +42,7 @@ HBM_PEAK_GBS = 8000.0
 # is reported only while the sources are unchanged.
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_hist_L1M_gqa32x8_B4096_k12_traffic.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2502_13189_amd", "csrc", f)
-                  for f in ("attn_mfma.hip", "moba_internal.h")]
+                  for f in ("attn_mfma.hip", "mfma_tile.h", "moba_internal.h")]
 
 
 def kernel_source_hash():
