@@ -19,17 +19,17 @@
 //          tile and wave: S^T = K . Q^T and dP^T = V . dO^T (K and V
 //          row-major from LDS, Q^T and dO^T operands in registers), then
 //          dQ^T += K^T . dS^T from the packed K^T tile: 48 MFMAs.
-//   dkdv   key side: a work-group (4 waves, one per SIMD, so each wave may
-//          hold 512 registers) owns 128 keys of one block and kv-head
-//          (wave w: 32 keys, with K, V, dK^T and dV^T in registers) and
-//          loops over every row that attends them, 64 rows at a time: the
-//          bin's routed history rows, then the block's own rows (causal).
-//          The rows' Q and dO arrive by LDS DMA, gathered row by row, into a
-//          swizzled row-major layout that also serves the transposed
-//          operands (ds_read_b64_tr_b16).  Per 32-row subtile and
-//          wave: S = Q . K^T, dP = dO . V^T, then dV^T += dO^T . P and
-//          dK^T += Q^T . dS: 32 MFMAs.  Each key has one owner, so dK and dV
-//          need neither atomics nor a merge.
+//   dkdv   key side: a work-group of 8 waves owns 128 keys of one block and
+//          kv-head, 32 per SIMD, and loops over every row that attends them,
+//          64 rows at a time: the bin's routed history rows, then the
+//          block's own rows (causal).  The rows' Q and dO arrive by LDS DMA,
+//          gathered row by row, into a swizzled row-major layout that also
+//          serves the transposed operands (ds_read_b64_tr_b16).  The two
+//          waves of a SIMD split the work for their 32 keys: per 32-row
+//          subtile the P-wave forms S = Q . K^T, P and dV^T += dO^T . P, the
+//          D-wave dP = dO . V^T, dS (with P from LDS) and dK^T += Q^T . dS:
+//          16 MFMAs each.  Each key has one owner, so dK and dV need
+//          neither atomics nor a merge.
 // P and dS enter the second products as bf16; every product accumulates in
 // fp32.
 #include "bwd_internal.h"
@@ -410,17 +410,6 @@ __device__ __forceinline__ s16x4 tr_read(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
 }
 
-// As pin_pipeline() for MFMAs whose operand takes two LDS reads.
-__device__ __forceinline__ void pin_pipeline_tr() {
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPre, 0);
-#pragma unroll
-  for (int j = 0; j < 16 - kPre; j++) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x008, kPre, 0);
-}
-
 struct __align__(16) RowTab {
   int t[kSlots][kChunk];
   int h[kSlots][kChunk];
@@ -484,101 +473,125 @@ __device__ __forceinline__ void row_store(RowTab& R, int slot, int lane, const R
   R.dlt[slot][lane] = dl;
 }
 
-// One 64-row chunk of the dK/dV kernel for this wave's 32 keys: per 32-row
-// subtile, S = Q K^T and dP = dO V^T, then P, dS, and dV^T += dO^T P,
-// dK^T += Q^T dS.  EDGE chunks hold rows that may not attend every key
-// (causal rows of the block itself, padding) or keys past the tile end.
-template <bool EDGE>
-__device__ __forceinline__ void dkdv_chunk(const char* qr, const char* dr, const RowTab& R, int slot,
-                                           const uint32_t (&offa)[8], const uint32_t (&offt)[2][4],
-                                           const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
-                                           f32x16 (&dka)[4], f32x16 (&dva)[4], int key, int k1,
-                                           float c2, int hh) {
-#pragma unroll 1
-  for (int st = 0; st < 2; st++) {
-    f32x16 sv, dpv;
+// P of one 32-row subtile as written by a P-wave for its D-wave:
+// [parity][pair][r4][lane] float4 (lane order, so every access is one
+// contiguous 1 KiB per wave).
+struct __align__(16) PExchange {
+  float4 p[2][kDkdvWaves / 2][4][64];
+};
+
+// S = Q K^T (P-wave) or dP = dO V^T (D-wave) of subtile st: 8 k-steps with
+// the A operands from the swizzled chunk buffer and B = this wave's K or V.
+__device__ __forceinline__ f32x16 sd_product(const char* buf, int st, const uint32_t (&offa)[8],
+                                             const bf16x8 (&kv)[8]) {
+  u32x4 op[8];
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-      sv[r] = 0.0f;
-      dpv[r] = 0.0f;
-    }
-    {
-      // 16 operand reads, kPre MFMAs ahead of their use
-      u32x4 op[16];
+  for (int j = 0; j < 8; j++) op[j] = *reinterpret_cast<const u32x4*>(buf + 8192 * st + offa[j]);
+  f32x16 acc;
 #pragma unroll
-      for (int j = 0; j < 16; j++)
-        op[j] = *reinterpret_cast<const u32x4*>(((j & 1) ? dr : qr) + 8192 * st + offa[j >> 1]);
+  for (int r = 0; r < 16; r++) acc[r] = 0.0f;
 #pragma unroll
-      for (int j = 0; j < 16; j++) {
-        if (j & 1) dpv = mfma(as_bf16x8(op[j]), vf[j >> 1], dpv);
-        else sv = mfma(as_bf16x8(op[j]), kf[j >> 1], sv);
-      }
-      pin_pipeline();
-    }
-    // this lane's rows: 32*st + 8*r4 + 4*hh + (0..3)
-    bf16x8 pb[2], sb[2];
+  for (int j = 0; j < 8; j++) acc = mfma(as_bf16x8(op[j]), kv[j], acc);
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-    for (int s2 = 0; s2 < 2; s2++) {
-      uint32_t wp[4], ws[4];
-#pragma unroll
-      for (int h2 = 0; h2 < 2; h2++) {
-        const int r4 = 2 * s2 + h2;
-        const int row0 = 32 * st + 8 * r4 + 4 * hh;
-        const float4 l2 = *reinterpret_cast<const float4*>(&R.lse2[slot][row0]);
-        const float4 dl = *reinterpret_cast<const float4*>(&R.dlt[slot][row0]);
-        const float lv[4] = {l2.x, l2.y, l2.z, l2.w};
-        const float dv[4] = {dl.x, dl.y, dl.z, dl.w};
-        float pr[4], ds[4];
-#pragma unroll
-        for (int c = 0; c < 4; c++) pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[4 * r4 + c], c2, -lv[c]));
-        if (EDGE) {
-          const int4 km = *reinterpret_cast<const int4*>(&R.kmax[slot][row0]);
-          const int kv[4] = {km.x, km.y, km.z, km.w};
-#pragma unroll
-          for (int c = 0; c < 4; c++) pr[c] = (key <= kv[c] && key < k1) ? pr[c] : 0.0f;
-        }
-#pragma unroll
-        for (int c = 0; c < 4; c++) ds[c] = pr[c] * (dpv[4 * r4 + c] - dv[c]);
-        wp[2 * h2] = pack_bf16(pr[0], pr[1]);
-        wp[2 * h2 + 1] = pack_bf16(pr[2], pr[3]);
-        ws[2 * h2] = pack_bf16(ds[0], ds[1]);
-        ws[2 * h2 + 1] = pack_bf16(ds[2], ds[3]);
-      }
-      pb[s2] = as_bf16x8(u32x4{wp[0], wp[1], wp[2], wp[3]});
-      sb[s2] = as_bf16x8(u32x4{ws[0], ws[1], ws[2], ws[3]});
-    }
-    // dV^T += dO^T . P and dK^T += Q^T . dS over this subtile's 32 rows
-    {
-      // 16 operands of two transposed reads each, kPre MFMAs ahead;
-      // j = 2 * (4 * s2 + dt) + (0: dV from dO^T, 1: dK from Q^T)
-      s16x4 tl[16], th[16];
-#pragma unroll
-      for (int j = 0; j < 16; j++) {
-        const int s2 = j >> 3, dt = (j >> 1) & 3;
-        const char* b = ((j & 1) ? qr : dr) + (32 * st + 16 * s2) * 256;
-        tl[j] = tr_read(b + offt[0][dt]);
-        th[j] = tr_read(b + offt[1][dt]);
-      }
-#pragma unroll
-      for (int j = 0; j < 16; j++) {
-        const int s2 = j >> 3, dt = (j >> 1) & 3;
-        const bf16x8 opj =
-            __builtin_bit_cast(bf16x8, __builtin_shufflevector(tl[j], th[j], 0, 1, 2, 3, 4, 5, 6, 7));
-        if (j & 1) dka[dt] = mfma(opj, sb[s2], dka[dt]);
-        else dva[dt] = mfma(opj, pb[s2], dva[dt]);
-      }
-      pin_pipeline_tr();
-    }
+  for (int j = 0; j < 4; j++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  return acc;
 }
 
+// acc^T (dims x keys) += X^T (dims x rows) . W (rows x keys) over subtile st,
+// X the swizzled chunk buffer read transposed, W the bf16 operands w[s2].
+__device__ __forceinline__ void g_product(f32x16 (&acc)[4], const char* buf, int st,
+                                          const uint32_t (&offt)[2][4], const bf16x8 (&w)[2]) {
+  s16x4 tl[8], th[8];
+#pragma unroll
+  for (int j = 0; j < 8; j++) {
+    const int s2 = j >> 2, dt = j & 3;
+    const char* b = buf + (32 * st + 16 * s2) * 256;
+    tl[j] = tr_read(b + offt[0][dt]);
+    th[j] = tr_read(b + offt[1][dt]);
+  }
+#pragma unroll
+  for (int j = 0; j < 8; j++) {
+    const int s2 = j >> 2, dt = j & 3;
+    acc[dt] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(tl[j], th[j], 0, 1, 2, 3, 4, 5,
+                                                                       6, 7)),
+                   w[s2], acc[dt]);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+}
+
+// P-wave: P = exp2(S c2 - lse2) of subtile st (zero where a row may not
+// attend the lane's key, EDGE chunks), into the exchange and as bf16
+// operands pb[s2].  A lane's values are rows 32*st + 8*r4 + 4*hh + (0..3).
+template <bool EDGE>
+__device__ __forceinline__ void p_weights(const f32x16& sv, const RowTab& R, int slot, int st,
+                                          int hh, int lane, int key, int k1, float c2,
+                                          float4 (&xo)[4][64], bf16x8 (&pb)[2]) {
+  uint32_t w[8];
+#pragma unroll
+  for (int r4 = 0; r4 < 4; r4++) {
+    const int row0 = 32 * st + 8 * r4 + 4 * hh;
+    const float4 l2 = *reinterpret_cast<const float4*>(&R.lse2[slot][row0]);
+    const float lv[4] = {l2.x, l2.y, l2.z, l2.w};
+    float pr[4];
+#pragma unroll
+    for (int c = 0; c < 4; c++) pr[c] = __builtin_amdgcn_exp2f(fmaf(sv[4 * r4 + c], c2, -lv[c]));
+    if (EDGE) {
+      const int4 km = *reinterpret_cast<const int4*>(&R.kmax[slot][row0]);
+      const int kv[4] = {km.x, km.y, km.z, km.w};
+#pragma unroll
+      for (int c = 0; c < 4; c++) pr[c] = (key <= kv[c] && key < k1) ? pr[c] : 0.0f;
+    }
+    xo[r4][lane] = make_float4(pr[0], pr[1], pr[2], pr[3]);
+    w[2 * r4] = pack_bf16(pr[0], pr[1]);
+    w[2 * r4 + 1] = pack_bf16(pr[2], pr[3]);
+  }
+  pb[0] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+  pb[1] = as_bf16x8(u32x4{w[4], w[5], w[6], w[7]});
+}
+
+// D-wave: dS = P (dP - Delta) of subtile st as bf16 operands sb[s2].
+__device__ __forceinline__ void ds_weights(const f32x16& dpv, const RowTab& R, int slot, int st,
+                                           int hh, int lane, const float4 (&xi)[4][64],
+                                           bf16x8 (&sb)[2]) {
+  uint32_t w[8];
+#pragma unroll
+  for (int r4 = 0; r4 < 4; r4++) {
+    const int row0 = 32 * st + 8 * r4 + 4 * hh;
+    const float4 dl = *reinterpret_cast<const float4*>(&R.dlt[slot][row0]);
+    const float4 pp = xi[r4][lane];
+    w[2 * r4] = pack_bf16(pp.x * (dpv[4 * r4] - dl.x), pp.y * (dpv[4 * r4 + 1] - dl.y));
+    w[2 * r4 + 1] = pack_bf16(pp.z * (dpv[4 * r4 + 2] - dl.z), pp.w * (dpv[4 * r4 + 3] - dl.w));
+  }
+  sb[0] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+  sb[1] = as_bf16x8(u32x4{w[4], w[5], w[6], w[7]});
+}
+
+// Work-group: 4 pairs of waves, pair q on SIMD q (waves q and q + 4), each
+// pair owning 32 keys.  The P-wave holds K, computes S and P and accumulates
+// dV^T; the D-wave holds V, computes dP and dS (with the P-wave's P, passed
+// through LDS behind one barrier per 32-row subtile) and accumulates dK^T.
+// Each wave so holds one 32-key operand set and one 32x128 accumulator, and
+// the two waves of a SIMD run matrix and vector work beside each other.
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
   __shared__ u32x4 lds[4 * kBufR];  // Q chunk x2, dO chunk x2
   __shared__ RowTab R;
+  __shared__ PExchange X;
   constexpr int kW = kDkdvWaves;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
+  const int pair = wave & 3, role = wave >> 2;  // role 0: P-wave, 1: D-wave
 
   // work-group -> (kv-head, key tile): each XCD takes a contiguous run (the
   // key tiles of one bin read the same rows), early blocks (longest row
@@ -604,28 +617,25 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   L.nrows = L.nhist + (int64_t)L.nct * p.G;
   const int nch = (int)((L.nrows + kChunk - 1) / kChunk);
 
-  // this wave's 32 keys: K and V as the B operands of S = Q K^T, dP = dO V^T
-  const int kw0 = kt.k0 + 32 * wave;
-  const bool wave_live = kw0 < kt.k1;
-  const bool wave_full = kw0 + 32 <= kt.k1;
+  // the pair's 32 keys; this wave's K (P-wave) or V (D-wave) as B operands
+  const int kw0 = kt.k0 + 32 * pair;
+  const bool live = kw0 < kt.k1;
+  const bool full = kw0 + 32 <= kt.k1;
   const int key = kw0 + qc;
   const int kld = min(key, kt.k1 - 1);
-  bf16x8 kf[8], vf[8];
+  bf16x8 kv[8];
   {
-    const __hip_bfloat16* kr = static_cast<const __hip_bfloat16*>(a.k) + (int64_t)kld * a.k_st +
-                               (int64_t)L.g * a.k_sh + 8 * hh;
-    const __hip_bfloat16* vr = static_cast<const __hip_bfloat16*>(a.v) + (int64_t)kld * a.v_st +
-                               (int64_t)L.g * a.v_sh + 8 * hh;
+    const __hip_bfloat16* src =
+        role == 0 ? static_cast<const __hip_bfloat16*>(a.k) + (int64_t)kld * a.k_st + (int64_t)L.g * a.k_sh
+                  : static_cast<const __hip_bfloat16*>(a.v) + (int64_t)kld * a.v_st + (int64_t)L.g * a.v_sh;
 #pragma unroll
-    for (int kk = 0; kk < 8; kk++) {
-      kf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(kr + 16 * kk));
-      vf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(vr + 16 * kk));
-    }
+    for (int kk = 0; kk < 8; kk++)
+      kv[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 8 * hh + 16 * kk));
   }
 
-  // DMA: instruction j = wave + 4x writes buffer chunks 64j .. 64j+63; lane L
-  // fills row 4j + L/16, stored chunk L % 16, i.e. logical chunk
-  // (L % 16) ^ swz(row)
+  // DMA: instruction j (0..15, per tensor) writes buffer chunks 64j ..
+  // 64j+63; wave w issues j = w + 8x; lane L fills row 4j + L/16, stored
+  // chunk L % 16, i.e. logical chunk (L % 16) ^ swz(row)
   constexpr int kDx = kDmaR / kW;
   static_assert(kDmaR % kW == 0, "whole DMA instructions per wave");
   int drow[kDx];
@@ -670,14 +680,11 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
                                  (4 * (dt ^ trow) + (cl ^ (hh + 2 * x))) * 16 + 8 * (i & 1));
   }
 
-  f32x16 dka[4], dva[4];
+  f32x16 acc[4];  // P-wave: dV^T, D-wave: dK^T (dims x keys)
 #pragma unroll
   for (int dt = 0; dt < 4; dt++)
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-      dka[dt][r] = 0.0f;
-      dva[dt][r] = 0.0f;
-    }
+    for (int r = 0; r < 16; r++) acc[dt][r] = 0.0f;
   const float c2 = a.scale_log2;
 
   // prologue: row tables of chunks 0 and 1, chunk 0 landed
@@ -697,15 +704,27 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
     if (fetch) nf = row_fetch(a, p, L, i + 2, lane);
     if (i + 1 < nch)
       dma_rows((i + 1) % kSlots, lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
-
-    if (wave_live) {
-      const char* qr = reinterpret_cast<const char*>(lds + cur * kBufR);
-      const char* dr = reinterpret_cast<const char*>(lds + 2 * kBufR + cur * kBufR);
-      const int slot = i % kSlots;
-      if ((int64_t)(i + 1) * kChunk > L.nhist || !wave_full)
-        dkdv_chunk<true>(qr, dr, R, slot, offa, offt, kf, vf, dka, dva, key, kt.k1, c2, hh);
-      else
-        dkdv_chunk<false>(qr, dr, R, slot, offa, offt, kf, vf, dka, dva, key, kt.k1, c2, hh);
+    const char* qr = reinterpret_cast<const char*>(lds + cur * kBufR);
+    const char* dr = reinterpret_cast<const char*>(lds + 2 * kBufR + cur * kBufR);
+    const int slot = i % kSlots;
+    const bool edge = (int64_t)(i + 1) * kChunk > L.nhist || !full;
+#pragma unroll 1
+    for (int st = 0; st < 2; st++) {
+      f32x16 sd;  // P-wave: S, D-wave: dP
+      bf16x8 wb[2];
+      if (live) {
+        sd = sd_product(role == 0 ? qr : dr, st, offa, kv);
+        if (role == 0) {
+          if (edge) p_weights<true>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
+          else p_weights<false>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
+        }
+      }
+      __syncthreads();
+      if (live) {
+        if (role == 1) ds_weights(sd, R, slot, st, hh, lane, X.p[st][pair], wb);
+        // P-wave: dV^T += dO^T P; D-wave: dK^T += Q^T dS
+        g_product(acc, role == 0 ? dr : qr, st, offt, wb);
+      }
     }
     dma_wait();
     if (fetch) row_store(R, (i + 2) % kSlots, lane, nf);
@@ -713,24 +732,20 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   }
 
   // -------------------------------------------------------------- epilogue
-  if (!wave_live || key >= kt.k1) return;
-  const float scl = a.scale;
-  __hip_bfloat16* dkr =
-      static_cast<__hip_bfloat16*>(a.dk) + (int64_t)key * a.dk_st + (int64_t)L.g * a.dk_sh;
-  __hip_bfloat16* dvr =
-      static_cast<__hip_bfloat16*>(a.dv) + (int64_t)key * a.dv_st + (int64_t)L.g * a.dv_sh;
+  if (!live || key >= kt.k1) return;
+  const float scl = role == 0 ? 1.0f : a.scale;
+  __hip_bfloat16* dst = role == 0 ? static_cast<__hip_bfloat16*>(a.dv) + (int64_t)key * a.dv_st +
+                                        (int64_t)L.g * a.dv_sh
+                                  : static_cast<__hip_bfloat16*>(a.dk) + (int64_t)key * a.dk_st +
+                                        (int64_t)L.g * a.dk_sh;
 #pragma unroll
   for (int dt = 0; dt < 4; dt++)
 #pragma unroll
     for (int r4 = 0; r4 < 4; r4++) {
-      const int d = 32 * dt + 8 * r4 + 4 * hh;
       uint2 w;
-      w.x = pack_bf16(dka[dt][4 * r4] * scl, dka[dt][4 * r4 + 1] * scl);
-      w.y = pack_bf16(dka[dt][4 * r4 + 2] * scl, dka[dt][4 * r4 + 3] * scl);
-      *reinterpret_cast<uint2*>(dkr + d) = w;
-      w.x = pack_bf16(dva[dt][4 * r4], dva[dt][4 * r4 + 1]);
-      w.y = pack_bf16(dva[dt][4 * r4 + 2], dva[dt][4 * r4 + 3]);
-      *reinterpret_cast<uint2*>(dvr + d) = w;
+      w.x = pack_bf16(acc[dt][4 * r4] * scl, acc[dt][4 * r4 + 1] * scl);
+      w.y = pack_bf16(acc[dt][4 * r4 + 2] * scl, acc[dt][4 * r4 + 3] * scl);
+      *reinterpret_cast<uint2*>(dst + 32 * dt + 8 * r4 + 4 * hh) = w;
     }
 }
 

@@ -6,8 +6,8 @@
 
 namespace moba {
 
-constexpr int kDkdvWaves = 4;                 // waves per dK/dV work-group (one per SIMD)
-constexpr int kKeysPerDkdv = 32 * kDkdvWaves;  // keys per dK/dV work-group
+constexpr int kDkdvWaves = 8;                       // waves per dK/dV work-group (two per SIMD)
+constexpr int kKeysPerDkdv = 32 * (kDkdvWaves / 2);  // keys per dK/dV work-group (32 per SIMD)
 
 // Keys [k0, k1) of global block b; the block's tokens end at bend.  One dK/dV
 // work-group per key tile and kv-head.
