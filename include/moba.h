@@ -137,6 +137,20 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
                                hipStream_t stream);
 
 /*
+ * Backward of moba_dense_forward: gradients of causal full attention (Eq. 1)
+ * w.r.t. q, k and v, with out and lse from moba_dense_forward.  Same
+ * conventions, dtype (bf16 only) and precision as moba_backward.  With
+ * moba_dense_forward it lets a caller switch any attention call between
+ * full attention and MoBA, in both directions (the per-layer choice of
+ * Sec. 2.2 "Hybrid of MoBA and Full Attention" and the layer-wise hybrid of
+ * Sec. 3.2, whose last layers stay full attention).
+ */
+moba_status moba_dense_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                                const moba_tensor* cu_seqlens, const moba_tensor* out,
+                                const moba_tensor* lse, const moba_tensor* dout, moba_tensor* dq,
+                                moba_tensor* dk, moba_tensor* dv, hipStream_t stream);
+
+/*
  * Block mean-pool of the keys (Eq. 6; Algorithm 1, mean_pool).
  * kbar [nblk_total, Hkv, D] f32 contiguous, device: row b = blk_off[s] + j
  * holds the mean of k over the tokens of block j of sequence s (a short last

@@ -60,6 +60,7 @@ def load() -> ctypes.CDLL:
     sig = {
         "moba_forward": [P, P, P, P, i32, i32, P, P, vp],
         "moba_backward": [P, P, P, P, i32, i32, P, P, P, P, P, P, vp],
+        "moba_dense_backward": [P, P, P, P, P, P, P, P, P, P, vp],
         "moba_dense_forward": [P, P, P, P, P, P, vp],
         "moba_pool": [P, P, i32, P, vp],
         "moba_select": [P, P, P, i32, i32, P, P, vp],
@@ -159,6 +160,23 @@ def backward(q, k, v, cu_seqlens, block_size: int, topk: int, out, lse, dout, dq
                                               int(block_size), int(topk), _ref(d[4]), _ref(d[5]),
                                               _ref(d[6]), _ref(d[7]), _ref(d[8]), _ref(d[9]),
                                               _stream(q, stream)))
+    return dq, dk, dv
+
+
+def dense_backward(q, k, v, cu_seqlens, out, lse, dout, dq=None, dk=None, dv=None, stream=None):
+    """Gradients of dense_forward() (causal full attention) w.r.t. q, k, v (bf16)."""
+    lib = load()
+    cu = _cu(cu_seqlens)
+    if dq is None:
+        dq = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if dk is None:
+        dk = torch.empty_like(k, memory_format=torch.contiguous_format)
+    if dv is None:
+        dv = torch.empty_like(v, memory_format=torch.contiguous_format)
+    d = [describe(t) for t in (q, k, v, cu, out, lse, dout, dq, dk, dv)]
+    _check("moba_dense_backward", lib.moba_dense_backward(
+        _ref(d[0]), _ref(d[1]), _ref(d[2]), _ref(d[3]), _ref(d[4]), _ref(d[5]), _ref(d[6]),
+        _ref(d[7]), _ref(d[8]), _ref(d[9]), _stream(q, stream)))
     return dq, dk, dv
 
 

@@ -592,10 +592,17 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   return MOBA_OK;
 }
 
-moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+}  // extern "C"
+
+namespace {
+
+// The backward of moba_forward; with `dense`, of moba_dense_forward (each
+// sequence one block, top-1: the causal current block is the whole prefix).
+moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
                           const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
                           const moba_tensor* out, const moba_tensor* lse, const moba_tensor* dout,
-                          moba_tensor* dq, moba_tensor* dk, moba_tensor* dv, hipStream_t stream) {
+                          moba_tensor* dq, moba_tensor* dk, moba_tensor* dv, hipStream_t stream,
+                          bool dense) {
   Inputs in;
   View vo, vdo, vdq, vdk, vdv;
   moba_status st = check_inputs(q, k, v, cu_seqlens, out, lse, &in, &vo);
@@ -610,16 +617,23 @@ moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba
       dv->shape[0] != in.T)
     return MOBA_ERR_SHAPE;
   if (vdo.H != in.Hq || vdq.H != in.Hq || vdk.H != in.Hkv || vdv.H != in.Hkv) return MOBA_ERR_SHAPE;
-  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
-  if (topk < 1) return MOBA_ERR_TOPK;
+  if (!dense && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (!dense && topk < 1) return MOBA_ERR_TOPK;
   if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
   if (in.T == 0) return MOBA_OK;
+  if (dense) {
+    int64_t lmax = 1;
+    for (size_t s = 0; s + 1 < in.cu.size(); s++)
+      lmax = std::max<int64_t>(lmax, (int64_t)in.cu[s + 1] - in.cu[s]);
+    block_size = (int32_t)lmax;
+    topk = 1;
+  }
 
   int64_t nbmax = 0;
   for (size_t s = 0; s + 1 < in.cu.size(); s++)
     nbmax = std::max<int64_t>(nbmax, ceil_div((int64_t)in.cu[s + 1] - in.cu[s], block_size));
   if (nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
-  const int kk = (int)std::min<int64_t>(topk, nbmax);
+  const int kk = (int)std::max<int64_t>(1, std::min<int64_t>(topk, nbmax));
   if (kk - 1 > 63 && kk - 1 < nbmax - 1) return MOBA_ERR_UNSUPPORTED;
   if ((uint64_t)in.T * in.Hq * (uint64_t)std::max(kk - 1, 1) >= (uint64_t(1) << 32))
     return MOBA_ERR_UNSUPPORTED;
@@ -735,6 +749,25 @@ moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba
     MOBA_LAUNCH(launch_bwd_dq_cur(a, p, stream));
   }
   return MOBA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                          const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                          const moba_tensor* out, const moba_tensor* lse, const moba_tensor* dout,
+                          moba_tensor* dq, moba_tensor* dk, moba_tensor* dv, hipStream_t stream) {
+  return backward_impl(q, k, v, cu_seqlens, block_size, topk, out, lse, dout, dq, dk, dv, stream,
+                       false);
+}
+
+moba_status moba_dense_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
+                                const moba_tensor* cu_seqlens, const moba_tensor* out,
+                                const moba_tensor* lse, const moba_tensor* dout, moba_tensor* dq,
+                                moba_tensor* dk, moba_tensor* dv, hipStream_t stream) {
+  return backward_impl(q, k, v, cu_seqlens, 0, 0, out, lse, dout, dq, dk, dv, stream, true);
 }
 
 moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,

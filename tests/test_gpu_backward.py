@@ -69,3 +69,36 @@ def test_backward_rejects_f32():
     with pytest.raises(binding.MobaError) as e:
         binding.backward(q, k, v, cu, 32, 2, out, lse, torch.zeros_like(q))
     assert e.value.name == "MOBA_ERR_DTYPE"
+
+
+DENSE = [((300,), 2, 2), ((1000, 0, 517), 4, 2), ((129, 64, 1), 8, 1), ((1300,), 4, 1)]
+
+
+@pytest.mark.parametrize("seqlens,hq,hkv", DENSE,
+                         ids=["-".join(map(str, c[0])) + "_h%dx%d" % c[1:] for c in DENSE])
+def test_dense_backward(seqlens, hq, hkv):
+    """moba_dense_backward: gradients of causal full attention (Eq. 1), the
+    full-attention side of the per-call switch, against the oracle's gradients
+    for one block per sequence (every row attends its whole causal prefix)."""
+    from oracle import oracle
+
+    seed = sum(seqlens) + 11
+    q, k, v, cu = inputs.make(seqlens, hq, hkv, 128, torch.bfloat16, 64, 0.5, seed, device=DEV)
+    dout = inputs.make_dout(q.shape, torch.bfloat16, seed, device=DEV)
+    out, lse = binding.dense_forward(q, k, v, cu)
+    dq, dk, dv = binding.dense_backward(q, k, v, cu, out, lse, dout)
+    torch.cuda.synchronize()
+    T = q.shape[0]
+    B = max(max(seqlens), 1)
+    sel = np.zeros((T * hq, 1), np.int32)
+    qn, kn, vn = parity.host_inputs(q, k, v)
+    odq, odk, odv, cq, ck, cv = oracle.attend_backward(qn, kn, vn, inputs.to_oracle(dout),
+                                                       cu.numpy(), B, sel, kv_window="all",
+                                                       with_bounds=True)
+    for name, g, ref, c in (("dq", dq, odq, cq), ("dk", dk, odk, ck), ("dv", dv, odv, cv)):
+        g = g.float().cpu().numpy().astype(np.float64).reshape(ref.shape)
+        err = np.abs(g - ref)
+        ratio = float((err / (np.abs(ref) + c + 1e-30)).max())
+        mean_rel = float(err.mean() / np.abs(ref).mean())
+        print("%s: %.2e of (|ref| + c), mean %.2e" % (name, ratio, mean_rel))
+        assert ratio <= parity.BWD_ELEM_U and mean_rel <= parity.BWD_MEAN_REL, name
