@@ -151,6 +151,37 @@ moba_status moba_dense_backward(const moba_tensor* q, const moba_tensor* k, cons
                                 moba_tensor* dk, moba_tensor* dv, hipStream_t stream);
 
 /*
+ * Decode: one new query per sequence against its key/value cache.
+ *
+ * q [S, Hq, D] bf16: the new token of each sequence.  k_cache, v_cache
+ * [T, Hkv, D] bf16 hold every sequence's cached keys and values, packed as
+ * described by cu_seqlens [S+1] (int32, host or device; every sequence
+ * non-empty), and already include each new token's key and value as its
+ * sequence's last entry.  So query s sits at position L_s - 1 of sequence s
+ * and its result is the last row of the prefill over the cache:
+ *   topk >= 1: MoBA with block_size and topk (the gate of Eq. 5 / Eq. 6 over
+ *              the sequence's complete past blocks, top-k with the current
+ *              block counted, attention over the selected blocks and the
+ *              current block up to the query);
+ *   topk == 0: causal full attention over the whole cache (Eq. 1), which is
+ *              what the paper uses for generation (Sec. 3.3); block_size is
+ *              then ignored.
+ * kbar (nullable, MoBA only): the cache's block means as written by
+ * moba_pool for the same cu_seqlens and block_size; when NULL they are
+ * computed on the fly, which reads the whole key cache.  A decode loop keeps
+ * kbar and recomputes it only when a block completes.
+ * out [S, Hq, D] bf16 and lse [Hq, S] f32 (natural log) as for moba_forward.
+ * Hq / Hkv must not exceed 16.  Gate scores are fp32 sums over the dims in
+ * order; near-ties may be broken differently from moba_select's matrix-core
+ * gate.  Each call rebuilds the per-shape tables when cu_seqlens changes
+ * (one device synchronization).
+ */
+moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
+                        const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
+                        const moba_tensor* kbar, int32_t block_size, int32_t topk, moba_tensor* out,
+                        moba_tensor* lse, hipStream_t stream);
+
+/*
  * Block mean-pool of the keys (Eq. 6; Algorithm 1, mean_pool).
  * kbar [nblk_total, Hkv, D] f32 contiguous, device: row b = blk_off[s] + j
  * holds the mean of k over the tokens of block j of sequence s (a short last

@@ -61,6 +61,7 @@ def load() -> ctypes.CDLL:
         "moba_forward": [P, P, P, P, i32, i32, P, P, vp],
         "moba_backward": [P, P, P, P, i32, i32, P, P, P, P, P, P, vp],
         "moba_dense_backward": [P, P, P, P, P, P, P, P, P, P, vp],
+        "moba_decode": [P, P, P, P, P, i32, i32, P, P, vp],
         "moba_dense_forward": [P, P, P, P, P, P, vp],
         "moba_pool": [P, P, i32, P, vp],
         "moba_select": [P, P, P, i32, i32, P, P, vp],
@@ -178,6 +179,28 @@ def dense_backward(q, k, v, cu_seqlens, out, lse, dout, dq=None, dk=None, dv=Non
         _ref(d[0]), _ref(d[1]), _ref(d[2]), _ref(d[3]), _ref(d[4]), _ref(d[5]), _ref(d[6]),
         _ref(d[7]), _ref(d[8]), _ref(d[9]), _stream(q, stream)))
     return dq, dk, dv
+
+
+def decode(q, k_cache, v_cache, cu_seqlens, block_size: int, topk: int, kbar=None, out=None,
+           lse=None, stream=None):
+    """One new query per sequence against its cache (topk == 0: full
+    attention).  q [S, Hq, 128] bf16; k_cache/v_cache [T, Hkv, 128] bf16 with
+    each new token's key/value last in its sequence; kbar: optional block
+    means from pool().  Returns (out [S, Hq, 128], lse [Hq, S])."""
+    lib = load()
+    cu = _cu(cu_seqlens)
+    S, Hq = q.shape[0], q.shape[1]
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    if lse is None:
+        lse = torch.empty((Hq, S), dtype=torch.float32, device=q.device)
+    d = [describe(t) for t in (q, k_cache, v_cache, cu)]
+    dkb = describe(kbar) if kbar is not None else None
+    do, dl = describe(out), describe(lse)
+    _check("moba_decode", lib.moba_decode(_ref(d[0]), _ref(d[1]), _ref(d[2]), _ref(d[3]),
+                                          _ref(dkb), int(block_size), int(topk), _ref(do),
+                                          _ref(dl), _stream(q, stream)))
+    return out, lse
 
 
 def dense_forward(q, k, v, cu_seqlens, out=None, lse=None, stream=None):

@@ -1,0 +1,310 @@
+// Decode: one new query per sequence against its key/value cache.  Query s
+// sits at the last position L_s - 1 of sequence s (its key and value are the
+// cache's last entries), so its result is the last row of the prefill over
+// the cache: MoBA (the gate of Eq. 5 / Eq. 6 with the causal rules of
+// Sec. 2.2, attention of Eq. 2 over the key set of Eq. 4) or causal full
+// attention (Eq. 1), which is what the paper uses for generation (Sec. 3.3).
+//
+// Decode reads each attended key once per kv-head and does ~2 FLOP per byte,
+// far below the ridge of either the matrix cores or the vector ALUs, so it is
+// bound by HBM: the kernels use the vector ALUs, read K rows one per lane and
+// V rows coalesced, and in MoBA mode touch only the selected blocks.
+//
+//   gate     one wave per (sequence, query head): fp32 scores of the query
+//            against the block means of the sequence's complete past blocks
+//            (sequential fp32 sums, one block per lane), then top-(k-1) by
+//            k-1 rounds of a wave-wide argmax (ties: lower block index), and
+//            the selection written ascending with the current block last.
+//   attend   one work-group per (sequence, kv-head, 256-key chunk; chunks
+//            never cross a block boundary), all query heads of the group:
+//            scores with one key per lane, a per-head softmax over the chunk,
+//            P V with one dimension pair per lane and 64 keys per wave; the
+//            normalised partial and its lse go to the workspace.  In MoBA
+//            mode a chunk whose block no head of the group selected exits.
+//   combine  one row per 16 lanes: log-sum-exp merge of the row's partials
+//            in chunk order, rounded once to the output dtype.
+#include "decode_internal.h"
+
+#include <math.h>
+
+namespace moba {
+namespace {
+
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Key range of chunk x of sequence length L: block j = x / nsub, piece
+// i = x % nsub of kDecodeChunk keys, cut at the block end and at L.
+__device__ __forceinline__ void chunk_range(int x, int nsub, int B, int64_t L, int64_t& u0,
+                                            int64_t& u1) {
+  const int64_t j = x / nsub, i = x % nsub;
+  u0 = j * B + i * kDecodeChunk;
+  u1 = min(min(u0 + kDecodeChunk, (j + 1) * (int64_t)B), L);
+}
+
+// ================================================================== gate
+__global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem p) {
+  __shared__ float qs[4][kHeadDim];
+  __shared__ float sc[4][kMaxBlocksPerSeq];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;  // s * Hq + h
+  const bool active = row < (int64_t)p.S * p.Hq;
+  const int s = active ? (int)(row / p.Hq) : 0;
+  const int h = active ? (int)(row % p.Hq) : 0;
+  const int g = h / p.G;
+  const SeqInfo sq = a.seqs[s];
+  if (active) {
+    const __hip_bfloat16* qr = a.q + (int64_t)s * a.q_ss + (int64_t)h * a.q_sh;
+    const uint32_t w = reinterpret_cast<const uint32_t*>(qr)[lane];
+    qs[wave][2 * lane] = bf16_lo(w);
+    qs[wave][2 * lane + 1] = bf16_hi(w);
+  }
+  __syncthreads();
+  if (!active) return;
+  const int c = (int)((sq.len - 1) / p.B);  // current block; candidates j < c
+  // scores, one block per lane, dims in order
+  for (int j = lane; j < c; j += 64) {
+    const float* kb = a.kbar + ((int64_t)(sq.blk_off + j) * p.Hkv + g) * kHeadDim;
+    float acc = 0.0f;
+#pragma unroll 8
+    for (int d = 0; d < kHeadDim; d += 4) {
+      const float4 kv = *reinterpret_cast<const float4*>(kb + d);
+      acc = fmaf(qs[wave][d], kv.x, acc);
+      acc = fmaf(qs[wave][d + 1], kv.y, acc);
+      acc = fmaf(qs[wave][d + 2], kv.z, acc);
+      acc = fmaf(qs[wave][d + 3], kv.w, acc);
+    }
+    sc[wave][j] = acc;
+  }
+  // top-(k-1): rounds of a wave-wide argmax over (score desc, index asc);
+  // lane L owns candidates L, L + 64, ... and marks its taken ones in a mask
+  const int kh = p.topk - 1;
+  const int nh = min(kh, c);
+  uint64_t taken = 0;
+  for (int r = 0; r < nh; r++) {
+    float best = -INFINITY;
+    int bj = INT32_MAX;
+    for (int j = lane, x = 0; j < c; j += 64, x++) {
+      if ((taken >> x) & 1) continue;
+      const float v = sc[wave][j];
+      if (v > best || (v == best && j < bj)) { best = v; bj = j; }
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float ob = __shfl_xor(best, m, 64);
+      const int oj = __shfl_xor(bj, m, 64);
+      if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+    }
+    if (bj < c && bj % 64 == lane) taken |= uint64_t(1) << (bj / 64);
+  }
+  // ascending: round x covers candidates 64x .. 64x+63, one per lane
+  int32_t* out = a.sel + row * p.topk;
+  int pos = 0;
+  for (int x = 0; 64 * x < c; x++) {
+    const bool mine = (taken >> x) & 1;
+    const uint64_t bal = __ballot(mine);
+    if (mine) out[pos + __popcll(bal & ((uint64_t(1) << lane) - 1))] = 64 * x + lane;
+    pos += __popcll(bal);
+  }
+  if (lane == 0) out[nh] = c;
+  for (int x = nh + 1 + lane; x < p.topk; x += 64) out[x] = -1;
+}
+
+// ================================================================ attend
+__global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Problem p) {
+  __shared__ float qs[kDecodeMaxGroup][kHeadDim];
+  __shared__ float ps[kDecodeMaxGroup][kDecodeChunk];
+  __shared__ float red[4][kDecodeMaxGroup][2];
+  __shared__ float2 accs[4][kDecodeMaxGroup][64];
+  __shared__ int use_head[kDecodeMaxGroup];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int x = blockIdx.x;
+  const int s = blockIdx.y / p.Hkv, g = blockIdx.y % p.Hkv;
+  const SeqInfo sq = a.seqs[s];
+  const int G = p.G;
+  int64_t u0, u1;
+  chunk_range(x, a.nsub, a.chunk_block, sq.len, u0, u1);
+  if (u0 >= u1) return;
+  // heads of the group that attend this chunk
+  if (tid < G) {
+    const int h = g * G + tid;
+    int use = 1;
+    if (!a.full) {
+      const int j = (int)(u0 / p.B);
+      const int32_t* sl = a.sel + ((int64_t)s * p.Hq + h) * p.topk;
+      use = 0;
+      for (int y = 0; y < p.topk; y++) use |= sl[y] == j;
+    }
+    use_head[tid] = use;
+  }
+  for (int i = tid; i < G * (kHeadDim / 2); i += 256) {
+    const int hl = i / (kHeadDim / 2), d2 = i % (kHeadDim / 2);
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + (int64_t)s * a.q_ss +
+                                                         (int64_t)(g * G + hl) * a.q_sh)[d2];
+    qs[hl][2 * d2] = bf16_lo(w);
+    qs[hl][2 * d2 + 1] = bf16_hi(w);
+  }
+  __syncthreads();
+  int any = 0;
+  for (int hl = 0; hl < G; hl++) any |= use_head[hl];
+  if (!any) return;
+
+  // scores: lane = key u0 + 64 * wave + lane
+  const int64_t u = u0 + 64 * wave + lane;
+  const bool kv_ok = u < u1;
+  float kr[kHeadDim];
+  {
+    const int64_t t = sq.tok_start + (kv_ok ? u : u0);
+    const uint4* kp = reinterpret_cast<const uint4*>(a.k + t * a.k_st + (int64_t)g * a.k_sh);
+#pragma unroll
+    for (int c8 = 0; c8 < kHeadDim / 8; c8++) {
+      const uint4 w = kp[c8];
+      kr[8 * c8 + 0] = bf16_lo(w.x); kr[8 * c8 + 1] = bf16_hi(w.x);
+      kr[8 * c8 + 2] = bf16_lo(w.y); kr[8 * c8 + 3] = bf16_hi(w.y);
+      kr[8 * c8 + 4] = bf16_lo(w.z); kr[8 * c8 + 5] = bf16_hi(w.z);
+      kr[8 * c8 + 6] = bf16_lo(w.w); kr[8 * c8 + 7] = bf16_hi(w.w);
+    }
+  }
+  const float c2 = a.scale_log2;
+  for (int hl = 0; hl < G; hl++) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int d = 0; d < kHeadDim; d++) acc = fmaf(qs[hl][d], kr[d], acc);
+    const float sv = kv_ok ? acc * c2 : -INFINITY;
+    float m = sv;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    ps[hl][64 * wave + lane] = sv;
+    if (lane == 0) red[wave][hl][0] = m;
+  }
+  __syncthreads();
+  // per head: chunk max, weights, sum
+  for (int hl = 0; hl < G; hl++) {
+    const float m = fmaxf(fmaxf(red[0][hl][0], red[1][hl][0]), fmaxf(red[2][hl][0], red[3][hl][0]));
+    const float pv = kv_ok ? __builtin_amdgcn_exp2f(ps[hl][64 * wave + lane] - m) : 0.0f;
+    ps[hl][64 * wave + lane] = pv;
+    float l = pv;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o, 64);
+    if (lane == 0) red[wave][hl][1] = l;
+  }
+  __syncthreads();
+  // P V: wave w sums keys 64w .. 64w+63 for dims 2*lane, 2*lane+1
+  float2 acc[kDecodeMaxGroup];
+#pragma unroll
+  for (int hl = 0; hl < kDecodeMaxGroup; hl++) acc[hl] = make_float2(0.0f, 0.0f);
+  const int64_t kend = min((int64_t)64, u1 - (u0 + 64 * wave));
+  for (int kk = 0; kk < kend; kk++) {
+    const int64_t t = sq.tok_start + u0 + 64 * wave + kk;
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.v + t * a.v_st + (int64_t)g * a.v_sh)[lane];
+    const float v0 = bf16_lo(w), v1 = bf16_hi(w);
+#pragma unroll
+    for (int hl = 0; hl < kDecodeMaxGroup; hl++) {
+      if (hl < G) {
+        const float pw = ps[hl][64 * wave + kk];
+        acc[hl].x = fmaf(pw, v0, acc[hl].x);
+        acc[hl].y = fmaf(pw, v1, acc[hl].y);
+      }
+    }
+  }
+#pragma unroll
+  for (int hl = 0; hl < kDecodeMaxGroup; hl++)
+    if (hl < G) accs[wave][hl][lane] = acc[hl];
+  __syncthreads();
+  // normalised partial and lse per attending head; wave w handles heads w, w+4, ...
+  for (int hl = wave; hl < G; hl += 4) {
+    if (!use_head[hl]) continue;
+    const float m = fmaxf(fmaxf(red[0][hl][0], red[1][hl][0]), fmaxf(red[2][hl][0], red[3][hl][0]));
+    const float l = red[0][hl][1] + red[1][hl][1] + red[2][hl][1] + red[3][hl][1];
+    const float inv = 1.0f / l;
+    float2 o = accs[0][hl][lane];
+#pragma unroll
+    for (int w = 1; w < 4; w++) {
+      o.x += accs[w][hl][lane].x;
+      o.y += accs[w][hl][lane].y;
+    }
+    const int64_t pr = ((int64_t)s * p.Hq + g * G + hl) * a.nchunk + x;
+    reinterpret_cast<float2*>(a.part_o + pr * kHeadDim)[lane] = make_float2(o.x * inv, o.y * inv);
+    if (lane == 0) a.part_lse[pr] = (m + __builtin_amdgcn_logf(l)) * kLn2;
+  }
+}
+
+// =============================================================== combine
+__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Problem p) {
+  const int64_t row = (int64_t)blockIdx.x * 16 + threadIdx.x / 16;  // s * Hq + h
+  const int l16 = threadIdx.x % 16;
+  if (row >= (int64_t)p.S * p.Hq) return;
+  const int s = (int)(row / p.Hq), h = (int)(row % p.Hq);
+  const SeqInfo sq = a.seqs[s];
+  float M = -INFINITY, wsum = 0.0f, acc[8];
+#pragma unroll
+  for (int d = 0; d < 8; d++) acc[d] = 0.0f;
+  auto fold = [&](int x) {
+    const int64_t pr = row * a.nchunk + x;
+    const float lv = a.part_lse[pr];
+    const float4* op = reinterpret_cast<const float4*>(a.part_o + pr * kHeadDim + 8 * l16);
+    const float4 o0 = op[0], o1 = op[1];
+    const float Mn = fmaxf(M, lv);
+    const float sc = __builtin_amdgcn_exp2f((M - Mn) * kLog2e);
+    const float w = __builtin_amdgcn_exp2f((lv - Mn) * kLog2e);
+    const float f[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+#pragma unroll
+    for (int d = 0; d < 8; d++) acc[d] = fmaf(w, f[d], acc[d] * sc);
+    wsum = wsum * sc + w;
+    M = Mn;
+  };
+  if (a.full) {
+    const int n = (int)((sq.len + kDecodeChunk - 1) / kDecodeChunk);
+    for (int x = 0; x < n; x++) fold(x);
+  } else {
+    const int32_t* sl = a.sel + row * p.topk;
+    for (int y = 0; y < p.topk; y++) {
+      const int j = sl[y];
+      if (j < 0) break;
+      for (int i = 0; i < a.nsub; i++) {
+        const int64_t u0 = (int64_t)j * p.B + (int64_t)i * kDecodeChunk;
+        if (u0 >= min((int64_t)(j + 1) * p.B, (int64_t)sq.len)) break;
+        fold(j * a.nsub + i);
+      }
+    }
+  }
+  const float inv = 1.0f / wsum;
+  uint32_t w[4];
+#pragma unroll
+  for (int e = 0; e < 4; e++) {
+    const float lo = acc[2 * e] * inv, hi = acc[2 * e + 1] * inv;
+    w[e] = (uint32_t)__bfloat16_as_ushort(__float2bfloat16(lo)) |
+           ((uint32_t)__bfloat16_as_ushort(__float2bfloat16(hi)) << 16);
+  }
+  *reinterpret_cast<uint4*>(a.out + (int64_t)s * a.o_ss + (int64_t)h * a.o_sh + 8 * l16) =
+      make_uint4(w[0], w[1], w[2], w[3]);
+  if (l16 == 0) a.lse[(int64_t)h * p.S + s] = M + __builtin_amdgcn_logf(wsum) * kLn2;
+}
+
+}  // namespace
+
+hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t st) {
+  const int64_t rows = (int64_t)p.S * p.Hq;
+  if (rows <= 0 || a.full) return hipSuccess;
+  decode_gate_kernel<<<(unsigned)((rows + 3) / 4), 256, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream_t st) {
+  if (p.S <= 0 || a.nchunk <= 0) return hipSuccess;
+  dim3 grid((unsigned)a.nchunk, (unsigned)(p.S * p.Hkv));
+  decode_attend_kernel<<<grid, 256, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_combine(const DecodeArgs& a, const Problem& p, hipStream_t st) {
+  const int64_t rows = (int64_t)p.S * p.Hq;
+  if (rows <= 0) return hipSuccess;
+  decode_combine_kernel<<<(unsigned)((rows + 15) / 16), 256, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
+}  // namespace moba

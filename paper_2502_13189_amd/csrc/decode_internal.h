@@ -1,0 +1,36 @@
+// Internal declarations of the decode path (one new query per sequence
+// against its key/value cache), shared by the host library and the kernels.
+#pragma once
+
+#include "moba_internal.h"
+
+namespace moba {
+
+constexpr int kDecodeChunk = 256;     // keys per attention work-group
+constexpr int kDecodeMaxGroup = 16;   // largest Hq / Hkv the decode kernels take
+
+struct DecodeArgs {
+  const __hip_bfloat16* q; int64_t q_ss, q_sh;  // [S, Hq, D]
+  const __hip_bfloat16* k; int64_t k_st, k_sh;  // cache [T, Hkv, D]
+  const __hip_bfloat16* v; int64_t v_st, v_sh;
+  const float* kbar;     // [nblk_total, Hkv, D] block means of the cache (MoBA)
+  const SeqInfo* seqs;   // per cached sequence
+  int32_t* sel;          // [S, Hq, topk] selection (MoBA)
+  float* part_o;         // [S * Hq, nchunk, D] normalised partials
+  float* part_lse;       // [S * Hq, nchunk]
+  __hip_bfloat16* out; int64_t o_ss, o_sh;  // [S, Hq, D]
+  float* lse;            // [Hq, S]
+  int nsub;              // chunks per block
+  int nchunk;            // chunk slots per row
+  int chunk_block;       // block length the chunks are cut at
+  int full;              // 1: causal full attention, 0: MoBA
+  float scale_log2;
+};
+
+// Every launcher enqueues on `st` and returns the launch status.  p.S is the
+// number of sequences (= queries), p.T the cache length.
+hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t st);
+hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream_t st);
+hipError_t launch_decode_combine(const DecodeArgs& a, const Problem& p, hipStream_t st);
+
+}  // namespace moba

@@ -13,6 +13,7 @@
 // workspace cap limits.
 #include "moba.h"
 #include "bwd_internal.h"
+#include "decode_internal.h"
 #include "moba_internal.h"
 
 #include <algorithm>
@@ -811,6 +812,116 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
   { Phase ph("dense", stream);
     MOBA_LAUNCH(in.bf16 ? launch_attn_causal_bf16(true, a, p, stream)
                         : launch_attn_causal_f32(true, a, p, stream)); }
+  return MOBA_OK;
+}
+
+moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
+                        const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
+                        const moba_tensor* kbar, int32_t block_size, int32_t topk, moba_tensor* out,
+                        moba_tensor* lse, hipStream_t stream) {
+  if (missing(q) || missing(k_cache) || missing(v_cache) || missing(out) || missing(lse) ||
+      !cu_seqlens || !cu_seqlens->data)
+    return MOBA_ERR_NULL;
+  if (q->dtype != MOBA_BF16) return MOBA_ERR_DTYPE;
+  View vq, vk, vv, vo;
+  moba_status st;
+  if ((st = check_3d(q, MOBA_BF16, &vq)) != MOBA_OK) return st;
+  if ((st = check_3d(k_cache, MOBA_BF16, &vk)) != MOBA_OK) return st;
+  if ((st = check_3d(v_cache, MOBA_BF16, &vv)) != MOBA_OK) return st;
+  if ((st = check_3d(out, MOBA_BF16, &vo)) != MOBA_OK) return st;
+  const int64_t S = q->shape[0], T = k_cache->shape[0];
+  const int Hq = (int)q->shape[1], Hkv = (int)k_cache->shape[1];
+  if (v_cache->shape[0] != T || v_cache->shape[1] != Hkv || out->shape[0] != S ||
+      out->shape[1] != Hq || Hq % Hkv != 0)
+    return MOBA_ERR_SHAPE;
+  if (Hq / Hkv > kDecodeMaxGroup) return MOBA_ERR_UNSUPPORTED;
+  const int64_t lshape[2] = {Hq, S};
+  if ((st = check_contig(lse, MOBA_F32, 2, lshape)) != MOBA_OK) return st;
+  if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
+  if (cu_seqlens->shape[0] != S + 1) return MOBA_ERR_SHAPE;
+  if (topk < 0) return MOBA_ERR_TOPK;
+  const bool full = topk == 0;
+  if (!full && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (T >= (int64_t(1) << 31)) return MOBA_ERR_UNSUPPORTED;
+  std::vector<int32_t> cu;
+  if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
+  if (S == 0) return MOBA_OK;
+  int64_t lmax = 0;
+  for (int64_t s = 0; s < S; s++) {
+    if (cu[s + 1] == cu[s]) return MOBA_ERR_SEQLENS;  // every query needs its own cached token
+    lmax = std::max<int64_t>(lmax, (int64_t)cu[s + 1] - cu[s]);
+  }
+  const int B = full ? kDecodeChunk : block_size;
+  const int64_t nbmax = ceil_div(lmax, B);
+  if (!full && nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
+  const int kk = full ? 1 : (int)std::min<int64_t>(topk, nbmax);
+  if (kbar && !full) {
+    if (missing(kbar)) return MOBA_ERR_NULL;
+    int64_t nb = 0;
+    for (int64_t s = 0; s < S; s++) nb += ceil_div((int64_t)cu[s + 1] - cu[s], block_size);
+    const int64_t ks[3] = {nb, Hkv, kHeadDim};
+    if ((st = check_contig(kbar, MOBA_F32, 3, ks)) != MOBA_OK) return st;
+  }
+
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  const Plan* pl;
+  const SeqInfo* d_seqs;
+  const CausalTile* d_tiles;
+  if ((st = get_plan(dc, cu, Hkv, Hkv, B, kk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+                     &d_tiles)) != MOBA_OK)
+    return st;
+  Problem p = pl->p;
+  p.S = (int)S;
+  p.Hq = Hq;
+  p.G = Hq / Hkv;
+  p.topk = kk;
+  const int nsub = full ? 1 : (int)ceil_div(B, kDecodeChunk);
+  const int64_t nchunk = nbmax * nsub;
+  const bool own_kbar = !full && !kbar;
+  auto layout = [&](Bump* bp, float** kb, int32_t** sel, float** po, float** pls) {
+    *kb = bp->take<float>(own_kbar ? (int64_t)p.nblk_total * Hkv * kHeadDim : 0);
+    *sel = bp->take<int32_t>(full ? 0 : S * Hq * kk);
+    *po = bp->take<float>(S * Hq * nchunk * kHeadDim);
+    *pls = bp->take<float>(S * Hq * nchunk);
+  };
+  {
+    Bump sz(nullptr);
+    float *a0, *a2, *a3;
+    int32_t* a1;
+    layout(&sz, &a0, &a1, &a2, &a3);
+    if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
+    if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
+  }
+  Bump bp(dc->ws);
+  DecodeArgs a{};
+  float* kb_ws;
+  layout(&bp, &kb_ws, &a.sel, &a.part_o, &a.part_lse);
+  a.q = static_cast<const __hip_bfloat16*>(vq.data); a.q_ss = vq.st; a.q_sh = vq.sh;
+  a.k = static_cast<const __hip_bfloat16*>(vk.data); a.k_st = vk.st; a.k_sh = vk.sh;
+  a.v = static_cast<const __hip_bfloat16*>(vv.data); a.v_st = vv.st; a.v_sh = vv.sh;
+  a.out = static_cast<__hip_bfloat16*>(vo.data); a.o_ss = vo.st; a.o_sh = vo.sh;
+  a.lse = static_cast<float*>(lse->data);
+  a.kbar = own_kbar ? kb_ws : (full ? nullptr : static_cast<const float*>(kbar->data));
+  a.seqs = d_seqs;
+  a.nsub = nsub;
+  a.nchunk = (int)nchunk;
+  a.chunk_block = B;
+  a.full = full ? 1 : 0;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)kHeadDim));
+  if (own_kbar) {
+    Phase ph("pool", stream);
+    MOBA_LAUNCH(launch_pool(vk.data, true, vk.st, vk.sh, d_seqs, p, kb_ws, stream));
+  }
+  if (!full) {
+    Phase ph("decode_gate", stream);
+    MOBA_LAUNCH(launch_decode_gate(a, p, stream));
+  }
+  { Phase ph("decode_attend", stream);
+    MOBA_LAUNCH(launch_decode_attend(a, p, stream)); }
+  { Phase ph("decode_combine", stream);
+    MOBA_LAUNCH(launch_decode_combine(a, p, stream)); }
   return MOBA_OK;
 }
 
