@@ -3,6 +3,7 @@
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--dense-steps N] [--no-cpu]
     python bench.py --sweep fig2a|fig2b|gran [--sweep-steps K] [--sweep-lengths L1,L2,..]
     python bench.py --backward [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --decode [--steps K] [--workload NAME]
 
 One step = one moba_forward call over the whole workload (pool, gate, route,
 history and current-block attention, merge), inputs resident in HBM.  The
@@ -263,6 +264,63 @@ def run_backward(args):
     }), flush=True)
 
 
+def run_decode(args):
+    """Decode on the workload's cache: one new query per sequence (the last
+    token's), full attention (the paper's choice for generation) and MoBA
+    with the cache's block means kept by the caller.  One JSON line with both
+    latencies and their HBM rates: bytes = the K/V rows each mode must read
+    (full: every cached key of every kv-head; MoBA: the union of the blocks
+    the group's query heads select, from the prefill gate's selection of the
+    same rows) plus the queries, block means and outputs."""
+    w = inputs.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    print("[bench] generating %s" % w.name, file=sys.stderr, flush=True)
+    q, k, v, cu = inputs.make_workload(w, device=dev)
+    last = (cu[1:] - 1).to(torch.int64).to(dev)
+    qd = q[last].contiguous()
+    S, Hq, Hkv, D, B = len(w.seqlens), w.hq, w.hkv, w.d, w.block_size
+    G = Hq // Hkv
+    kbar = binding.pool(k, cu, B)
+    sel = binding.select(q, k, cu, B, w.topk)[last].cpu().numpy()  # [S, Hq, topk]
+    del q
+    torch.cuda.synchronize()
+    out = torch.empty_like(qd)
+    lse = torch.empty((Hq, S), dtype=torch.float32, device=dev)
+    res = {}
+    for mode, kk in (("full", 0), ("moba", w.topk)):
+        step = lambda: binding.decode(qd, k, v, cu, B, kk, kbar=kbar, out=out, lse=lse)
+        for _ in range(max(args.warmup, 1)):
+            step()
+        torch.cuda.synchronize()
+        binding.profile_read()
+        binding.profile_enable(True)
+        t0 = time.perf_counter()
+        n = max(args.steps, 1) * 20
+        for _ in range(n):
+            step()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / n
+        binding.profile_enable(False)
+        phases = binding.profile_read()
+        if mode == "full":
+            kv_rows = sum(w.seqlens) * Hkv
+        else:
+            kv_rows = 0
+            for s_, L in enumerate(w.seqlens):
+                for g in range(Hkv):
+                    blocks = set(int(j) for j in sel[s_, g * G:(g + 1) * G].ravel() if j >= 0)
+                    kv_rows += sum(min(B, L - j * B) for j in blocks)
+        nbytes = kv_rows * 2 * D * 2 + S * Hq * D * 2 * 2 + (kbar.numel() * 4 if mode == "moba" else 0)
+        res[mode] = {"ms": round(ms, 4), "kv_rows_read": kv_rows, "bytes": nbytes,
+                     "gb_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "phases_ms": {k_: round(t / c, 4) for k_, (c, t) in phases.items()}}
+    print(json.dumps({"mode": "decode", "workload": w.name, "queries": S * Hq, "dtype": "bf16",
+                      "data": "synthetic", "full": res["full"], "moba": res["moba"],
+                      "speedup_moba_vs_full": round(res["full"]["ms"] / res["moba"]["ms"], 3)}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,6 +338,8 @@ def main():
     ap.add_argument("--sweep-dense-max", type=int, default=1 << 20)
     ap.add_argument("--backward", action="store_true",
                     help="time moba_backward on the workload instead (one JSON line)")
+    ap.add_argument("--decode", action="store_true",
+                    help="time moba_decode (full and MoBA) on the workload's cache instead")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -295,6 +355,9 @@ def main():
         return
     if args.backward:
         run_backward(args)
+        return
+    if args.decode:
+        run_decode(args)
         return
     w = inputs.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")

@@ -21,8 +21,9 @@
 //            P V with one dimension pair per lane and 64 keys per wave; the
 //            normalised partial and its lse go to the workspace.  In MoBA
 //            mode a chunk whose block no head of the group selected exits.
-//   combine  one row per 16 lanes: log-sum-exp merge of the row's partials
-//            in chunk order, rounded once to the output dtype.
+//   combine  one work-group per row: log-sum-exp merge of the row's
+//            partials (16 interleaved groups, then the groups in order),
+//            rounded once to the output dtype.
 #include "decode_internal.h"
 
 #include <math.h>
@@ -196,17 +197,24 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   float2 acc[kDecodeMaxGroup];
 #pragma unroll
   for (int hl = 0; hl < kDecodeMaxGroup; hl++) acc[hl] = make_float2(0.0f, 0.0f);
-  const int64_t kend = min((int64_t)64, u1 - (u0 + 64 * wave));
-  for (int kk = 0; kk < kend; kk++) {
-    const int64_t t = sq.tok_start + u0 + 64 * wave + kk;
-    const uint32_t w = reinterpret_cast<const uint32_t*>(a.v + t * a.v_st + (int64_t)g * a.v_sh)[lane];
-    const float v0 = bf16_lo(w), v1 = bf16_hi(w);
+  const int kend = (int)min((int64_t)64, u1 - (u0 + 64 * wave));
+  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(
+      a.v + (sq.tok_start + u0 + 64 * wave) * a.v_st + (int64_t)g * a.v_sh) + lane;
+  for (int k0 = 0; k0 < kend; k0 += 8) {
+    // eight V rows in flight, then their FMAs
+    uint32_t wv[8];
 #pragma unroll
-    for (int hl = 0; hl < kDecodeMaxGroup; hl++) {
-      if (hl < G) {
-        const float pw = ps[hl][64 * wave + kk];
-        acc[hl].x = fmaf(pw, v0, acc[hl].x);
-        acc[hl].y = fmaf(pw, v1, acc[hl].y);
+    for (int e = 0; e < 8; e++) wv[e] = k0 + e < kend ? vrow[(int64_t)(k0 + e) * a.v_st / 2] : 0u;
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      const float v0 = bf16_lo(wv[e]), v1 = bf16_hi(wv[e]);
+#pragma unroll
+      for (int hl = 0; hl < kDecodeMaxGroup; hl++) {
+        if (hl < G) {
+          const float pw = k0 + e < kend ? ps[hl][64 * wave + k0 + e] : 0.0f;
+          acc[hl].x = fmaf(pw, v0, acc[hl].x);
+          acc[hl].y = fmaf(pw, v1, acc[hl].y);
+        }
       }
     }
   }
@@ -233,10 +241,14 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
 }
 
 // =============================================================== combine
+// One work-group per row: 16 groups of 16 lanes each fold every 16th of the
+// row's partials (8 dims per lane, online rescale), then the 16 group results
+// are merged in group order.
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Problem p) {
-  const int64_t row = (int64_t)blockIdx.x * 16 + threadIdx.x / 16;  // s * Hq + h
-  const int l16 = threadIdx.x % 16;
-  if (row >= (int64_t)p.S * p.Hq) return;
+  __shared__ float gm[16], gw[16];
+  __shared__ float go[16][kHeadDim];
+  const int64_t row = blockIdx.x;  // s * Hq + h
+  const int grp = threadIdx.x / 16, l16 = threadIdx.x % 16;
   const int s = (int)(row / p.Hq), h = (int)(row % p.Hq);
   const SeqInfo sq = a.seqs[s];
   float M = -INFINITY, wsum = 0.0f, acc[8];
@@ -258,30 +270,41 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
   };
   if (a.full) {
     const int n = (int)((sq.len + kDecodeChunk - 1) / kDecodeChunk);
-    for (int x = 0; x < n; x++) fold(x);
+    for (int x = grp; x < n; x += 16) fold(x);
   } else {
+    // the row's chunks: z = y * nsub + i for selection entry y, piece i
     const int32_t* sl = a.sel + row * p.topk;
-    for (int y = 0; y < p.topk; y++) {
+    for (int z = grp; z < p.topk * a.nsub; z += 16) {
+      const int y = z / a.nsub, i = z % a.nsub;
       const int j = sl[y];
-      if (j < 0) break;
-      for (int i = 0; i < a.nsub; i++) {
-        const int64_t u0 = (int64_t)j * p.B + (int64_t)i * kDecodeChunk;
-        if (u0 >= min((int64_t)(j + 1) * p.B, (int64_t)sq.len)) break;
-        fold(j * a.nsub + i);
-      }
+      if (j < 0) continue;
+      const int64_t u0 = (int64_t)j * p.B + (int64_t)i * kDecodeChunk;
+      if (u0 >= min((int64_t)(j + 1) * p.B, (int64_t)sq.len)) continue;
+      fold(j * a.nsub + i);
     }
   }
-  const float inv = 1.0f / wsum;
-  uint32_t w[4];
 #pragma unroll
-  for (int e = 0; e < 4; e++) {
-    const float lo = acc[2 * e] * inv, hi = acc[2 * e + 1] * inv;
-    w[e] = (uint32_t)__bfloat16_as_ushort(__float2bfloat16(lo)) |
-           ((uint32_t)__bfloat16_as_ushort(__float2bfloat16(hi)) << 16);
+  for (int d = 0; d < 8; d++) go[grp][8 * l16 + d] = acc[d];
+  if (l16 == 0) {
+    gm[grp] = M;
+    gw[grp] = wsum;
   }
-  *reinterpret_cast<uint4*>(a.out + (int64_t)s * a.o_ss + (int64_t)h * a.o_sh + 8 * l16) =
-      make_uint4(w[0], w[1], w[2], w[3]);
-  if (l16 == 0) a.lse[(int64_t)h * p.S + s] = M + __builtin_amdgcn_logf(wsum) * kLn2;
+  __syncthreads();
+  if (threadIdx.x >= kHeadDim) return;
+  const int d = threadIdx.x;
+  float Mt = -INFINITY;
+#pragma unroll
+  for (int x = 0; x < 16; x++) Mt = fmaxf(Mt, gm[x]);
+  float o = 0.0f, wt = 0.0f;
+#pragma unroll
+  for (int x = 0; x < 16; x++) {
+    if (gw[x] == 0.0f) continue;  // a group without partials
+    const float sc = __builtin_amdgcn_exp2f((gm[x] - Mt) * kLog2e);
+    o = fmaf(sc, go[x][d], o);
+    wt = fmaf(sc, gw[x], wt);
+  }
+  a.out[(int64_t)s * a.o_ss + (int64_t)h * a.o_sh + d] = __float2bfloat16(o / wt);
+  if (d == 0) a.lse[(int64_t)h * p.S + s] = Mt + __builtin_amdgcn_logf(wt) * kLn2;
 }
 
 }  // namespace
@@ -303,7 +326,7 @@ hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream
 hipError_t launch_decode_combine(const DecodeArgs& a, const Problem& p, hipStream_t st) {
   const int64_t rows = (int64_t)p.S * p.Hq;
   if (rows <= 0) return hipSuccess;
-  decode_combine_kernel<<<(unsigned)((rows + 15) / 16), 256, 0, st>>>(a, p);
+  decode_combine_kernel<<<(unsigned)rows, 256, 0, st>>>(a, p);
   return hipGetLastError();
 }
 
