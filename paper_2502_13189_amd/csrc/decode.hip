@@ -15,12 +15,15 @@
 //            (sequential fp32 sums, one block per lane), then top-(k-1) by
 //            k-1 rounds of a wave-wide argmax (ties: lower block index), and
 //            the selection written ascending with the current block last.
+//   plan     (MoBA) one wave per (sequence, kv-head): the union of the
+//            blocks the group's query heads selected, ascending.
 //   attend   one work-group per (sequence, kv-head, 256-key chunk; chunks
-//            never cross a block boundary), all query heads of the group:
+//            never cross a block boundary; in MoBA mode only the chunks of
+//            the group's selected blocks), all query heads of the group:
 //            scores with one key per lane, a per-head softmax over the chunk,
 //            P V with one dimension pair per lane and 64 keys per wave; the
-//            normalised partial and its lse go to the workspace.  In MoBA
-//            mode a chunk whose block no head of the group selected exits.
+//            normalised partial and its lse go to the workspace; a head that
+//            did not select the chunk's block skips it.
 //   combine  one work-group per row: log-sum-exp merge of the row's
 //            partials (16 interleaved groups, then the groups in order),
 //            rounded once to the output dtype.
@@ -114,16 +117,59 @@ __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem 
   for (int x = nh + 1 + lane; x < p.topk; x += 64) out[x] = -1;
 }
 
+// ================================================================== plan
+// One wave per (sequence, kv-head): a bitmask of the blocks any query head
+// of the group selected, written out ascending (lane w owns mask word w).
+__global__ __launch_bounds__(64) void decode_plan_kernel(DecodeArgs a, Problem p) {
+  __shared__ unsigned long long mask[kMaxBlocksPerSeq / 64];
+  const int lane = threadIdx.x;
+  const int s = blockIdx.x / p.Hkv, g = blockIdx.x % p.Hkv;
+  mask[lane] = 0;
+  __syncthreads();
+  for (int i = lane; i < p.G * p.topk; i += 64) {
+    const int h = g * p.G + i / p.topk;
+    const int j = a.sel[((int64_t)s * p.Hq + h) * p.topk + i % p.topk];
+    if (j >= 0) atomicOr(&mask[j >> 6], 1ull << (j & 63));
+  }
+  __syncthreads();
+  const unsigned long long w = mask[lane];
+  int before = __popcll(w);  // exclusive prefix of the set-bit counts over lanes
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(before, d, 64);
+    if (lane >= d) before += o;
+  }
+  before -= __popcll(w);
+  int32_t* out = a.blocks + (int64_t)blockIdx.x * a.nunion;
+  unsigned long long rest = w;
+  int pos = before;
+  while (rest) {
+    const int b = __ffsll((long long)rest) - 1;
+    out[pos++] = 64 * lane + b;
+    rest &= rest - 1;
+  }
+  const int total = __shfl(before + __popcll(w), 63, 64);
+  for (int x = total + lane; x < a.nunion; x += 64) out[x] = -1;
+}
+
 // ================================================================ attend
+// GM: the group size rounded up to a power of two (sizes the LDS arrays, so
+// small groups leave room for more resident work-groups).
+template <int GM>
 __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Problem p) {
-  __shared__ float qs[kDecodeMaxGroup][kHeadDim];
-  __shared__ float ps[kDecodeMaxGroup][kDecodeChunk];
-  __shared__ float red[4][kDecodeMaxGroup][2];
-  __shared__ float2 accs[4][kDecodeMaxGroup][64];
-  __shared__ int use_head[kDecodeMaxGroup];
+  __shared__ float qs[GM][kHeadDim];
+  __shared__ float ps[GM][kDecodeChunk];
+  __shared__ float red[4][GM][2];
+  __shared__ float2 accs[4][GM][64];
+  __shared__ int use_head[GM];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int x = blockIdx.x;
   const int s = blockIdx.y / p.Hkv, g = blockIdx.y % p.Hkv;
+  int x = blockIdx.x;  // chunk id: block * nsub + piece
+  if (!a.full) {       // MoBA: the grid runs over the group's selected blocks only
+    const int j = a.blocks[(int64_t)blockIdx.y * a.nunion + blockIdx.x / a.nsub];
+    if (j < 0) return;
+    x = j * a.nsub + blockIdx.x % a.nsub;
+  }
   const SeqInfo sq = a.seqs[s];
   const int G = p.G;
   int64_t u0, u1;
@@ -156,24 +202,27 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   // scores: lane = key u0 + 64 * wave + lane
   const int64_t u = u0 + 64 * wave + lane;
   const bool kv_ok = u < u1;
-  float kr[kHeadDim];
+  uint32_t kw[kHeadDim / 2];  // the key row, packed bf16 pairs
   {
     const int64_t t = sq.tok_start + (kv_ok ? u : u0);
     const uint4* kp = reinterpret_cast<const uint4*>(a.k + t * a.k_st + (int64_t)g * a.k_sh);
 #pragma unroll
     for (int c8 = 0; c8 < kHeadDim / 8; c8++) {
       const uint4 w = kp[c8];
-      kr[8 * c8 + 0] = bf16_lo(w.x); kr[8 * c8 + 1] = bf16_hi(w.x);
-      kr[8 * c8 + 2] = bf16_lo(w.y); kr[8 * c8 + 3] = bf16_hi(w.y);
-      kr[8 * c8 + 4] = bf16_lo(w.z); kr[8 * c8 + 5] = bf16_hi(w.z);
-      kr[8 * c8 + 6] = bf16_lo(w.w); kr[8 * c8 + 7] = bf16_hi(w.w);
+      kw[4 * c8] = w.x;
+      kw[4 * c8 + 1] = w.y;
+      kw[4 * c8 + 2] = w.z;
+      kw[4 * c8 + 3] = w.w;
     }
   }
   const float c2 = a.scale_log2;
   for (int hl = 0; hl < G; hl++) {
     float acc = 0.0f;
 #pragma unroll
-    for (int d = 0; d < kHeadDim; d++) acc = fmaf(qs[hl][d], kr[d], acc);
+    for (int d2 = 0; d2 < kHeadDim / 2; d2++) {
+      acc = fmaf(qs[hl][2 * d2], bf16_lo(kw[d2]), acc);
+      acc = fmaf(qs[hl][2 * d2 + 1], bf16_hi(kw[d2]), acc);
+    }
     const float sv = kv_ok ? acc * c2 : -INFINITY;
     float m = sv;
 #pragma unroll
@@ -194,9 +243,9 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   }
   __syncthreads();
   // P V: wave w sums keys 64w .. 64w+63 for dims 2*lane, 2*lane+1
-  float2 acc[kDecodeMaxGroup];
+  float2 acc[GM];
 #pragma unroll
-  for (int hl = 0; hl < kDecodeMaxGroup; hl++) acc[hl] = make_float2(0.0f, 0.0f);
+  for (int hl = 0; hl < GM; hl++) acc[hl] = make_float2(0.0f, 0.0f);
   const int kend = (int)min((int64_t)64, u1 - (u0 + 64 * wave));
   const uint32_t* vrow = reinterpret_cast<const uint32_t*>(
       a.v + (sq.tok_start + u0 + 64 * wave) * a.v_st + (int64_t)g * a.v_sh) + lane;
@@ -209,7 +258,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
     for (int e = 0; e < 8; e++) {
       const float v0 = bf16_lo(wv[e]), v1 = bf16_hi(wv[e]);
 #pragma unroll
-      for (int hl = 0; hl < kDecodeMaxGroup; hl++) {
+      for (int hl = 0; hl < GM; hl++) {
         if (hl < G) {
           const float pw = k0 + e < kend ? ps[hl][64 * wave + k0 + e] : 0.0f;
           acc[hl].x = fmaf(pw, v0, acc[hl].x);
@@ -219,7 +268,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
     }
   }
 #pragma unroll
-  for (int hl = 0; hl < kDecodeMaxGroup; hl++)
+  for (int hl = 0; hl < GM; hl++)
     if (hl < G) accs[wave][hl][lane] = acc[hl];
   __syncthreads();
   // normalised partial and lse per attending head; wave w handles heads w, w+4, ...
@@ -316,10 +365,21 @@ hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t
   return hipGetLastError();
 }
 
+hipError_t launch_decode_plan(const DecodeArgs& a, const Problem& p, hipStream_t st) {
+  if (p.S <= 0 || a.full) return hipSuccess;
+  decode_plan_kernel<<<(unsigned)(p.S * p.Hkv), 64, 0, st>>>(a, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream_t st) {
   if (p.S <= 0 || a.nchunk <= 0) return hipSuccess;
-  dim3 grid((unsigned)a.nchunk, (unsigned)(p.S * p.Hkv));
-  decode_attend_kernel<<<grid, 256, 0, st>>>(a, p);
+  const int nx = a.full ? a.nchunk : a.nunion * a.nsub;
+  dim3 grid((unsigned)nx, (unsigned)(p.S * p.Hkv));
+  if (p.G <= 1) decode_attend_kernel<1><<<grid, 256, 0, st>>>(a, p);
+  else if (p.G <= 2) decode_attend_kernel<2><<<grid, 256, 0, st>>>(a, p);
+  else if (p.G <= 4) decode_attend_kernel<4><<<grid, 256, 0, st>>>(a, p);
+  else if (p.G <= 8) decode_attend_kernel<8><<<grid, 256, 0, st>>>(a, p);
+  else decode_attend_kernel<kDecodeMaxGroup><<<grid, 256, 0, st>>>(a, p);
   return hipGetLastError();
 }
 

@@ -879,25 +879,29 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   p.topk = kk;
   const int nsub = full ? 1 : (int)ceil_div(B, kDecodeChunk);
   const int64_t nchunk = nbmax * nsub;
+  // blocks any head of a group can select: G (k - 1) history blocks plus the current one
+  const int nunion = full ? 0 : (int)std::min<int64_t>(nbmax, (int64_t)(Hq / Hkv) * (kk - 1) + 1);
   const bool own_kbar = !full && !kbar;
-  auto layout = [&](Bump* bp, float** kb, int32_t** sel, float** po, float** pls) {
+  auto layout = [&](Bump* bp, float** kb, int32_t** sel, int32_t** blk, float** po, float** pls) {
     *kb = bp->take<float>(own_kbar ? (int64_t)p.nblk_total * Hkv * kHeadDim : 0);
     *sel = bp->take<int32_t>(full ? 0 : S * Hq * kk);
+    *blk = bp->take<int32_t>(S * Hkv * nunion);
     *po = bp->take<float>(S * Hq * nchunk * kHeadDim);
     *pls = bp->take<float>(S * Hq * nchunk);
   };
   {
     Bump sz(nullptr);
     float *a0, *a2, *a3;
-    int32_t* a1;
-    layout(&sz, &a0, &a1, &a2, &a3);
+    int32_t *a1, *a4;
+    layout(&sz, &a0, &a1, &a4, &a2, &a3);
     if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
     if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
   }
   Bump bp(dc->ws);
   DecodeArgs a{};
   float* kb_ws;
-  layout(&bp, &kb_ws, &a.sel, &a.part_o, &a.part_lse);
+  layout(&bp, &kb_ws, &a.sel, &a.blocks, &a.part_o, &a.part_lse);
+  a.nunion = nunion;
   a.q = static_cast<const __hip_bfloat16*>(vq.data); a.q_ss = vq.st; a.q_sh = vq.sh;
   a.k = static_cast<const __hip_bfloat16*>(vk.data); a.k_st = vk.st; a.k_sh = vk.sh;
   a.v = static_cast<const __hip_bfloat16*>(vv.data); a.v_st = vv.st; a.v_sh = vv.sh;
@@ -915,8 +919,10 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
     MOBA_LAUNCH(launch_pool(vk.data, true, vk.st, vk.sh, d_seqs, p, kb_ws, stream));
   }
   if (!full) {
-    Phase ph("decode_gate", stream);
-    MOBA_LAUNCH(launch_decode_gate(a, p, stream));
+    { Phase ph("decode_gate", stream);
+      MOBA_LAUNCH(launch_decode_gate(a, p, stream)); }
+    Phase ph("decode_plan", stream);
+    MOBA_LAUNCH(launch_decode_plan(a, p, stream));
   }
   { Phase ph("decode_attend", stream);
     MOBA_LAUNCH(launch_decode_attend(a, p, stream)); }
