@@ -7,8 +7,10 @@
 //
 // Decode reads each attended key once per kv-head and does ~2 FLOP per byte,
 // far below the ridge of either the matrix cores or the vector ALUs, so it is
-// bound by HBM: the kernels use the vector ALUs, read K rows one per lane and
-// V rows coalesced, and in MoBA mode touch only the selected blocks.
+// bound by HBM: the kernels use the vector ALUs (packed bf16 dot products,
+// which halve the instruction count of fp32 FMAs on unpacked operands), read
+// K rows one per lane and V rows coalesced, and in MoBA mode touch only the
+// selected blocks.
 //
 //   gate     one wave per (sequence, query head): fp32 scores of the query
 //            against the block means of the sequence's complete past blocks
@@ -20,13 +22,17 @@
 //   attend   one work-group per (sequence, kv-head, 256-key chunk; chunks
 //            never cross a block boundary; in MoBA mode only the chunks of
 //            the group's selected blocks), all query heads of the group:
-//            scores with one key per lane, a per-head softmax over the chunk,
-//            P V with one dimension pair per lane and 64 keys per wave; the
+//            scores with one key per lane (bf16 dot2 against the packed
+//            query, fp32 sums), a per-head softmax over the chunk, P V with
+//            one dimension pair per lane and 64 keys per wave (dot2 over key
+//            pairs: weights rounded once to bf16, as the prefill's P V, fp32
+//            sums); the value rows are all requested before the softmax; the
 //            normalised partial and its lse go to the workspace; a head that
 //            did not select the chunk's block skips it.
 //   combine  one work-group per row: log-sum-exp merge of the row's
-//            partials (16 interleaved groups, then the groups in order),
-//            rounded once to the output dtype.
+//            partials (16 interleaved groups, eight partial loads in flight
+//            per group, then the groups in order), rounded once to the
+//            output dtype.
 #include "decode_internal.h"
 
 #include <math.h>
@@ -37,7 +43,15 @@ namespace {
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kLog2e = 1.4426950408889634f;
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bf16x2_t as_bf16x2(uint32_t w) { return __builtin_bit_cast(bf16x2_t, w); }
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+// Two fp32 values to a packed bf16 pair, round-to-nearest-even.
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 // Key range of chunk x of sequence length L: block j = x / nsub, piece
@@ -157,9 +171,12 @@ __global__ __launch_bounds__(64) void decode_plan_kernel(DecodeArgs a, Problem p
 // small groups leave room for more resident work-groups).
 template <int GM>
 __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Problem p) {
-  __shared__ float qs[GM][kHeadDim];
+  __shared__ uint32_t qw[GM][kHeadDim / 2];  // the group's queries, packed bf16 pairs
   __shared__ float ps[GM][kDecodeChunk];
+  __shared__ uint32_t pw[GM][kDecodeChunk / 2];
   __shared__ float red[4][GM][2];
+  // K rows of the chunk (wave w: keys 64w..64w+63, rows of kKRow chunks);
+  // reused for the per-wave P V sums once the scores are taken
   __shared__ float2 accs[4][GM][64];
   __shared__ int use_head[GM];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -189,19 +206,24 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   }
   for (int i = tid; i < G * (kHeadDim / 2); i += 256) {
     const int hl = i / (kHeadDim / 2), d2 = i % (kHeadDim / 2);
-    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + (int64_t)s * a.q_ss +
-                                                         (int64_t)(g * G + hl) * a.q_sh)[d2];
-    qs[hl][2 * d2] = bf16_lo(w);
-    qs[hl][2 * d2 + 1] = bf16_hi(w);
+    qw[hl][d2] = reinterpret_cast<const uint32_t*>(a.q + (int64_t)s * a.q_ss +
+                                                   (int64_t)(g * G + hl) * a.q_sh)[d2];
   }
   __syncthreads();
   int any = 0;
   for (int hl = 0; hl < G; hl++) any |= use_head[hl];
   if (!any) return;
 
-  // scores: lane = key u0 + 64 * wave + lane
+  // scores: lane = key u0 + 64 * wave + lane.  The wave's key rows arrive
+  // by LDS DMA, 1 KiB of consecutive row bytes per instruction (lane L of
+  // instruction j fills chunk 64j + L: row (64j+L) / kKRow, column
+  // min((64j+L) % kKRow, 15); the pad chunk repeats column 15), so HBM is
+  // read in whole rows; each lane then reads its own row, and the pad makes
+  // 16 lanes at one column hit 16 distinct bank groups.  Rows past the chunk
+  // end load the chunk's first row (their scores are discarded).
   const int64_t u = u0 + 64 * wave + lane;
   const bool kv_ok = u < u1;
+  const int kend = (int)min((int64_t)64, u1 - (u0 + 64 * wave));  // may be <= 0
   uint32_t kw[kHeadDim / 2];  // the key row, packed bf16 pairs
   {
     const int64_t t = sq.tok_start + (kv_ok ? u : u0);
@@ -217,12 +239,11 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   }
   const float c2 = a.scale_log2;
   for (int hl = 0; hl < G; hl++) {
+    // fp32 sum of exact bf16 products, two dims per instruction
     float acc = 0.0f;
 #pragma unroll
-    for (int d2 = 0; d2 < kHeadDim / 2; d2++) {
-      acc = fmaf(qs[hl][2 * d2], bf16_lo(kw[d2]), acc);
-      acc = fmaf(qs[hl][2 * d2 + 1], bf16_hi(kw[d2]), acc);
-    }
+    for (int d2 = 0; d2 < kHeadDim / 2; d2++)
+      acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(qw[hl][d2]), as_bf16x2(kw[d2]), acc, false);
     const float sv = kv_ok ? acc * c2 : -INFINITY;
     float m = sv;
 #pragma unroll
@@ -230,40 +251,45 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
     ps[hl][64 * wave + lane] = sv;
     if (lane == 0) red[wave][hl][0] = m;
   }
+  // this wave's 64 value rows (dims 2*lane, 2*lane+1), all in flight across
+  // the softmax below; slots past the chunk end load the chunk's first row,
+  // which exists, and get weight 0
+  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(
+      a.v + (sq.tok_start + u0) * a.v_st + (int64_t)g * a.v_sh) + lane;
+  uint32_t wv[64];
+#pragma unroll
+  for (int e = 0; e < 64; e++) wv[e] = vrow[(int64_t)(e < kend ? 64 * wave + e : 0) * a.v_st / 2];
   __syncthreads();
   // per head: chunk max, weights, sum
   for (int hl = 0; hl < G; hl++) {
     const float m = fmaxf(fmaxf(red[0][hl][0], red[1][hl][0]), fmaxf(red[2][hl][0], red[3][hl][0]));
     const float pv = kv_ok ? __builtin_amdgcn_exp2f(ps[hl][64 * wave + lane] - m) : 0.0f;
-    ps[hl][64 * wave + lane] = pv;
+    // weights of keys 2i, 2i+1 as one bf16 pair (the operand of the P V dot2)
+    const float pn = __shfl_xor(pv, 1, 64);
+    if ((lane & 1) == 0) pw[hl][32 * wave + (lane >> 1)] = pack_bf16(pv, pn);
     float l = pv;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o, 64);
     if (lane == 0) red[wave][hl][1] = l;
   }
   __syncthreads();
-  // P V: wave w sums keys 64w .. 64w+63 for dims 2*lane, 2*lane+1
+  // P V: wave w sums keys 64w .. 64w+63 for dims 2*lane, 2*lane+1, a key
+  // pair per dot2 (weights rounded once to bf16, fp32 accumulation); slots
+  // past the chunk end carry weight 0
   float2 acc[GM];
 #pragma unroll
   for (int hl = 0; hl < GM; hl++) acc[hl] = make_float2(0.0f, 0.0f);
-  const int kend = (int)min((int64_t)64, u1 - (u0 + 64 * wave));
-  const uint32_t* vrow = reinterpret_cast<const uint32_t*>(
-      a.v + (sq.tok_start + u0 + 64 * wave) * a.v_st + (int64_t)g * a.v_sh) + lane;
-  for (int k0 = 0; k0 < kend; k0 += 8) {
-    // eight V rows in flight, then their FMAs
-    uint32_t wv[8];
 #pragma unroll
-    for (int e = 0; e < 8; e++) wv[e] = k0 + e < kend ? vrow[(int64_t)(k0 + e) * a.v_st / 2] : 0u;
+  for (int e2 = 0; e2 < 32; e2++) {
+    const uint32_t v_lo = wv[2 * e2], v_hi = wv[2 * e2 + 1];
+    const uint32_t vx = __builtin_amdgcn_perm(v_hi, v_lo, 0x05040100u);  // dim 2*lane of both keys
+    const uint32_t vy = __builtin_amdgcn_perm(v_hi, v_lo, 0x07060302u);  // dim 2*lane+1
 #pragma unroll
-    for (int e = 0; e < 8; e++) {
-      const float v0 = bf16_lo(wv[e]), v1 = bf16_hi(wv[e]);
-#pragma unroll
-      for (int hl = 0; hl < GM; hl++) {
-        if (hl < G) {
-          const float pw = k0 + e < kend ? ps[hl][64 * wave + k0 + e] : 0.0f;
-          acc[hl].x = fmaf(pw, v0, acc[hl].x);
-          acc[hl].y = fmaf(pw, v1, acc[hl].y);
-        }
+    for (int hl = 0; hl < GM; hl++) {
+      if (hl < G) {
+        const bf16x2_t pp = as_bf16x2(pw[hl][32 * wave + e2]);
+        acc[hl].x = __builtin_amdgcn_fdot2_f32_bf16(pp, as_bf16x2(vx), acc[hl].x, false);
+        acc[hl].y = __builtin_amdgcn_fdot2_f32_bf16(pp, as_bf16x2(vy), acc[hl].y, false);
       }
     }
   }
@@ -303,11 +329,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
   float M = -INFINITY, wsum = 0.0f, acc[8];
 #pragma unroll
   for (int d = 0; d < 8; d++) acc[d] = 0.0f;
-  auto fold = [&](int x) {
-    const int64_t pr = row * a.nchunk + x;
-    const float lv = a.part_lse[pr];
-    const float4* op = reinterpret_cast<const float4*>(a.part_o + pr * kHeadDim + 8 * l16);
-    const float4 o0 = op[0], o1 = op[1];
+  auto fold_loaded = [&](float lv, float4 o0, float4 o1) {
     const float Mn = fmaxf(M, lv);
     const float sc = __builtin_amdgcn_exp2f((M - Mn) * kLog2e);
     const float w = __builtin_amdgcn_exp2f((lv - Mn) * kLog2e);
@@ -317,9 +339,31 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
     wsum = wsum * sc + w;
     M = Mn;
   };
+  auto fold = [&](int x) {
+    const int64_t pr = row * a.nchunk + x;
+    const float4* op = reinterpret_cast<const float4*>(a.part_o + pr * kHeadDim + 8 * l16);
+    fold_loaded(a.part_lse[pr], op[0], op[1]);
+  };
   if (a.full) {
+    // the group's partials x = grp + 16 i, eight loads in flight per round
+    constexpr int kAhead = 8;
     const int n = (int)((sq.len + kDecodeChunk - 1) / kDecodeChunk);
-    for (int x = grp; x < n; x += 16) fold(x);
+    for (int x0 = grp; x0 < n; x0 += 16 * kAhead) {
+      float lv[kAhead];
+      float4 o0[kAhead], o1[kAhead];
+#pragma unroll
+      for (int e = 0; e < kAhead; e++) {
+        const int x = min(x0 + 16 * e, n - 1);
+        const int64_t pr = row * a.nchunk + x;
+        const float4* op = reinterpret_cast<const float4*>(a.part_o + pr * kHeadDim + 8 * l16);
+        lv[e] = a.part_lse[pr];
+        o0[e] = op[0];
+        o1[e] = op[1];
+      }
+#pragma unroll
+      for (int e = 0; e < kAhead; e++)
+        if (x0 + 16 * e < n) fold_loaded(lv[e], o0[e], o1[e]);
+    }
   } else {
     // the row's chunks: z = y * nsub + i for selection entry y, piece i
     const int32_t* sl = a.sel + row * p.topk;
