@@ -37,6 +37,8 @@ CASES = [
     ((333, 1), 2, 1, 7, 6),
     ((1500,), 4, 1, 512, 3),
     ((1300, 900), 8, 1, 300, 3),
+    ((40, 17), 2, 1, 1, 4),      # one-key blocks
+    ((600, 45), 16, 1, 64, 3),   # 16 query heads per kv-head
 ]
 
 

@@ -42,6 +42,8 @@ CASES = [
     ((5000,), 4, 1, 1000, 2),
     ((333, 1), 2, 1, 7, 6),
     ((4097, 4096, 300), 8, 2, 512, 4),
+    ((600, 45), 16, 1, 64, 3),   # the largest group decode takes
+    ((50, 2), 2, 1, 1, 5),       # one-key blocks
 ]
 
 
