@@ -237,3 +237,30 @@ def moba_backward_parity(q, k, v, cu, B, topk, dout, exact_sel=False):
                                                              ref[worst], c[worst]))
         assert mean_rel <= BWD_MEAN_REL, "%s mean |err| %.3e of mean |ref|" % (name, mean_rel)
     return res
+
+
+def decode_ambiguous_rows(q_rows, rows, T, Hq, kn, cu, B, topk):
+    """Decode rows (given by their query vectors q_rows and row ids) whose
+    oracle top-(k-1) boundary is within the gate's rounding bound, where two
+    selections are correct.  Returns (oracle selection, ambiguous mask)."""
+    kbar, kabs = oracle.pool(kn, cu, B, with_abs=True)
+    osel = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows)
+    nmax = int(osel.max()) + 2
+    _, sc = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows, nmax=nmax)
+    qf = np.abs(_widen(np.asarray(q_rows).reshape(len(rows), -1)))
+    boff = block_offsets(cu, B)
+    G = Hq // kn.shape[1]
+    amb = np.zeros(len(rows), bool)
+    for i, r in enumerate(rows):
+        t, h = int(r) // Hq, int(r) % Hq
+        s = int(seq_of_tokens(cu, t))
+        c = (t - int(cu[s])) // B
+        nh = min(topk - 1, c)
+        if nh == 0 or nh >= c:
+            continue
+        cand = sc[i, :c]
+        order = sorted(range(c), key=lambda j: (-cand[j], j))
+        ja, jb = order[nh - 1], order[nh]
+        tau = TAU_SCALE * (qf[i] @ kabs[boff[s] + ja, h // G] + qf[i] @ kabs[boff[s] + jb, h // G])
+        amb[i] = cand[ja] - cand[jb] <= tau
+    return osel, amb

@@ -54,31 +54,6 @@ def decode_case(seqlens, hq, hkv, B, seed):
     return q, qd, k, v, cu
 
 
-def ambiguous_rows(q_rows, rows, T, Hq, kn, cu, B, topk):
-    """Rows whose top-(k-1) boundary is within the gate's rounding bound."""
-    kbar, kabs = oracle.pool(kn, cu, B, with_abs=True)
-    osel = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows)
-    nmax = int(osel.max()) + 2
-    _, sc = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows, nmax=nmax)
-    qf = np.abs(parity._widen(np.asarray(q_rows).reshape(len(rows), -1)))
-    boff = parity.block_offsets(cu, B)
-    G = Hq // kn.shape[1]
-    amb = np.zeros(len(rows), bool)
-    for i, r in enumerate(rows):
-        t, h = int(r) // Hq, int(r) % Hq
-        s = int(parity.seq_of_tokens(cu, t))
-        c = (t - int(cu[s])) // B
-        nh = min(topk - 1, c)
-        if nh == 0 or nh >= c:
-            continue
-        cand = sc[i, :c]
-        order = sorted(range(c), key=lambda j: (-cand[j], j))
-        ja, jb = order[nh - 1], order[nh]
-        tau = parity.TAU_SCALE * (qf[i] @ kabs[boff[s] + ja, h // G] + qf[i] @ kabs[boff[s] + jb, h // G])
-        amb[i] = cand[ja] - cand[jb] <= tau
-    return osel, amb
-
-
 @pytest.mark.parametrize("seqlens,hq,hkv,B,topk", CASES,
                          ids=["-".join(map(str, c[0])) + "_h%dx%d_B%d_k%d" % c[1:] for c in CASES])
 @pytest.mark.parametrize("mode", ["moba_kbar", "moba", "full"])
@@ -102,7 +77,7 @@ def test_decode(seqlens, hq, hkv, B, topk, mode):
         oout, olse = oracle.attend_rows(q_rows, T, hq, kn, vn, cun, Bf, sel, rows)
         keep = np.ones(len(rows), bool)
     else:
-        osel, amb = ambiguous_rows(q_rows, rows, T, hq, kn, cun, B, topk)
+        osel, amb = parity.decode_ambiguous_rows(q_rows, rows, T, hq, kn, cun, B, topk)
         oout, olse = oracle.attend_rows(q_rows, T, hq, kn, vn, cun, B, osel, rows)
         keep = ~amb
     mx, mean, lmx = parity.compare_outputs(gout[keep], glse[keep], oout[keep], olse[keep], "bf16",
