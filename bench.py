@@ -2,8 +2,8 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--dense-steps N] [--no-cpu]
     python bench.py --sweep fig2a|fig2b|gran [--sweep-steps K] [--sweep-lengths L1,L2,..]
-    python bench.py --backward [--steps K] [--warmup W] [--workload NAME]
-    python bench.py --decode [--steps K] [--workload NAME]
+    python bench.py --backward [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+    python bench.py --decode [--steps K] [--workload NAME] [--no-cpu]
 
 One step = one moba_forward call over the whole workload (pool, gate, route,
 history and current-block attention, merge), inputs resident in HBM.  The
@@ -18,6 +18,9 @@ dim 128, bf16, block 4096, top-12).  Prints one JSON line:
                  FLOPs per launch / its mean launch time from HIP events on
                  the library's stream, against the 2516.6 TFLOP/s bf16 peak
   cpu_baseline   the fp64 oracle on a fixed sample of rows, host cores
+--backward and --decode print one line each of their own, with their own
+oracle baseline (dQ of sampled rows; the whole decode call); --no-cpu skips
+every baseline.
 """
 from __future__ import annotations
 
@@ -148,6 +151,78 @@ def cpu_baseline(w, q, k, v, cu, n_rows, seed=7):
     }
 
 
+def cpu_baseline_backward(w, q, k, v, dout, cu, n_rows, seed=7):
+    """The oracle's backward on n_rows seeded rows of the workload: the
+    query-side gradient dQ (the S, dP and dQ products, 6*D FLOP per attended
+    pair, for the oracle's own selection of those rows).  The key-side
+    gradients would need fp64 accumulators over every key and are left out."""
+    from oracle import oracle
+
+    oracle.set_threads(len(os.sched_getaffinity(0)))
+    T, Hq, D = q.shape
+    rng = np.random.default_rng(seed)
+    rows = np.sort(rng.choice(T * Hq, size=n_rows, replace=False)).astype(np.int64)
+    rows_t = torch.as_tensor(rows, device=q.device)
+    q_r = inputs.to_oracle(q.reshape(T * Hq, D)[rows_t])
+    d_r = inputs.to_oracle(dout.reshape(T * Hq, D)[rows_t])
+    kn, vn = inputs.to_oracle(k), inputs.to_oracle(v)
+    cun = cu.numpy()
+    kbar = oracle.pool(kn, cun, w.block_size)
+    sel = oracle.select_rows(q_r, T, Hq, kbar, cun, w.block_size, w.topk, rows)
+    t0 = time.perf_counter()
+    oracle.attend_backward(q_r, kn, vn, d_r, cun, w.block_size, sel, rows=rows, shape=(T, Hq))
+    t1 = time.perf_counter()
+    cum = np.asarray(cun, np.int64)
+    t = rows // Hq
+    s = np.searchsorted(cum, t, side="right") - 1
+    tau = t - cum[s]
+    c = tau // w.block_size
+    keys = (tau - c * w.block_size + 1) + w.block_size * np.minimum(w.topk - 1, c)
+    flop = 6.0 * D * float(keys.sum())
+    return {
+        "value": flop / (t1 - t0) / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.threads(),
+        "kind": "oracle",
+        "sample": ("fp64 oracle dQ (S, dP, dQ: 6*D FLOP per attended pair) of %d seeded rows "
+                   "(t*Hq+h) of the %s workload for the oracle's selection: %.3g FLOP in %.1f s"
+                   % (n_rows, w.name, flop, t1 - t0)),
+        "cpu_model": _cpu_model(),
+    }
+
+
+def cpu_baseline_decode(w, qd, k, v, cu):
+    """The oracle on the decode workload itself (every sequence's new query,
+    every head): full attention over the cache, and MoBA (block means of the
+    cache, gate, attention).  Milliseconds per decode call."""
+    from oracle import oracle
+
+    oracle.set_threads(len(os.sched_getaffinity(0)))
+    S, Hq, D = qd.shape
+    T = int(cu[-1])
+    q_rows = inputs.to_oracle(qd.reshape(S * Hq, D))
+    kn, vn = inputs.to_oracle(k), inputs.to_oracle(v)
+    cun = cu.numpy()
+    rows = np.array([(int(cun[s + 1]) - 1) * Hq + h for s in range(S) for h in range(Hq)], np.int64)
+    t0 = time.perf_counter()
+    oracle.attend_rows(q_rows, T, Hq, kn, vn, cun, max(w.seqlens), np.zeros((len(rows), 1), np.int32),
+                       rows)
+    t1 = time.perf_counter()
+    kbar = oracle.pool(kn, cun, w.block_size)
+    sel = oracle.select_rows(q_rows, T, Hq, kbar, cun, w.block_size, w.topk, rows)
+    oracle.attend_rows(q_rows, T, Hq, kn, vn, cun, w.block_size, sel, rows)
+    t2 = time.perf_counter()
+    return {
+        "value": {"full": round((t1 - t0) * 1e3, 1), "moba": round((t2 - t1) * 1e3, 1)},
+        "unit": "ms per decode call",
+        "cores": oracle.threads(),
+        "kind": "oracle",
+        "sample": ("the whole decode call (%d rows) in fp64: full attention over the cache; MoBA "
+                   "with the block mean-pool of the cache included" % len(rows)),
+        "cpu_model": _cpu_model(),
+    }
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -254,6 +329,11 @@ def run_backward(args):
         "bwd_dq_cur": kernel_rate("bwd_dq_cur", 6.0 * w.d * w.hq * cur),
         "bwd_dkdv": kernel_rate("bwd_dkdv", 8.0 * w.d * pairs),
     }
+    cpu = None
+    if not args.no_cpu:
+        n_rows = max(1, args.cpu_rows * 2 // 3)
+        print("[bench] oracle baseline: dQ of %d rows" % n_rows, file=sys.stderr, flush=True)
+        cpu = cpu_baseline_backward(w, q, k, v, dout, cu, n_rows)
     print(json.dumps({
         "mode": "backward", "workload": w.name, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 3), "algorithmic_flop": flop, "tflops": round(tflops, 2),
@@ -261,6 +341,7 @@ def run_backward(args):
         "data": "synthetic",
         "phases_ms_per_step": {n: round(t / args.steps, 3) for n, (c, t) in phases.items()},
         "executed_tflops_per_kernel": rates,
+        "cpu_baseline": cpu,
     }), flush=True)
 
 
@@ -315,9 +396,14 @@ def run_decode(args):
                      "gb_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
                      "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "phases_ms": {k_: round(t / c, 4) for k_, (c, t) in phases.items()}}
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] oracle baseline: both decode modes", file=sys.stderr, flush=True)
+        cpu = cpu_baseline_decode(w, qd, k, v, cu)
     print(json.dumps({"mode": "decode", "workload": w.name, "queries": S * Hq, "dtype": "bf16",
                       "data": "synthetic", "full": res["full"], "moba": res["moba"],
-                      "speedup_moba_vs_full": round(res["full"]["ms"] / res["moba"]["ms"], 3)}),
+                      "speedup_moba_vs_full": round(res["full"]["ms"] / res["moba"]["ms"], 3),
+                      "cpu_baseline": cpu}),
           flush=True)
 
 
@@ -342,7 +428,7 @@ def main():
                     help="time moba_decode (full and MoBA) on the workload's cache instead")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
