@@ -386,6 +386,10 @@ constexpr int kChunk = 64;          // rows per chunk
 constexpr int kBufR = kChunk * 16;  // one row-major Q or dO chunk: 64 rows x 16 16-byte chunks
 constexpr int kDmaR = kBufR / 64;   // DMA instructions per chunk and tensor (16)
 constexpr int kSlots = 3;           // row tables in flight
+constexpr int kSpinLimit = 1 << 20; // polls of a hand-over flag before giving up
+// s_waitcnt operand that waits for LDS operations only (lgkmcnt 0, vmcnt and
+// expcnt at their maxima)
+constexpr int kWaitLds = 0xC07F;
 
 // Swizzled row-major chunk: the logical 16-byte chunk c of row r is stored
 // at r*16 + (c ^ swz(r)), swz(r) = 4*(r % 4) + (r / 4) % 4.  Both reads of
@@ -411,8 +415,8 @@ __device__ __forceinline__ s16x4 tr_read(const char* p) {
 }
 
 struct __align__(16) RowTab {
-  int t[kSlots][kChunk];
-  int h[kSlots][kChunk];
+  int64_t qoff[kSlots][kChunk];  // byte offset of the row's Q vector (t * q_st + h * q_sh)
+  int64_t doff[kSlots][kChunk];  // byte offset of the row's dO vector
   int kmax[kSlots][kChunk];   // last key the row may attend (causal rows), -1 for padding
   float lse2[kSlots][kChunk];
   float dlt[kSlots][kChunk];
@@ -452,7 +456,8 @@ __device__ __forceinline__ RowFetch row_fetch(const BwdArgs& a, const Problem& p
   return f;
 }
 
-__device__ __forceinline__ void row_store(RowTab& R, int slot, int lane, const RowFetch& f) {
+__device__ __forceinline__ void row_store(const BwdArgs& a, RowTab& R, int slot, int lane,
+                                          const RowFetch& f) {
   int t = f.t, h = f.h, km = -1;
   float l2 = INFINITY, dl = 0.0f;
   if (f.kind == 0) {
@@ -466,8 +471,8 @@ __device__ __forceinline__ void row_store(RowTab& R, int slot, int lane, const R
     dl = f.ld.y;
     km = t;
   }
-  R.t[slot][lane] = t;
-  R.h[slot][lane] = h;
+  R.qoff[slot][lane] = ((int64_t)t * a.q_st + (int64_t)h * a.q_sh) * 2;
+  R.doff[slot][lane] = ((int64_t)t * a.do_st + (int64_t)h * a.do_sh) * 2;
   R.kmax[slot][lane] = km;
   R.lse2[slot][lane] = l2;
   R.dlt[slot][lane] = dl;
@@ -587,11 +592,13 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   __shared__ u32x4 lds[4 * kBufR];  // Q chunk x2, dO chunk x2
   __shared__ RowTab R;
   __shared__ PExchange X;
+  __shared__ int pflag[kDkdvWaves / 2];  // subtiles whose P the pair's P-wave has written
   constexpr int kW = kDkdvWaves;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
-  const int pair = wave & 3, role = wave >> 2;  // role 0: P-wave, 1: D-wave
+  // role 0: P-wave, 1: D-wave (wave-uniform: scalar branches)
+  const int pair = wave & 3, role = __builtin_amdgcn_readfirstlane(wave >> 2);
 
   // work-group -> (kv-head, key tile): each XCD takes a contiguous run (the
   // key tiles of one bin read the same rows), early blocks (longest row
@@ -650,10 +657,9 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   auto dma_rows = [&](int slot, u32x4* qbuf, u32x4* dbuf) {
 #pragma unroll
     for (int x = 0; x < kDx; x++) {
-      const int64_t t = R.t[slot][drow[x]], h = R.h[slot][drow[x]];
-      __builtin_amdgcn_global_load_lds(qb + (t * a.q_st + h * a.q_sh) * 2 + dcol[x],
+      __builtin_amdgcn_global_load_lds(qb + R.qoff[slot][drow[x]] + dcol[x],
                                        qbuf + 64 * (wave + kW * x), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(db + (t * a.do_st + h * a.do_sh) * 2 + dcol[x],
+      __builtin_amdgcn_global_load_lds(db + R.doff[slot][drow[x]] + dcol[x],
                                        dbuf + 64 * (wave + kW * x), 16, 0, 0);
     }
   };
@@ -688,9 +694,10 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   const float c2 = a.scale_log2;
 
   // prologue: row tables of chunks 0 and 1, chunk 0 landed
+  if (tid < kDkdvWaves / 2) pflag[tid] = 0;
   if (wave == 0) {
-    row_store(R, 0, lane, row_fetch(a, p, L, 0, lane));
-    if (nch > 1) row_store(R, 1, lane, row_fetch(a, p, L, 1, lane));
+    row_store(a, R, 0, lane, row_fetch(a, p, L, 0, lane));
+    if (nch > 1) row_store(a, R, 1, lane, row_fetch(a, p, L, 1, lane));
   }
   __syncthreads();
   dma_rows(0, lds, lds + 2 * kBufR);
@@ -719,7 +726,26 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
           else p_weights<false>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
         }
       }
-      __syncthreads();
+      // P-wave -> D-wave hand-over of P(st) within the pair (the other pairs
+      // do not wait).  Everything exchanged is in LDS: the P-wave raises the
+      // pair's flag once its exchange writes have completed (lgkmcnt 0; the
+      // DMA still in flight is not waited for), the D-wave reads the exchange
+      // only after it has seen the flag.  The wait is bounded so that it
+      // always ends.
+      __builtin_amdgcn_sched_barrier(0);  // keep the two halves' schedules apart
+      const int seq = 2 * i + st + 1;
+      volatile __attribute__((address_space(3))) int* flag =
+          (volatile __attribute__((address_space(3))) int*)&pflag[pair];
+      if (live && role == 0) {
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(kWaitLds);
+        *flag = seq;
+      }
+      if (live && role == 1) {
+        int n = 0;
+        while (*flag < seq && ++n < kSpinLimit) __builtin_amdgcn_s_sleep(1);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      }
       if (live) {
         if (role == 1) ds_weights(sd, R, slot, st, hh, lane, X.p[st][pair], wb);
         // P-wave: dV^T += dO^T P; D-wave: dK^T += Q^T dS
@@ -727,7 +753,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
       }
     }
     dma_wait();
-    if (fetch) row_store(R, (i + 2) % kSlots, lane, nf);
+    if (fetch) row_store(a, R, (i + 2) % kSlots, lane, nf);
     __syncthreads();
   }
 
