@@ -190,6 +190,7 @@ constexpr int kDqStage = 2 * kBufK + kBufV;  // K, V (row-major), K^T (packed)
 template <int MODE>
 __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
   __shared__ u32x4 lds[2 * kDqStage];
+  __shared__ RowInfo rtab[MODE == kHist ? 1 : kRows];  // current-block rows (see below)
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
@@ -268,6 +269,9 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
     }
   }
   const float2 ld = a.ld[(int64_t)ri.h * p.T + ri.t];
+  // current-block tiles: the row's bookkeeping waits in LDS (registers are
+  // the loop's; measured: the history variant runs faster keeping it)
+  if (MODE != kHist && hh == 0) rtab[rloc] = ri;
 
   // ------------------------------------------------------------ key tiles
   const int64_t rb = kbeg - tok0, re = kend - tok0;
@@ -319,7 +323,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
     if (edge) {
       lo = (int)max((int64_t)0, kbeg - u0) - 4 * hh;
       const int64_t lim = min((int64_t)kKeyTile, kend - u0);
-      hi = (int)(MODE == kHist ? lim : min(lim, ri.t + 1 - u0)) - 4 * hh;
+      hi = (int)(MODE == kHist ? lim : min(lim, rtab[rloc].t + 1 - u0)) - 4 * hh;
     }
     bf16x8 db[4];
 #pragma unroll
@@ -334,10 +338,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
   }
 
   // -------------------------------------------------------------- epilogue
-  if (!ri.valid) return;
+  const RowInfo r = MODE == kHist ? ri : rtab[rloc];
+  if (!r.valid) return;
   const float scl = a.scale;
   if constexpr (MODE == kHist) {
-    float* dst = a.dq_part + ri.dst * kHeadDim;
+    float* dst = a.dq_part + r.dst * kHeadDim;
 #pragma unroll
     for (int dt = 0; dt < 4; dt++)
 #pragma unroll
@@ -352,8 +357,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
       for (int r = 0; r < 16; r++) acc[dt][r] *= scl;
     // history slots of this row, in slot order
     const int kh = p.topk - 1;
-    const int nh = (int)min((int64_t)kh, (ri.t - tok0) / p.B);
-    const float* part = a.dq_part + ri.dst * kh * kHeadDim;
+    const int nh = (int)min((int64_t)kh, (r.t - tok0) / p.B);
+    const float* part = a.dq_part + r.dst * kh * kHeadDim;
     for (int x = 0; x < nh; x++) {
 #pragma unroll
       for (int dt = 0; dt < 4; dt++)
@@ -368,7 +373,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
         }
     }
     __hip_bfloat16* drow =
-        static_cast<__hip_bfloat16*>(a.dq) + ri.t * a.dq_st + (int64_t)ri.h * a.dq_sh;
+        static_cast<__hip_bfloat16*>(a.dq) + r.t * a.dq_st + (int64_t)r.h * a.dq_sh;
 #pragma unroll
     for (int dt = 0; dt < 4; dt++)
 #pragma unroll
