@@ -188,3 +188,91 @@ def test_binding_refuses_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError):
         binding.load()
+
+
+# ------------------------------------------------- backward and decode checks
+class BwdCase(Case):
+    def __init__(self, **kw):
+        super().__init__(**kw)
+        T, hq, d = self.q.shape[0], self.q.shape[1], self.q.shape[2]
+        hkv = self.k.shape[1]
+        self.dout = desc([T, hq, d], self.q.dtype)
+        self.dq = desc([T, hq, d], self.q.dtype)
+        self.dk = desc([T, hkv, d], self.q.dtype)
+        self.dv = desc([T, hkv, d], self.q.dtype)
+
+    def backward(self, lib, B=16, topk=3, dense=False):
+        r = ctypes.byref
+        common = (r(self.q), r(self.k), r(self.v), r(self.cu))
+        tail = (r(self.out), r(self.lse), r(self.dout), r(self.dq), r(self.dk), r(self.dv), None)
+        if dense:
+            return binding.STATUS[lib.moba_dense_backward(*common, *tail)]
+        return binding.STATUS[lib.moba_backward(*common, B, topk, *tail)]
+
+
+def test_backward_validation(lib):
+    assert BwdCase(dtype=binding.MOBA_F32).backward(lib) == "MOBA_ERR_DTYPE"  # bf16 only
+    c = BwdCase()
+    c.dk.data = None
+    assert c.backward(lib) == "MOBA_ERR_NULL"
+    c = BwdCase()
+    c.dv.shape[1] = 4  # kv-head count of the inputs is 2
+    assert c.backward(lib) == "MOBA_ERR_SHAPE"
+    c = BwdCase()
+    c.dq.shape[0] = 255
+    assert c.backward(lib, dense=True) == "MOBA_ERR_SHAPE"
+    c = BwdCase()
+    c.dout.stride[0] = 4 * 128 + 4
+    assert c.backward(lib) == "MOBA_ERR_LAYOUT"
+    assert BwdCase().backward(lib, B=0) == "MOBA_ERR_BLOCK_SIZE"
+    assert BwdCase().backward(lib, topk=0) == "MOBA_ERR_TOPK"
+    assert BwdCase(cu=(0, 300, 256)).backward(lib) == "MOBA_ERR_SEQLENS"
+    assert BwdCase(T=5000, cu=(0, 5000)).backward(lib, B=1, topk=2) == "MOBA_ERR_UNSUPPORTED"
+    c = BwdCase(T=0, cu=(0, 0))
+    for t in (c.q, c.k, c.v, c.out, c.lse, c.dout, c.dq, c.dk, c.dv):
+        t.data = None
+    assert c.backward(lib) == "MOBA_OK"
+    assert c.backward(lib, dense=True) == "MOBA_OK"
+
+
+class DecCase:
+    def __init__(self, S=2, T=300, hq=4, hkv=2, cu=(0, 100, 300), dtype=binding.MOBA_BF16):
+        self.cu_arr = np.array(cu, dtype=np.int32)
+        self.q = desc([S, hq, 128], dtype)
+        self.k = desc([T, hkv, 128], dtype)
+        self.v = desc([T, hkv, 128], dtype)
+        self.out = desc([S, hq, 128], dtype)
+        self.lse = desc([hq, S], binding.MOBA_F32)
+        self.cu = desc([len(cu)], binding.MOBA_I32, data=self.cu_arr.ctypes.data)
+        self.kbar = None
+
+    def decode(self, lib, B=16, topk=3):
+        r = ctypes.byref
+        kb = r(self.kbar) if self.kbar is not None else None
+        return binding.STATUS[lib.moba_decode(r(self.q), r(self.k), r(self.v), r(self.cu), kb, B,
+                                              topk, r(self.out), r(self.lse), None)]
+
+
+def test_decode_validation(lib):
+    assert DecCase(dtype=binding.MOBA_F32).decode(lib) == "MOBA_ERR_DTYPE"
+    c = DecCase()
+    c.v.data = None
+    assert c.decode(lib) == "MOBA_ERR_NULL"
+    assert DecCase(hq=32, hkv=1).decode(lib) == "MOBA_ERR_UNSUPPORTED"  # group > 16
+    assert DecCase(hq=6, hkv=4).decode(lib) == "MOBA_ERR_SHAPE"
+    assert DecCase(S=3).decode(lib) == "MOBA_ERR_SHAPE"  # cu_seqlens has S + 1 entries
+    assert DecCase().decode(lib, topk=-1) == "MOBA_ERR_TOPK"
+    assert DecCase().decode(lib, B=0) == "MOBA_ERR_BLOCK_SIZE"
+    assert DecCase(cu=(0, 0, 300)).decode(lib) == "MOBA_ERR_SEQLENS"  # empty cache
+    assert DecCase(cu=(0, 200, 100)).decode(lib) == "MOBA_ERR_SEQLENS"
+    c = DecCase()
+    c.lse.stride[0] = 5
+    assert c.decode(lib) == "MOBA_ERR_LAYOUT"
+    c = DecCase()
+    c.kbar = desc([10, 2, 128], binding.MOBA_F32)  # ceil(100/16) + ceil(200/16) = 20 blocks
+    assert c.decode(lib) == "MOBA_ERR_SHAPE"
+    c = DecCase(S=0, T=0, cu=(0,))
+    for t in (c.q, c.k, c.v, c.out, c.lse):
+        t.data = None
+    assert c.decode(lib) == "MOBA_OK"  # no sequences: nothing to do
+    assert DecCase(S=0, cu=(0,)).decode(lib) == "MOBA_ERR_SEQLENS"  # cache rows no sequence owns
