@@ -12,9 +12,9 @@
 // K rows one per lane and V rows coalesced, and in MoBA mode touch only the
 // selected blocks.
 //
-//   gate     one wave per (sequence, query head): fp32 scores of the query
-//            against the block means of the sequence's complete past blocks
-//            (sequential fp32 sums, one block per lane), then top-(k-1) by
+//   gate     one work-group per (sequence, query head): fp32 scores of the
+//            query against the block means of the sequence's complete past
+//            blocks (sequential fp32 sums, one block per thread), then top-(k-1) by
 //            k-1 rounds of a wave-wide argmax (ties: lower block index), and
 //            the selection written ascending with the current block last.
 //   plan     (MoBA) one wave per (sequence, kv-head): the union of the
@@ -64,39 +64,44 @@ __device__ __forceinline__ void chunk_range(int x, int nsub, int B, int64_t L, i
 }
 
 // ================================================================== gate
+// One work-group per (sequence, query head): its four waves score the
+// candidate blocks (one block per thread, all of a block's loads in flight),
+// then wave 0 selects.
 __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem p) {
-  __shared__ float qs[4][kHeadDim];
-  __shared__ float sc[4][kMaxBlocksPerSeq];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + wave;  // s * Hq + h
-  const bool active = row < (int64_t)p.S * p.Hq;
-  const int s = active ? (int)(row / p.Hq) : 0;
-  const int h = active ? (int)(row % p.Hq) : 0;
+  __shared__ float qs[kHeadDim];
+  __shared__ float sc[kMaxBlocksPerSeq];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int64_t row = blockIdx.x;  // s * Hq + h
+  const int s = (int)(row / p.Hq), h = (int)(row % p.Hq);
   const int g = h / p.G;
   const SeqInfo sq = a.seqs[s];
-  if (active) {
+  if (tid < kHeadDim / 2) {
     const __hip_bfloat16* qr = a.q + (int64_t)s * a.q_ss + (int64_t)h * a.q_sh;
-    const uint32_t w = reinterpret_cast<const uint32_t*>(qr)[lane];
-    qs[wave][2 * lane] = bf16_lo(w);
-    qs[wave][2 * lane + 1] = bf16_hi(w);
+    const uint32_t w = reinterpret_cast<const uint32_t*>(qr)[tid];
+    qs[2 * tid] = bf16_lo(w);
+    qs[2 * tid + 1] = bf16_hi(w);
   }
   __syncthreads();
-  if (!active) return;
   const int c = (int)((sq.len - 1) / p.B);  // current block; candidates j < c
-  // scores, one block per lane, dims in order
-  for (int j = lane; j < c; j += 64) {
-    const float* kb = a.kbar + ((int64_t)(sq.blk_off + j) * p.Hkv + g) * kHeadDim;
+  // scores, one block per thread, dims in order
+  for (int j = tid; j < c; j += 256) {
+    const float4* kb = reinterpret_cast<const float4*>(
+        a.kbar + ((int64_t)(sq.blk_off + j) * p.Hkv + g) * kHeadDim);
+    float4 kv[kHeadDim / 4];
+#pragma unroll
+    for (int d4 = 0; d4 < kHeadDim / 4; d4++) kv[d4] = kb[d4];
     float acc = 0.0f;
-#pragma unroll 8
-    for (int d = 0; d < kHeadDim; d += 4) {
-      const float4 kv = *reinterpret_cast<const float4*>(kb + d);
-      acc = fmaf(qs[wave][d], kv.x, acc);
-      acc = fmaf(qs[wave][d + 1], kv.y, acc);
-      acc = fmaf(qs[wave][d + 2], kv.z, acc);
-      acc = fmaf(qs[wave][d + 3], kv.w, acc);
+#pragma unroll
+    for (int d4 = 0; d4 < kHeadDim / 4; d4++) {
+      acc = fmaf(qs[4 * d4], kv[d4].x, acc);
+      acc = fmaf(qs[4 * d4 + 1], kv[d4].y, acc);
+      acc = fmaf(qs[4 * d4 + 2], kv[d4].z, acc);
+      acc = fmaf(qs[4 * d4 + 3], kv[d4].w, acc);
     }
-    sc[wave][j] = acc;
+    sc[j] = acc;
   }
+  __syncthreads();
+  if (tid >= 64) return;
   // top-(k-1): rounds of a wave-wide argmax over (score desc, index asc);
   // lane L owns candidates L, L + 64, ... and marks its taken ones in a mask
   const int kh = p.topk - 1;
@@ -107,7 +112,7 @@ __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem 
     int bj = INT32_MAX;
     for (int j = lane, x = 0; j < c; j += 64, x++) {
       if ((taken >> x) & 1) continue;
-      const float v = sc[wave][j];
+      const float v = sc[j];
       if (v > best || (v == best && j < bj)) { best = v; bj = j; }
     }
 #pragma unroll
@@ -405,7 +410,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
 hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t st) {
   const int64_t rows = (int64_t)p.S * p.Hq;
   if (rows <= 0 || a.full) return hipSuccess;
-  decode_gate_kernel<<<(unsigned)((rows + 3) / 4), 256, 0, st>>>(a, p);
+  decode_gate_kernel<<<(unsigned)rows, 256, 0, st>>>(a, p);
   return hipGetLastError();
 }
 
