@@ -31,7 +31,8 @@
 //          16 MFMAs each.  Each key has one owner, so dK and dV need
 //          neither atomics nor a merge.
 // P and dS enter the second products as bf16; every product accumulates in
-// fp32.
+// fp32.  The key side forms dS from the bf16 P its dV product uses (the value
+// it receives from the pair's P-wave); the query side from its fp32 P.
 #include "bwd_internal.h"
 #include "mfma_tile.h"
 
@@ -483,11 +484,12 @@ __device__ __forceinline__ void row_store(const BwdArgs& a, RowTab& R, int slot,
   R.dlt[slot][lane] = dl;
 }
 
-// P of one 32-row subtile as written by a P-wave for its D-wave:
-// [parity][pair][r4][lane] float4 (lane order, so every access is one
-// contiguous 1 KiB per wave).
+// P of one 32-row subtile as written by a P-wave for its D-wave, the bf16
+// operands the P-wave feeds its own dV product (so dS = P (dP - Delta) uses
+// the same rounded P as dV): [parity][pair][half][lane] 16 bytes (lane
+// order, so every access is one contiguous 1 KiB per wave).
 struct __align__(16) PExchange {
-  float4 p[2][kDkdvWaves / 2][4][64];
+  uint4 p[2][kDkdvWaves / 2][2][64];
 };
 
 // S = Q K^T (P-wave) or dP = dO V^T (D-wave) of subtile st: 8 k-steps with
@@ -546,7 +548,7 @@ __device__ __forceinline__ void g_product(f32x16 (&acc)[4], const char* buf, int
 template <bool EDGE>
 __device__ __forceinline__ void p_weights(const f32x16& sv, const RowTab& R, int slot, int st,
                                           int hh, int lane, int key, int k1, float c2,
-                                          float4 (&xo)[4][64], bf16x8 (&pb)[2]) {
+                                          uint4 (&xo)[2][64], bf16x8 (&pb)[2]) {
   uint32_t w[8];
 #pragma unroll
   for (int r4 = 0; r4 < 4; r4++) {
@@ -562,24 +564,29 @@ __device__ __forceinline__ void p_weights(const f32x16& sv, const RowTab& R, int
 #pragma unroll
       for (int c = 0; c < 4; c++) pr[c] = (key <= kv[c] && key < k1) ? pr[c] : 0.0f;
     }
-    xo[r4][lane] = make_float4(pr[0], pr[1], pr[2], pr[3]);
     w[2 * r4] = pack_bf16(pr[0], pr[1]);
     w[2 * r4 + 1] = pack_bf16(pr[2], pr[3]);
   }
   pb[0] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
   pb[1] = as_bf16x8(u32x4{w[4], w[5], w[6], w[7]});
+  xo[0][lane] = make_uint4(w[0], w[1], w[2], w[3]);
+  xo[1][lane] = make_uint4(w[4], w[5], w[6], w[7]);
 }
 
 // D-wave: dS = P (dP - Delta) of subtile st as bf16 operands sb[s2].
 __device__ __forceinline__ void ds_weights(const f32x16& dpv, const RowTab& R, int slot, int st,
-                                           int hh, int lane, const float4 (&xi)[4][64],
+                                           int hh, int lane, const uint4 (&xi)[2][64],
                                            bf16x8 (&sb)[2]) {
   uint32_t w[8];
+  const uint4 x0 = xi[0][lane], x1 = xi[1][lane];
+  const uint32_t pw[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
   for (int r4 = 0; r4 < 4; r4++) {
     const int row0 = 32 * st + 8 * r4 + 4 * hh;
     const float4 dl = *reinterpret_cast<const float4*>(&R.dlt[slot][row0]);
-    const float4 pp = xi[r4][lane];
+    const float4 pp = make_float4(__uint_as_float(pw[2 * r4] << 16), __uint_as_float(pw[2 * r4] & 0xffff0000u),
+                                  __uint_as_float(pw[2 * r4 + 1] << 16),
+                                  __uint_as_float(pw[2 * r4 + 1] & 0xffff0000u));
     w[2 * r4] = pack_bf16(pp.x * (dpv[4 * r4] - dl.x), pp.y * (dpv[4 * r4 + 1] - dl.y));
     w[2 * r4 + 1] = pack_bf16(pp.z * (dpv[4 * r4 + 2] - dl.z), pp.w * (dpv[4 * r4 + 3] - dl.w));
   }
