@@ -27,9 +27,11 @@
 //   online softmax in fp32 on S^T: a lane holds one query and 32 of the
 //   tile's 64 keys, so the row max needs one exchange with the partner lane
 //   (lane ^ 32) and the row sum is kept per lane and combined at the end.
-//   The running max is only raised when a tile's max exceeds it by more than
-//   2^8 (exp2 units): the weights then stay below 2^8 and the rescale of the
-//   accumulators is skipped on most tiles.
+//   The weights are formed under the running max without taking the tile's
+//   max first; only when some lane's sum of them exceeds 2^8 (so a weight
+//   might) is the row max taken, the running max raised and the weights
+//   formed again.  Weights stay at most 2^8 and the max and the rescale are
+//   skipped on almost every tile.
 //   O^T (dims x queries) += V^T . P^T      4 dim tiles x 4 k-steps, P^T
 //   straight from the softmax registers (packed to bf16).
 // The accumulator layout of a 32x32 MFMA gives lane l the column l % 32 and
@@ -54,22 +56,52 @@ enum { kHist = 0, kCur = 1, kDense = 2 };
 
 constexpr int kRows = kTileRowsMfma;               // query rows per work-group (256)
 constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 70 KiB: two K and two V^T buffers
-constexpr float kRescaleSlack = 8.0f;              // exp2 units
+constexpr float kSumLimit = 256.0f;  // largest per-lane weight sum kept without a rescale
 constexpr float kLn2 = 0.69314718055994531f;
 
-// Masking and online softmax of S(i); the weights leave as bf16 P^T operands
-// pb[2*th + s2] (keys 32*th + 16*s2 .. +15).
+// Weights of S under the running max m as bf16 P^T operands pb[2*th + s2]
+// (keys 32*th + 16*s2 .. +15); returns this lane's sum of them.
+__device__ __forceinline__ float weights(const f32x16 (&s)[2], float m, bf16x8 (&pb)[4], float c2) {
+  float ts = 0.0f;
+#pragma unroll
+  for (int th = 0; th < 2; th++)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; s2++) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[th][8 * s2 + 2 * e], c2, -m));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[th][8 * s2 + 2 * e + 1], c2, -m));
+        w[e] = pack_bf16(p0, p1);
+        ts += p0 + p1;
+      }
+      pb[2 * th + s2] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
+    }
+  return ts;
+}
+
+// Masking and online softmax of S(i); the weights leave as bf16 P^T operands.
+// The weights are first formed under the running max; only if some lane's
+// sum of them exceeds 2^8 (so possibly a weight above 2^8), or on the first
+// tile, is the tile's row max taken, the accumulators rescaled and the
+// weights formed again.  Weights therefore never exceed 2^8.
 template <int MODE>
 __device__ __forceinline__ void softmax(f32x16 (&s)[2], float& m, float& l, f32x16 (&o)[4],
                                         bf16x8 (&pb)[4], bool edge, int lo, int hi, float c2) {
   if (edge) mask_keys(s, lo, hi);
-  float mx = -INFINITY;
+  float ts = 0.0f;
+  bool redo = __builtin_amdgcn_ballot_w64(m == -INFINITY) != 0;
+  if (!redo) {
+    ts = weights(s, m, pb, c2);
+    redo = __builtin_amdgcn_ballot_w64(!(ts <= kSumLimit)) != 0;
+  }
+  if (redo) {
+    float mx = -INFINITY;
 #pragma unroll
-  for (int th = 0; th < 2; th++)
+    for (int th = 0; th < 2; th++)
 #pragma unroll
-    for (int r = 0; r < 16; r++) mx = fmaxf(mx, s[th][r]);
-  mx = fmaxf(mx, xor32(mx)) * c2;
-  if (__builtin_amdgcn_ballot_w64(mx > m + kRescaleSlack) != 0) {
+      for (int r = 0; r < 16; r++) mx = fmaxf(mx, s[th][r]);
+    mx = fmaxf(mx, xor32(mx)) * c2;
     const float m_new = fmaxf(m, mx);
     const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m - m_new);
     l *= alpha;
@@ -78,22 +110,9 @@ __device__ __forceinline__ void softmax(f32x16 (&s)[2], float& m, float& l, f32x
 #pragma unroll
       for (int r = 0; r < 16; r++) o[dt][r] *= alpha;
     m = m_new;
+    ts = weights(s, m == -INFINITY ? 0.0f : m, pb, c2);
   }
-  const float m_use = m == -INFINITY ? 0.0f : m;
-#pragma unroll
-  for (int th = 0; th < 2; th++)
-#pragma unroll
-    for (int s2 = 0; s2 < 2; s2++) {
-      uint32_t w[4];
-#pragma unroll
-      for (int e = 0; e < 4; e++) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[th][8 * s2 + 2 * e], c2, -m_use));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[th][8 * s2 + 2 * e + 1], c2, -m_use));
-        w[e] = pack_bf16(p0, p1);
-        l += p0 + p1;
-      }
-      pb[2 * th + s2] = as_bf16x8(u32x4{w[0], w[1], w[2], w[3]});
-    }
+  l += ts;
 }
 
 template <int MODE>
