@@ -296,8 +296,14 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
         }
       }
       __builtin_amdgcn_wave_barrier();
-      // this lane's row: 32 scores in block order
-      const int jend = min(kChunk, c - jc);
+      // this lane's row: 32 scores in block order.  Only scores above the
+      // list's last entry at the chunk start can enter it (the last entry
+      // only rises, and an equal later score never displaces an earlier
+      // one), so those are marked and inserted in block order; the other
+      // insertions would leave the list unchanged.
+      const int jend = min(kChunk, c - jc);  // blocks from c on never enter
+      uint32_t msk = 0;
+      const float thr = KM > 0 ? sc[KM > 0 ? KM - 1 : 0] : INFINITY;
 #pragma unroll
       for (int b4 = 0; b4 < kChunk / 4; b4++) {
         const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
@@ -306,8 +312,14 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
         for (int e = 0; e < 4; e++) {
           const int b = 4 * b4 + e;
           if (scores && b < jend && jc + b < nmax) scores[row * nmax + jc + b] = f[e];
-          // blocks at or after the row's current block never enter the list
-          if constexpr (KM > 0) insert_top<KM>(sc, id, b < jend ? f[e] : -INFINITY, jc + b);
+          if (b < jend && f[e] > thr) msk |= 1u << b;
+        }
+      }
+      if constexpr (KM > 0) {
+        while (msk) {
+          const int b = __builtin_ctz(msk);
+          msk &= msk - 1;
+          insert_top<KM>(sc, id, st[wave][lane][b], jc + b);
         }
       }
       __builtin_amdgcn_wave_barrier();
