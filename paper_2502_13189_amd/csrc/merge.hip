@@ -6,7 +6,8 @@
 // accumulated in fp32 in a fixed order (current block first, then history
 // slots ascending) and rounded once to bf16.
 //
-// 16 lanes per row, 8 dims (one 16-byte load) per lane and partial.  Partials
+// 16 lanes per row, 8 dims (one 16-byte load) per lane and partial; each
+// lane loads one slot's lse and the row's lanes share them.  Partials
 // are read in groups of kGroup, all loads of a group in flight at once, with
 // an online rescale between groups (one group covers top-k up to 13).
 #include "moba_internal.h"
@@ -75,12 +76,13 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a, Problem p) {
   for (int x0 = 0; x0 < nh; x0 += kGroup) {
     uint4 v[kGroup];
     float lv[kGroup];
+    // the group's lse values: lane l16 of the row loads slot x0 + l16, the
+    // others read it from that lane
+    const float lmine = x0 + l16 < nh ? lp[x0 + l16] : 0.0f;
 #pragma unroll
     for (int j = 0; j < kGroup; j++) {
-      if (x0 + j < nh) {
-        v[j] = op[(int64_t)(x0 + j) * (kHeadDim / 8)];
-        lv[j] = lp[x0 + j];
-      }
+      lv[j] = __shfl(lmine, j, kLanesPerRow);
+      if (x0 + j < nh) v[j] = op[(int64_t)(x0 + j) * (kHeadDim / 8)];
     }
     float Mg = M;
 #pragma unroll
