@@ -25,6 +25,8 @@
 namespace moba {
 namespace {
 
+constexpr size_t kRouteLdsMax = 160 * 1024;  // LDS of one gfx950 work-group
+
 struct ChunkPos {
   int s;
   int r;      // chunk index within the sequence
@@ -130,7 +132,8 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
                                                             Problem p,
                                                             const int32_t* __restrict__ hist,
                                                             const int64_t* __restrict__ bin_start,
-                                                            uint32_t* __restrict__ entries) {
+                                                            uint32_t* __restrict__ entries,
+                                                            bool use_pre) {
   extern __shared__ uint32_t lds[];
   const int g = blockIdx.y;
   const ChunkPos cp = chunk_pos(seqs, p, blockIdx.x);
@@ -138,6 +141,8 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
   const int nb = sq.nblk;
   uint32_t* mask = lds;            // [nb][8]
   uint32_t* running = lds + 8 * nb;  // [nb]
+  // with use_pre: [nb][8] bytes, the set bits of each block's words below a word
+  uint8_t* pre = reinterpret_cast<uint8_t*>(lds + 9 * nb);
   const int kh = p.topk - 1;
   const int tid = threadIdx.x, word = tid >> 5, bit = tid & 31;
   const int32_t* chunk_off = hist + (int64_t)g * p.hist_words + sq.hist_off + (int64_t)cp.r * nb;
@@ -160,13 +165,28 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
       for (int x = 0; x < nh; x++) atomicOr(&mask[sel[row * p.topk + x] * 8 + word], 1u << bit);
     }
     __syncthreads();
+    if (use_pre) {
+      for (int j = tid; j < nb; j += 256) {
+        uint32_t acc = 0;  // at most 7 * 32
+#pragma unroll
+        for (int w = 0; w < 8; w++) {
+          pre[j * 8 + w] = (uint8_t)acc;
+          acc += __popc(mask[j * 8 + w]);
+        }
+      }
+      __syncthreads();
+    }
     if (valid) {
       const uint64_t r = (uint64_t)g * TG + (uint64_t)(sq.tok_start + tl) * p.G + hl;
       for (int x = 0; x < nh; x++) {
         const int j = sel[row * p.topk + x];
         const uint32_t* m = mask + j * 8;
         uint32_t rank = running[j] + __popc(m[word] & ((1u << bit) - 1u));
-        for (int w = 0; w < word; w++) rank += __popc(m[w]);
+        if (use_pre) {
+          rank += pre[j * 8 + word];
+        } else {
+          for (int w = 0; w < word; w++) rank += __popc(m[w]);
+        }
         const int64_t pos = bstart[j] + chunk_off[j] + rank;
         entries[pos] = (uint32_t)(r * (uint64_t)kh + (uint64_t)x);
       }
@@ -204,14 +224,17 @@ hipError_t launch_route(const int32_t* sel, const SeqInfo* seqs, const Problem& 
   if (e != hipSuccess) return e;
   if (p.route_chunks > 0 && p.hist_entries > 0) {
     dim3 grid((unsigned)p.route_chunks, p.Hkv);
-    const size_t lds = (size_t)p.nblk_max * 9 * sizeof(uint32_t);
+    // the per-block prefix table when it fits beside the masks in LDS
+    const size_t base = (size_t)p.nblk_max * 9 * sizeof(uint32_t);
+    const bool use_pre = base + (size_t)p.nblk_max * 8 <= kRouteLdsMax;
+    const size_t lds = use_pre ? base + (size_t)p.nblk_max * 8 : base;
     if (lds > 65536) {
       e = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_scatter_kernel),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
     }
     route_scatter_kernel<<<grid, 256, lds, st>>>(
-        sel, seqs, p, rb.hist, rb.bin_start, rb.entries);
+        sel, seqs, p, rb.hist, rb.bin_start, rb.entries, use_pre);
     e = hipGetLastError();
   }
   return e;
