@@ -39,6 +39,7 @@ CASES = [
     ((1300, 900), 8, 1, 300, 3),
     ((40, 17), 2, 1, 1, 4),      # one-key blocks
     ((600, 45), 16, 1, 64, 3),   # 16 query heads per kv-head
+    ((200, 37), 64, 1, 32, 4),   # 64 query heads per kv-head
 ]
 
 

@@ -48,6 +48,7 @@ SMALL = [
     ((333, 1), 2, 1, 7, 6, torch.bfloat16),
     ((40, 17), 2, 1, 1, 4, torch.bfloat16),        # one-key blocks
     ((600,), 32, 1, 64, 3, torch.bfloat16),        # 32 query heads per kv-head
+    ((300, 45), 128, 1, 64, 3, torch.bfloat16),    # the largest group, 128 query heads per kv-head
     ((257, 3), 4, 2, 4096, 2, torch.bfloat16),     # block larger than every sequence
     ((4000,), 2, 1, 1, 3, torch.bfloat16),         # 4000 blocks: routing ranks without its LDS prefix table
     ((300,), 2, 2, 64, 3, torch.float32),
