@@ -28,8 +28,9 @@
 //          waves of a SIMD split the work for their 32 keys: per 32-row
 //          subtile the P-wave forms S = Q . K^T, P and dV^T += dO^T . P, the
 //          D-wave dP = dO . V^T, dS (with P from LDS) and dK^T += Q^T . dS:
-//          16 MFMAs each.  Each key has one owner, so dK and dV need
-//          neither atomics nor a merge.
+//          16 MFMAs each; the D-wave's dK product of a subtile runs one
+//          subtile late, beside the P-wave's exponentials of the next.  Each
+//          key has one owner, so dK and dV need neither atomics nor a merge.
 // P and dS enter the second products as bf16; every product accumulates in
 // fp32.  The key side forms dS from the bf16 P its dV product uses (the value
 // it receives from the pair's P-wave); the query side from its fp32 P.
@@ -601,7 +602,7 @@ __device__ __forceinline__ void ds_weights(const f32x16& dpv, const RowTab& R, i
 // Each wave so holds one 32-key operand set and one 32x128 accumulator, and
 // the two waves of a SIMD run matrix and vector work beside each other.
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
-  __shared__ u32x4 lds[4 * kBufR];  // Q chunk x2, dO chunk x2
+  __shared__ u32x4 lds[5 * kBufR];  // Q chunk x3 (dK runs a subtile late), dO chunk x2
   __shared__ RowTab R;
   __shared__ PExchange X;
   __shared__ int pflag[kDkdvWaves / 2];  // subtiles whose P the pair's P-wave has written
@@ -712,61 +713,78 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
     if (nch > 1) row_store(a, R, 1, lane, row_fetch(a, p, L, 1, lane));
   }
   __syncthreads();
-  dma_rows(0, lds, lds + 2 * kBufR);
+  dma_rows(0, lds, lds + 3 * kBufR);
   dma_wait();
   __syncthreads();
 
-  for (int i = 0; i < nch; i++) {
-    const int cur = i & 1;
-    RowFetch nf;
-    const bool fetch = wave == 0 && i + 2 < nch;
-    if (fetch) nf = row_fetch(a, p, L, i + 2, lane);
-    if (i + 1 < nch)
-      dma_rows((i + 1) % kSlots, lds + (cur ^ 1) * kBufR, lds + 2 * kBufR + (cur ^ 1) * kBufR);
-    const char* qr = reinterpret_cast<const char*>(lds + cur * kBufR);
-    const char* dr = reinterpret_cast<const char*>(lds + 2 * kBufR + cur * kBufR);
-    const int slot = i % kSlots;
-    const bool edge = (int64_t)(i + 1) * kChunk > L.nhist || !full;
+  // The two roles run separate copies of the chunk loop (same DMA, row
+  // tables and one barrier per chunk), so neither carries the other's
+  // registers.  D-wave: dK^T += Q^T dS of a subtile runs one subtile late,
+  // beside the P-wave's exponentials of the next one (Q chunks are
+  // triple-buffered for it).
+  volatile __attribute__((address_space(3))) int* flag =
+      (volatile __attribute__((address_space(3))) int*)&pflag[pair];
+  if (role == 0) {
+    for (int i = 0; i < nch; i++) {
+      const int cur = i & 1;
+      RowFetch nf;
+      const bool fetch = wave == 0 && i + 2 < nch;
+      if (fetch) nf = row_fetch(a, p, L, i + 2, lane);
+      if (i + 1 < nch)
+        dma_rows((i + 1) % kSlots, lds + ((i + 1) % 3) * kBufR, lds + (3 + (cur ^ 1)) * kBufR);
+      const char* qr = reinterpret_cast<const char*>(lds + (i % 3) * kBufR);
+      const char* dr = reinterpret_cast<const char*>(lds + (3 + cur) * kBufR);
+      const int slot = i % kSlots;
+      const bool edge = (int64_t)(i + 1) * kChunk > L.nhist || !full;
 #pragma unroll 1
-    for (int st = 0; st < 2; st++) {
-      f32x16 sd;  // P-wave: S, D-wave: dP
-      bf16x8 wb[2];
-      if (live) {
-        sd = sd_product(role == 0 ? qr : dr, st, offa, kv);
-        if (role == 0) {
-          if (edge) p_weights<true>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
-          else p_weights<false>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
-        }
-      }
-      // P-wave -> D-wave hand-over of P(st) within the pair (the other pairs
-      // do not wait).  Everything exchanged is in LDS: the P-wave raises the
-      // pair's flag once its exchange writes have completed (lgkmcnt 0; the
-      // DMA still in flight is not waited for), the D-wave reads the exchange
-      // only after it has seen the flag.  The wait is bounded so that it
-      // always ends.
-      __builtin_amdgcn_sched_barrier(0);  // keep the two halves' schedules apart
-      const int seq = 2 * i + st + 1;
-      volatile __attribute__((address_space(3))) int* flag =
-          (volatile __attribute__((address_space(3))) int*)&pflag[pair];
-      if (live && role == 0) {
+      for (int st = 0; st < 2; st++) {
+        if (!live) continue;
+        bf16x8 wb[2];
+        const f32x16 sd = sd_product(qr, st, offa, kv);  // S
+        if (edge) p_weights<true>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
+        else p_weights<false>(sd, R, slot, st, hh, lane, key, kt.k1, c2, X.p[st][pair], wb);
+        // hand P(st) to the pair's D-wave: raise the flag once the exchange
+        // writes have completed (lgkmcnt 0; the DMA in flight is not waited for)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_s_waitcnt(kWaitLds);
-        *flag = seq;
+        *flag = 2 * i + st + 1;
+        g_product(acc, dr, st, offt, wb);  // dV^T += dO^T P
       }
-      if (live && role == 1) {
+      dma_wait();
+      if (fetch) row_store(a, R, (i + 2) % kSlots, lane, nf);
+      __syncthreads();
+    }
+  } else {
+    bool have_prev = false;
+    const char* q_prev = nullptr;
+    int st_prev = 0;
+    bf16x8 wb_prev[2];
+    for (int i = 0; i < nch; i++) {
+      const int cur = i & 1;
+      if (i + 1 < nch)
+        dma_rows((i + 1) % kSlots, lds + ((i + 1) % 3) * kBufR, lds + (3 + (cur ^ 1)) * kBufR);
+      const char* qr = reinterpret_cast<const char*>(lds + (i % 3) * kBufR);
+      const char* dr = reinterpret_cast<const char*>(lds + (3 + cur) * kBufR);
+      const int slot = i % kSlots;
+#pragma unroll 1
+      for (int st = 0; st < 2; st++) {
+        if (!live) continue;
+        const f32x16 sd = sd_product(dr, st, offa, kv);  // dP
+        if (have_prev) g_product(acc, q_prev, st_prev, offt, wb_prev);  // dK^T += Q^T dS
+        // wait (bounded, so it always ends) for the P-wave's P(st)
+        const int seq = 2 * i + st + 1;
         int n = 0;
         while (*flag < seq && ++n < kSpinLimit) __builtin_amdgcn_s_sleep(1);
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        ds_weights(sd, R, slot, st, hh, lane, X.p[st][pair], wb_prev);
+        have_prev = true;
+        q_prev = qr;
+        st_prev = st;
       }
-      if (live) {
-        if (role == 1) ds_weights(sd, R, slot, st, hh, lane, X.p[st][pair], wb);
-        // P-wave: dV^T += dO^T P; D-wave: dK^T += Q^T dS
-        g_product(acc, role == 0 ? dr : qr, st, offt, wb);
-      }
+      dma_wait();
+      __syncthreads();
     }
-    dma_wait();
-    if (fetch) row_store(a, R, (i + 2) % kSlots, lane, nf);
-    __syncthreads();
+    if (have_prev) g_product(acc, q_prev, st_prev, offt, wb_prev);
   }
 
   // -------------------------------------------------------------- epilogue
