@@ -598,7 +598,8 @@ __device__ __forceinline__ void ds_weights(const f32x16& dpv, const RowTab& R, i
 // Work-group: 4 pairs of waves, pair q on SIMD q (waves q and q + 4), each
 // pair owning 32 keys.  The P-wave holds K, computes S and P and accumulates
 // dV^T; the D-wave holds V, computes dP and dS (with the P-wave's P, passed
-// through LDS behind one barrier per 32-row subtile) and accumulates dK^T.
+// through LDS with a per-pair flag for each 32-row subtile) and accumulates
+// dK^T one subtile late.
 // Each wave so holds one 32-key operand set and one 32x128 accumulator, and
 // the two waves of a SIMD run matrix and vector work beside each other.
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
