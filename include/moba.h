@@ -39,6 +39,11 @@
  * arguments return a status code and touch nothing.  Kernel launch failures
  * return MOBA_ERR_HIP.  No function throws.
  *
+ * Per-shape tables (sequence offsets, tile lists) are built on the host for
+ * each new (cu_seqlens, heads, block size, top-k) and copied on `stream`; the
+ * last few are kept per device.  Their buffers grow in powers of two, and
+ * growing one synchronizes the device.
+ *
  * The library keeps one cached device workspace per device, grown on demand
  * (growing it synchronizes the device) and capped by the environment variable
  * MOBA_WORKSPACE_LIMIT_BYTES (default 64 GiB).  When one call needs more, the
@@ -173,8 +178,9 @@ moba_status moba_dense_backward(const moba_tensor* q, const moba_tensor* k, cons
  * out [S, Hq, D] bf16 and lse [Hq, S] f32 (natural log) as for moba_forward.
  * Hq / Hkv must not exceed 16.  Gate scores are fp32 sums over the dims in
  * order; near-ties may be broken differently from moba_select's matrix-core
- * gate.  Each call rebuilds the per-shape tables when cu_seqlens changes
- * (one device synchronization).
+ * gate.  A call whose cu_seqlens differs from those of recent calls (every
+ * step of a growing cache) builds new per-shape tables on the host and copies
+ * them on `stream`; it does not synchronize the device.
  */
 moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
                         const moba_tensor* v_cache, const moba_tensor* cu_seqlens,

@@ -311,13 +311,29 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
 }
 
 // ------------------------------------------------------------- device cache
+// A plan with its tables on the device.  The tables are built in pinned host
+// memory and copied on the caller's stream, so a new plan needs no device
+// synchronization: the copy runs after every earlier call's kernels (stream
+// order, and calls on different streams never overlap), and `uploaded` tells
+// when the staging buffer may be written again.
+struct PlanSlot {
+  std::vector<int64_t> key;  // empty: unused
+  Plan plan;
+  void* tab = nullptr;       // device tables
+  size_t tab_bytes = 0;
+  void* stage = nullptr;     // pinned host copy of the tables
+  size_t stage_bytes = 0;
+  hipEvent_t uploaded = nullptr;
+  bool pending = false;      // `uploaded` recorded after the last copy
+  uint64_t last_use = 0;
+};
+constexpr int kPlanSlots = 4;  // e.g. forward/backward, decode, and the step-level calls
+
 struct DevCache {
   void* ws = nullptr;
   size_t ws_bytes = 0;
-  void* tab = nullptr;
-  size_t tab_bytes = 0;
-  std::vector<int64_t> tab_key;
-  Plan plan;  // plan whose tables are on the device
+  PlanSlot slots[kPlanSlots];
+  uint64_t clock = 0;
 };
 std::mutex g_mu;
 std::map<int, DevCache> g_dev;
@@ -347,56 +363,86 @@ moba_status ensure_workspace(DevCache* dc, size_t bytes) {
 }
 
 // Plan for (cu, heads, B, topk, mode), with its tables resident on the device.
-// Rebuilt only when the key changes; the rebuild synchronizes the device
-// because kernels of earlier calls may still read the old tables.
-moba_status get_plan(DevCache* dc, const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk,
-                     TileMode mode, int tile_rows, const Plan** out, const SeqInfo** d_seqs,
-                     const CausalTile** d_tiles, const KeyTile** d_ktiles = nullptr) {
+// Kept in a small least-recently-used set of slots, so calls that alternate
+// between a few shapes rebuild nothing.  A rebuild copies the tables on
+// `stream` without synchronizing the device (only growing a slot's buffers
+// does).
+moba_status get_plan(DevCache* dc, hipStream_t stream, const std::vector<int32_t>& cu, int Hq,
+                     int Hkv, int B, int topk, TileMode mode, int tile_rows, const Plan** out,
+                     const SeqInfo** d_seqs, const CausalTile** d_tiles,
+                     const KeyTile** d_ktiles = nullptr) {
   std::vector<int64_t> key = {Hq, Hkv, B, topk, mode, tile_rows, (int64_t)cu.size()};
   key.insert(key.end(), cu.begin(), cu.end());
-  if (key != dc->tab_key || !dc->tab) {
+  PlanSlot* sl = nullptr;
+  for (PlanSlot& x : dc->slots)
+    if (!x.key.empty() && x.key == key) sl = &x;
+  if (!sl) {
+    sl = &dc->slots[0];
+    for (PlanSlot& x : dc->slots)
+      if (x.key.empty() || x.last_use < sl->last_use) sl = &x;
+    // the slot's previous copy must have read its staging buffer
+    if (sl->pending && hipEventSynchronize(sl->uploaded) != hipSuccess) return MOBA_ERR_HIP;
+    sl->pending = false;
+    sl->key.clear();
     Plan pl;
     build_plan(cu, Hq, Hkv, B, topk, mode, tile_rows, &pl);
     const size_t sb = pl.seqs.size() * sizeof(SeqInfo);
     const size_t tb = pl.tiles.size() * sizeof(CausalTile);
-    const size_t need = ((sb + kAlign - 1) / kAlign) * kAlign + ((tb + kAlign - 1) / kAlign) * kAlign +
-                        pl.ktiles.size() * sizeof(KeyTile) + kAlign;
-    if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
-    if (need > dc->tab_bytes) {
-      if (dc->tab) (void)hipFree(dc->tab);
-      dc->tab = nullptr;
-      dc->tab_bytes = 0;
-      if (hipMalloc(&dc->tab, need) != hipSuccess) {
+    const size_t toff = ((sb + kAlign - 1) / kAlign) * kAlign;
+    const size_t koff = toff + ((tb + kAlign - 1) / kAlign) * kAlign;
+    const size_t need = koff + pl.ktiles.size() * sizeof(KeyTile);
+    // buffers grow to a power of two (at least 64 KiB), so a growing cache
+    // rarely reallocates
+    size_t cap = size_t(1) << 16;
+    while (cap < need) cap <<= 1;
+    if (need > sl->tab_bytes || !sl->tab) {
+      // kernels of earlier calls may still read the old tables
+      if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
+      if (sl->tab) (void)hipFree(sl->tab);
+      sl->tab = nullptr;
+      sl->tab_bytes = 0;
+      if (hipMalloc(&sl->tab, cap) != hipSuccess) {
         (void)hipGetLastError();
-        dc->tab_key.clear();
+        sl->tab = nullptr;
         return MOBA_ERR_NO_MEMORY;
       }
-      dc->tab_bytes = need;
+      sl->tab_bytes = cap;
     }
-    char* base = static_cast<char*>(dc->tab);
-    if (sb && hipMemcpy(base, pl.seqs.data(), sb, hipMemcpyHostToDevice) != hipSuccess)
+    if (need > sl->stage_bytes || !sl->stage) {
+      if (sl->stage) (void)hipHostFree(sl->stage);
+      sl->stage = nullptr;
+      sl->stage_bytes = 0;
+      if (hipHostMalloc(&sl->stage, cap, hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        sl->stage = nullptr;
+        return MOBA_ERR_NO_MEMORY;
+      }
+      sl->stage_bytes = cap;
+    }
+    if (!sl->uploaded && hipEventCreateWithFlags(&sl->uploaded, hipEventDisableTiming) != hipSuccess) {
+      sl->uploaded = nullptr;
       return MOBA_ERR_HIP;
-    const size_t toff = ((sb + kAlign - 1) / kAlign) * kAlign;
-    if (!pl.tiles.empty() &&
-        hipMemcpy(base + toff, pl.tiles.data(), pl.tiles.size() * sizeof(CausalTile),
-                  hipMemcpyHostToDevice) != hipSuccess)
+    }
+    char* st = static_cast<char*>(sl->stage);
+    if (sb) std::memcpy(st, pl.seqs.data(), sb);
+    if (tb) std::memcpy(st + toff, pl.tiles.data(), tb);
+    if (!pl.ktiles.empty()) std::memcpy(st + koff, pl.ktiles.data(), pl.ktiles.size() * sizeof(KeyTile));
+    if (need && (hipMemcpyAsync(sl->tab, sl->stage, need, hipMemcpyHostToDevice, stream) != hipSuccess ||
+                 hipEventRecord(sl->uploaded, stream) != hipSuccess))
       return MOBA_ERR_HIP;
-    const size_t koff = toff + ((tb + kAlign - 1) / kAlign) * kAlign;
-    if (!pl.ktiles.empty() &&
-        hipMemcpy(base + koff, pl.ktiles.data(), pl.ktiles.size() * sizeof(KeyTile),
-                  hipMemcpyHostToDevice) != hipSuccess)
-      return MOBA_ERR_HIP;
-    dc->plan = std::move(pl);
-    dc->tab_key = std::move(key);
+    sl->pending = need != 0;
+    sl->plan = std::move(pl);
+    sl->key = std::move(key);
   }
-  const size_t sb = dc->plan.seqs.size() * sizeof(SeqInfo);
-  const size_t tb = dc->plan.tiles.size() * sizeof(CausalTile);
+  sl->last_use = ++dc->clock;
+  const size_t sb = sl->plan.seqs.size() * sizeof(SeqInfo);
+  const size_t tb = sl->plan.tiles.size() * sizeof(CausalTile);
   const size_t toff = ((sb + kAlign - 1) / kAlign) * kAlign;
-  *out = &dc->plan;
-  *d_seqs = static_cast<const SeqInfo*>(dc->tab);
-  *d_tiles = reinterpret_cast<const CausalTile*>(static_cast<char*>(dc->tab) + toff);
+  *out = &sl->plan;
+  *d_seqs = static_cast<const SeqInfo*>(sl->tab);
+  *d_tiles = reinterpret_cast<const CausalTile*>(static_cast<char*>(sl->tab) + toff);
   if (d_ktiles)
-    *d_ktiles = reinterpret_cast<const KeyTile*>(static_cast<char*>(dc->tab) + toff +
+    *d_ktiles = reinterpret_cast<const KeyTile*>(static_cast<char*>(sl->tab) + toff +
                                                  ((tb + kAlign - 1) / kAlign) * kAlign);
   return MOBA_OK;
 }
@@ -494,7 +540,7 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur,
+  if ((st = get_plan(dc, stream, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur,
                      in.bf16 ? kTileRowsMfma : kTileRowsF32, &pl, &d_seqs, &d_tiles)) !=
       MOBA_OK)
     return st;
@@ -646,7 +692,7 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
   const KeyTile* d_ktiles;
-  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur, kTileRowsMfma, &pl,
+  if ((st = get_plan(dc, stream, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur, kTileRowsMfma, &pl,
                      &d_seqs, &d_tiles, &d_ktiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
@@ -786,7 +832,7 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, in.cu, in.Hq, in.Hkv, 0, 1, kTilesDense,
+  if ((st = get_plan(dc, stream, in.cu, in.Hq, in.Hkv, 0, 1, kTilesDense,
                          in.bf16 ? kTileRowsMfma : kTileRowsF32, &pl, &d_seqs, &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
@@ -869,7 +915,7 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hkv, Hkv, B, kk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+  if ((st = get_plan(dc, stream, cu, Hkv, Hkv, B, kk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
                      &d_tiles)) != MOBA_OK)
     return st;
   Problem p = pl->p;
@@ -954,7 +1000,7 @@ moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hkv, Hkv, block_size, 1, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+  if ((st = get_plan(dc, stream, cu, Hkv, Hkv, block_size, 1, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
                       &d_tiles)) != MOBA_OK)
     return st;
   Phase ph("pool", stream);
@@ -1004,7 +1050,7 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hq, Hkv, block_size, topk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+  if ((st = get_plan(dc, stream, cu, Hq, Hkv, block_size, topk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
                       &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
@@ -1064,7 +1110,7 @@ moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, in
   const Plan* pl;
   const SeqInfo* d_seqs;
   const CausalTile* d_tiles;
-  if ((st = get_plan(dc, cu, Hq, num_kv_heads, block_size, topk, kTilesNone, kTileRowsMfma, &pl,
+  if ((st = get_plan(dc, stream, cu, Hq, num_kv_heads, block_size, topk, kTilesNone, kTileRowsMfma, &pl,
                      &d_seqs, &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
@@ -1109,7 +1155,11 @@ moba_status moba_release_workspace(void) {
   if (it == g_dev.end()) return MOBA_OK;
   if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
   if (it->second.ws) (void)hipFree(it->second.ws);
-  if (it->second.tab) (void)hipFree(it->second.tab);
+  for (PlanSlot& sl : it->second.slots) {
+    if (sl.tab) (void)hipFree(sl.tab);
+    if (sl.stage) (void)hipHostFree(sl.stage);
+    if (sl.uploaded) (void)hipEventDestroy(sl.uploaded);
+  }
   g_dev.erase(it);
   return MOBA_OK;
 }
