@@ -90,3 +90,34 @@ def test_decode_growing_cache(topk):
     torch.cuda.synchronize()
     for i, ((o, l), (ro, rl)) in enumerate(zip(got, ref)):
         assert torch.equal(o, ro) and torch.equal(l, rl), "step %d differs" % i
+
+
+def test_calls_on_a_side_stream():
+    """New shapes first seen on a side stream (default priority): their
+    tables are copied on that stream.  The streams are ordered with events,
+    as calls on different streams must not overlap."""
+    q, k, v = _data(3000, 4, 2, 21)
+    dout = inputs.make_dout(q.shape, q.dtype, 21, device=DEV)
+    splits = [(1234, 1766), (64, 2936), (3000,)]
+    cus = [inputs.cu_seqlens(s) for s in splits]
+    ref = []
+    for cu in cus:
+        o, l = binding.forward(q, k, v, cu, 64, 3)
+        g = binding.backward(q, k, v, cu, 64, 3, o, l, dout)
+        torch.cuda.synchronize()
+        ref.append((o.clone(), l.clone()) + tuple(x.clone() for x in g))
+    binding.release_workspace()  # drops the cached tables too
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream(device=DEV)
+    got = []
+    for i, cu in enumerate(cus):
+        st = side if i % 2 == 0 else main
+        st.wait_stream(main if st is side else side)
+        with torch.cuda.stream(st):
+            o, l = binding.forward(q, k, v, cu, 64, 3)
+            got.append((o, l) + tuple(binding.backward(q, k, v, cu, 64, 3, o, l, dout)))
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(got, ref)):
+        for name, x, y in zip(("out", "lse", "dq", "dk", "dv"), a, b):
+            assert torch.equal(x, y), "split %s, %s differs" % (splits[i], name)
