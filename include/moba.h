@@ -98,7 +98,10 @@ typedef enum {
  * and adds block c (the current block counts toward topk).  out[t, h] is
  * softmax attention over every key of the kept past blocks plus the keys of
  * block c up to and including t.  lse[h, t] is its log-sum-exp.
- * topk larger than the number of blocks selects every causal block.
+ * topk larger than the number of blocks selects every causal block: when
+ * topk is at least the block count of the longest sequence, every row
+ * attends its whole causal prefix and the call runs moba_dense_forward's
+ * kernels (the same result up to rounding).
  *
  * Arguments: see the conventions above.  block_size >= 1, topk >= 1.
  * Returns MOBA_OK or an error status; on error nothing has been enqueued
@@ -125,7 +128,8 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
  * stride).  Products accumulate in fp32; the softmax weights P and the score
  * gradients dS are rounded to bf16 for the second matrix-core products;
  * Delta = <dout, out> per row uses the bf16 out.  Deterministic: no atomics,
- * fixed summation order.
+ * fixed summation order.  When topk is at least the block count of the
+ * longest sequence, this is moba_dense_backward, as in moba_forward.
  */
 moba_status moba_backward(const moba_tensor* q, const moba_tensor* k, const moba_tensor* v,
                           const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
@@ -167,7 +171,9 @@ moba_status moba_dense_backward(const moba_tensor* q, const moba_tensor* k, cons
  *   topk >= 1: MoBA with block_size and topk (the gate of Eq. 5 / Eq. 6 over
  *              the sequence's complete past blocks, top-k with the current
  *              block counted, attention over the selected blocks and the
- *              current block up to the query);
+ *              current block up to the query); a topk of at least the
+ *              longest sequence's block count selects everything and runs
+ *              as topk == 0;
  *   topk == 0: causal full attention over the whole cache (Eq. 1), which is
  *              what the paper uses for generation (Sec. 3.3); block_size is
  *              then ignored.

@@ -507,6 +507,9 @@ AttnArgs make_args(const Inputs& in, const View& vo, float* lse) {
   return a;
 }
 
+moba_status dense_forward_impl(const Inputs& in, const View& vo, moba_tensor* lse,
+                               hipStream_t stream);
+
 }  // namespace
 
 // ======================================================================= ABI
@@ -528,6 +531,9 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   int64_t nbmax = 0;
   for (size_t s = 0; s + 1 < in.cu.size(); s++)
     nbmax = std::max<int64_t>(nbmax, ceil_div((int64_t)in.cu[s + 1] - in.cu[s], block_size));
+  // top-k covering every block of every sequence selects each row's whole
+  // causal prefix (Eq. 5 keeps all min(k, c + 1) blocks): full attention
+  if (topk >= nbmax) return dense_forward_impl(in, vo, lse, stream);
   if (nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
   const int kk = (int)std::min<int64_t>(topk, nbmax);
   if (kk - 1 > 63 && kk - 1 < nbmax - 1) return MOBA_ERR_UNSUPPORTED;
@@ -668,6 +674,13 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   if (!dense && topk < 1) return MOBA_ERR_TOPK;
   if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
   if (in.T == 0) return MOBA_OK;
+  if (!dense) {
+    // as in the forward: top-k covering every block is full attention
+    int64_t nb = 0;
+    for (size_t s = 0; s + 1 < in.cu.size(); s++)
+      nb = std::max<int64_t>(nb, ceil_div((int64_t)in.cu[s + 1] - in.cu[s], block_size));
+    dense = topk >= nb;
+  }
   if (dense) {
     int64_t lmax = 1;
     for (size_t s = 0; s + 1 < in.cu.size(); s++)
@@ -826,6 +839,17 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
   if (st != MOBA_OK) return st;
   if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
   if (in.T == 0) return MOBA_OK;
+  return dense_forward_impl(in, vo, lse, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Causal full attention over validated inputs (cu_seqlens already on the host).
+moba_status dense_forward_impl(const Inputs& in, const View& vo, moba_tensor* lse,
+                               hipStream_t stream) {
+  moba_status st;
   std::lock_guard<std::mutex> lk(g_mu);
   DevCache* dc = cache_for_current_device();
   if (!dc) return MOBA_ERR_HIP;
@@ -861,6 +885,10 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
   return MOBA_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
 moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
                         const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
                         const moba_tensor* kbar, int32_t block_size, int32_t topk, moba_tensor* out,
@@ -886,8 +914,8 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
   if (cu_seqlens->shape[0] != S + 1) return MOBA_ERR_SHAPE;
   if (topk < 0) return MOBA_ERR_TOPK;
-  const bool full = topk == 0;
-  if (!full && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  const bool want_full = topk == 0;
+  if (!want_full && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (T >= (int64_t(1) << 31)) return MOBA_ERR_UNSUPPORTED;
   std::vector<int32_t> cu;
   if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
@@ -897,11 +925,13 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
     if (cu[s + 1] == cu[s]) return MOBA_ERR_SEQLENS;  // every query needs its own cached token
     lmax = std::max<int64_t>(lmax, (int64_t)cu[s + 1] - cu[s]);
   }
+  // top-k covering every block of every sequence is full attention
+  const bool full = want_full || topk >= ceil_div(lmax, block_size);
   const int B = full ? kDecodeChunk : block_size;
   const int64_t nbmax = ceil_div(lmax, B);
   if (!full && nbmax > kMaxBlocksPerSeq) return MOBA_ERR_UNSUPPORTED;
   const int kk = full ? 1 : (int)std::min<int64_t>(topk, nbmax);
-  if (kbar && !full) {
+  if (kbar && !want_full) {
     if (missing(kbar)) return MOBA_ERR_NULL;
     int64_t nb = 0;
     for (int64_t s = 0; s < S; s++) nb += ceil_div((int64_t)cu[s + 1] - cu[s], block_size);

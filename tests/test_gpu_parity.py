@@ -226,3 +226,27 @@ def test_empty_batch():
     k = torch.empty((0, 2, 128), dtype=torch.bfloat16, device=DEV)
     o, l = binding.forward(q, k, k, torch.tensor([0, 0], dtype=torch.int32), 64, 3)
     assert o.shape == (0, 4, 128) and l.shape == (4, 0)
+
+
+def test_topk_covering_every_block_runs_the_dense_path():
+    """top-k at least the longest sequence's block count selects every causal
+    block (Eq. 5), so MoBA is full attention and the library runs the dense
+    kernels: forward, backward and decode equal the dense calls bit for bit
+    (the oracle comparisons of the cases with top-k > #blocks cover the
+    values)."""
+    q, k, v, cu = make((700, 300), 4, 2, torch.bfloat16, 128, offset=0.5, seed=37)  # 6 and 3 blocks
+    o1, l1 = binding.forward(q, k, v, cu, 128, 6)
+    o2, l2 = binding.dense_forward(q, k, v, cu)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    dout = inputs.make_dout(q.shape, q.dtype, 37, device=DEV)
+    g1 = binding.backward(q, k, v, cu, 128, 6, o1, l1, dout)
+    g2 = binding.dense_backward(q, k, v, cu, o2, l2, dout)
+    for x, y in zip(g1, g2):
+        assert torch.equal(x, y)
+    qd = q[(cu[1:] - 1).to(torch.int64).to(DEV)].contiguous()
+    d1 = binding.decode(qd, k, v, cu, 128, 6)
+    d2 = binding.decode(qd, k, v, cu, 128, 0)
+    assert torch.equal(d1[0], d2[0]) and torch.equal(d1[1], d2[1])
+    # one block fewer than the longest sequence has: the MoBA kernels run
+    o3, l3 = binding.forward(q, k, v, cu, 128, 5)
+    assert not torch.equal(o3, o2)
