@@ -1,7 +1,8 @@
 """Parity on seeded random shapes, beyond the hand-picked cases: ragged
 sequence mixes (including empty and one-token sequences), group sizes, block
 sizes that do and do not divide the 64-key tile, top-k from 1 to more than the
-number of blocks.  Every row and every gradient element is compared with the
+number of blocks; bf16 and fp32 forward, decode with and without the
+caller's block means.  Every row and every gradient element is compared with the
 oracle under the tolerances of tests/parity.py; decode rows with near-tied
 gate scores are skipped and counted as in tests/test_gpu_decode.py.
 """
@@ -48,6 +49,7 @@ def random_case(seed, max_tokens, nonempty=False):
 FWD_SEEDS = list(range(100, 124))
 BWD_SEEDS = list(range(200, 212))
 DEC_SEEDS = list(range(300, 312))
+F32_SEEDS = list(range(400, 408))
 
 
 @pytest.mark.parametrize("seed", FWD_SEEDS)
@@ -57,6 +59,15 @@ def test_random_forward(seed):
     r = parity.moba_parity(q, k, v, cu, B, topk, dtype="bf16")
     print(seqlens, hq, hkv, B, topk, "max %.2e mean %.2e lse %.2e ties %d" %
           (r["max_abs"], r["mean_abs"], r["lse_max_abs"], r["tie_rows"]))
+
+
+@pytest.mark.parametrize("seed", F32_SEEDS)
+def test_random_forward_f32(seed):
+    """fp32 inputs: the selection must equal the oracle's exactly."""
+    seqlens, hq, hkv, B, topk = random_case(seed, 600)
+    q, k, v, cu = inputs.make(seqlens, hq, hkv, 128, torch.float32, B, 0.5, seed, device=DEV)
+    r = parity.moba_parity(q, k, v, cu, B, topk, dtype="f32")
+    print(seqlens, hq, hkv, B, topk, "max %.2e lse %.2e" % (r["max_abs"], r["lse_max_abs"]))
 
 
 @pytest.mark.parametrize("seed", BWD_SEEDS)
@@ -69,14 +80,15 @@ def test_random_backward(seed):
 
 
 @pytest.mark.parametrize("seed", DEC_SEEDS)
-@pytest.mark.parametrize("mode", ["moba", "full"])
+@pytest.mark.parametrize("mode", ["moba", "moba_kbar", "full"])
 def test_random_decode(seed, mode):
     seqlens, hq, hkv, B, topk = random_case(seed, 900, nonempty=True)
     q, k, v, cu = inputs.make(seqlens, hq, hkv, 128, torch.bfloat16, B, 0.5, seed, device=DEV)
     T, S = q.shape[0], len(seqlens)
     last = (cu[1:] - 1).to(torch.int64)
     qd = q[last.to(DEV)].contiguous()
-    out, lse = binding.decode(qd, k, v, cu, B, 0 if mode == "full" else topk)
+    kbar = binding.pool(k, cu, B) if mode == "moba_kbar" else None
+    out, lse = binding.decode(qd, k, v, cu, B, 0 if mode == "full" else topk, kbar=kbar)
     torch.cuda.synchronize()
     rows = np.array([int(t) * hq + h for t in last for h in range(hq)], np.int64)
     q_rows = inputs.to_oracle(qd.reshape(S * hq, 128))
