@@ -29,10 +29,12 @@
 //            sums); the value rows are all requested before the softmax; the
 //            normalised partial and its lse go to the workspace; a head that
 //            did not select the chunk's block skips it.
-//   combine  one work-group per row: log-sum-exp merge of the row's
-//            partials (16 interleaved groups, eight partial loads in flight
-//            per group, then the groups in order), rounded once to the
-//            output dtype.
+//   combine  log-sum-exp merge of each row's partials: nsplit work-groups
+//            per row each fold a share of up to kCombineShare consecutive
+//            partial slots (16 interleaved groups, eight partial loads in
+//            flight per group, then the groups in order); with one share
+//            the work-group writes the row, otherwise a second kernel folds
+//            the shares in order.  Rounded once to the output dtype.
 #include "decode_internal.h"
 
 #include <math.h>
@@ -327,7 +329,9 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
 __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Problem p) {
   __shared__ float gm[16], gw[16];
   __shared__ float go[16][kHeadDim];
-  const int64_t row = blockIdx.x;  // s * Hq + h
+  const int64_t row = blockIdx.x / a.nsplit;  // s * Hq + h
+  const int share = (int)(blockIdx.x % a.nsplit);
+  const int xb = share * a.split_len;  // this work-group's partial slots start here
   const int grp = threadIdx.x / 16, l16 = threadIdx.x % 16;
   const int s = (int)(row / p.Hq), h = (int)(row % p.Hq);
   const SeqInfo sq = a.seqs[s];
@@ -352,8 +356,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
   if (a.full) {
     // the group's partials x = grp + 16 i, eight loads in flight per round
     constexpr int kAhead = 8;
-    const int n = (int)((sq.len + kDecodeChunk - 1) / kDecodeChunk);
-    for (int x0 = grp; x0 < n; x0 += 16 * kAhead) {
+    const int n = min((int)((sq.len + kDecodeChunk - 1) / kDecodeChunk), xb + a.split_len);
+    for (int x0 = xb + grp; x0 < n; x0 += 16 * kAhead) {
       float lv[kAhead];
       float4 o0[kAhead], o1[kAhead];
 #pragma unroll
@@ -372,7 +376,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
   } else {
     // the row's chunks: z = y * nsub + i for selection entry y, piece i
     const int32_t* sl = a.sel + row * p.topk;
-    for (int z = grp; z < p.topk * a.nsub; z += 16) {
+    const int zend = min(p.topk * a.nsub, xb + a.split_len);
+    for (int z = xb + grp; z < zend; z += 16) {
       const int y = z / a.nsub, i = z % a.nsub;
       const int j = sl[y];
       if (j < 0) continue;
@@ -400,6 +405,51 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
     const float sc = __builtin_amdgcn_exp2f((gm[x] - Mt) * kLog2e);
     o = fmaf(sc, go[x][d], o);
     wt = fmaf(sc, gw[x], wt);
+  }
+  if (a.nsplit == 1) {
+    a.out[(int64_t)s * a.o_ss + (int64_t)h * a.o_sh + d] = __float2bfloat16(o / wt);
+    if (d == 0) a.lse[(int64_t)h * p.S + s] = Mt + __builtin_amdgcn_logf(wt) * kLn2;
+    return;
+  }
+  // a share without partials leaves weight sum 0, which the second pass skips
+  float* m = a.mid + (int64_t)blockIdx.x * (kHeadDim + 2);
+  m[d] = o;
+  if (d == 0) {
+    m[kHeadDim] = Mt;
+    m[kHeadDim + 1] = wt;
+  }
+}
+
+// Second pass: one work-group per row folds its shares in order (every row
+// has at least the partial of the chunk holding its own key).
+__global__ __launch_bounds__(kHeadDim) void decode_fold_kernel(DecodeArgs a, Problem p) {
+  static_assert(kCombineMaxSplit <= kHeadDim, "one thread per share loads its max and sum");
+  __shared__ float sm[kCombineMaxSplit], sw[kCombineMaxSplit];
+  const int64_t row = blockIdx.x;
+  const int s = (int)(row / p.Hq), h = (int)(row % p.Hq);
+  const int d = threadIdx.x;
+  const float* m = a.mid + row * a.nsplit * (kHeadDim + 2);
+  if (d < a.nsplit) {
+    sm[d] = m[(int64_t)d * (kHeadDim + 2) + kHeadDim];
+    sw[d] = m[(int64_t)d * (kHeadDim + 2) + kHeadDim + 1];
+  }
+  __syncthreads();
+  float Mt = -INFINITY;
+  for (int x = 0; x < a.nsplit; x++)
+    if (sw[x] != 0.0f) Mt = fmaxf(Mt, sm[x]);
+  // every share's value in flight at once (slots past the last share
+  // re-read it and are not used)
+  float v[kCombineMaxSplit];
+#pragma unroll
+  for (int x = 0; x < kCombineMaxSplit; x++)
+    v[x] = m[(int64_t)min(x, a.nsplit - 1) * (kHeadDim + 2) + d];
+  float o = 0.0f, wt = 0.0f;
+#pragma unroll
+  for (int x = 0; x < kCombineMaxSplit; x++) {
+    if (x >= a.nsplit || sw[x] == 0.0f) continue;
+    const float sc = __builtin_amdgcn_exp2f((sm[x] - Mt) * kLog2e);
+    o = fmaf(sc, v[x], o);
+    wt = fmaf(sc, sw[x], wt);
   }
   a.out[(int64_t)s * a.o_ss + (int64_t)h * a.o_sh + d] = __float2bfloat16(o / wt);
   if (d == 0) a.lse[(int64_t)h * p.S + s] = Mt + __builtin_amdgcn_logf(wt) * kLn2;
@@ -435,7 +485,11 @@ hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream
 hipError_t launch_decode_combine(const DecodeArgs& a, const Problem& p, hipStream_t st) {
   const int64_t rows = (int64_t)p.S * p.Hq;
   if (rows <= 0) return hipSuccess;
-  decode_combine_kernel<<<(unsigned)rows, 256, 0, st>>>(a, p);
+  decode_combine_kernel<<<(unsigned)(rows * a.nsplit), 256, 0, st>>>(a, p);
+  if (a.nsplit == 1) return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  decode_fold_kernel<<<(unsigned)rows, kHeadDim, 0, st>>>(a, p);
   return hipGetLastError();
 }
 

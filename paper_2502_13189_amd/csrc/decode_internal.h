@@ -8,6 +8,8 @@ namespace moba {
 
 constexpr int kDecodeChunk = 256;     // keys per attention work-group
 constexpr int kDecodeMaxGroup = 16;   // largest Hq / Hkv the decode kernels take
+constexpr int kCombineShare = 64;    // partials one combine work-group folds
+constexpr int kCombineMaxSplit = 64; // combine work-groups per row, at most
 
 struct DecodeArgs {
   const __hip_bfloat16* q; int64_t q_ss, q_sh;  // [S, Hq, D]
@@ -25,6 +27,9 @@ struct DecodeArgs {
   int nsub;              // chunks per block
   int nchunk;            // chunk slots per row
   int chunk_block;       // block length the chunks are cut at
+  int nsplit;            // combine work-groups per row (1: no second pass)
+  int split_len;         // partial slots per combine work-group
+  float* mid;            // [S * Hq, nsplit, D + 2] per share: unnormalised o, max, weight sum
   int full;              // 1: causal full attention, 0: MoBA
   float scale_log2;
 };
@@ -35,6 +40,7 @@ hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t
 // MoBA: per (sequence, kv-head) the union of the group's selected blocks.
 hipError_t launch_decode_plan(const DecodeArgs& a, const Problem& p, hipStream_t st);
 hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream_t st);
+// Two passes when nsplit > 1: shares of each row's partials, then the shares.
 hipError_t launch_decode_combine(const DecodeArgs& a, const Problem& p, hipStream_t st);
 
 }  // namespace moba

@@ -958,25 +958,34 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   // blocks any head of a group can select: G (k - 1) history blocks plus the current one
   const int nunion = full ? 0 : (int)std::min<int64_t>(nbmax, (int64_t)(Hq / Hkv) * (kk - 1) + 1);
   const bool own_kbar = !full && !kbar;
-  auto layout = [&](Bump* bp, float** kb, int32_t** sel, int32_t** blk, float** po, float** pls) {
+  // combine: a row's partial slots (its chunks, or its selections' chunks)
+  // in shares of kCombineShare, one work-group each
+  const int64_t nslot = full ? nchunk : (int64_t)kk * nsub;
+  const int nsplit = (int)std::min<int64_t>(kCombineMaxSplit, ceil_div(nslot, kCombineShare));
+  const int split_len = (int)ceil_div(nslot, nsplit);
+  auto layout = [&](Bump* bp, float** kb, int32_t** sel, int32_t** blk, float** po, float** pls,
+                    float** mid) {
     *kb = bp->take<float>(own_kbar ? (int64_t)p.nblk_total * Hkv * kHeadDim : 0);
     *sel = bp->take<int32_t>(full ? 0 : S * Hq * kk);
     *blk = bp->take<int32_t>(S * Hkv * nunion);
     *po = bp->take<float>(S * Hq * nchunk * kHeadDim);
     *pls = bp->take<float>(S * Hq * nchunk);
+    *mid = bp->take<float>(nsplit > 1 ? S * Hq * nsplit * (kHeadDim + 2) : 0);
   };
   {
     Bump sz(nullptr);
-    float *a0, *a2, *a3;
+    float *a0, *a2, *a3, *a5;
     int32_t *a1, *a4;
-    layout(&sz, &a0, &a1, &a4, &a2, &a3);
+    layout(&sz, &a0, &a1, &a4, &a2, &a3, &a5);
     if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
     if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
   }
   Bump bp(dc->ws);
   DecodeArgs a{};
   float* kb_ws;
-  layout(&bp, &kb_ws, &a.sel, &a.blocks, &a.part_o, &a.part_lse);
+  layout(&bp, &kb_ws, &a.sel, &a.blocks, &a.part_o, &a.part_lse, &a.mid);
+  a.nsplit = nsplit;
+  a.split_len = split_len;
   a.nunion = nunion;
   a.q = static_cast<const __hip_bfloat16*>(vq.data); a.q_ss = vq.st; a.q_sh = vq.sh;
   a.k = static_cast<const __hip_bfloat16*>(vk.data); a.k_st = vk.st; a.k_sh = vk.sh;

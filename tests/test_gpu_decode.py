@@ -44,6 +44,7 @@ CASES = [
     ((4097, 4096, 300), 8, 2, 512, 4),
     ((600, 45), 16, 1, 64, 3),   # the largest group decode takes
     ((50, 2), 2, 1, 1, 5),       # one-key blocks
+    ((24000, 300), 4, 1, 4096, 5),  # combine in two shares per row (80 MoBA / 94 full slots)
 ]
 
 
