@@ -14,7 +14,8 @@
 //
 //   gate     one work-group per (sequence, query head): fp32 scores of the
 //            query against the block means of the sequence's complete past
-//            blocks (sequential fp32 sums, one block per thread), then top-(k-1) by
+//            blocks (coalesced loads staged through LDS; four partial sums
+//            over dim quarters, added in order), then top-(k-1) by
 //            k-1 rounds of a wave-wide argmax (ties: lower block index), and
 //            the selection written ascending with the current block last.
 //   plan     (MoBA) one wave per (sequence, kv-head): the union of the
@@ -66,12 +67,23 @@ __device__ __forceinline__ void chunk_range(int x, int nsub, int B, int64_t L, i
 }
 
 // ================================================================== gate
-// One work-group per (sequence, query head): its four waves score the
-// candidate blocks (one block per thread, all of a block's loads in flight),
-// then wave 0 selects.
+// One work-group per (sequence, query head).  The block means are read with
+// coalesced loads (each half-wave reads one block's 512 bytes), up to 256
+// blocks per pass, all of a pass's loads in flight at once; 64 blocks at a
+// time go through an LDS tile (rows padded by one float, so the dot products
+// read it without bank conflicts), where thread t forms the partial sum of
+// block t % 64 over dims [32 q, 32 q + 32), q = t / 64, and the four partials
+// are added in order.  Wave 0 then selects.
+constexpr int kGatePass = 256;              // blocks per pass
+constexpr int kGateChunk = 64;              // blocks per LDS tile
+constexpr int kGateRow = kHeadDim + 1;      // padded LDS row (floats)
+constexpr int kGateLoads = kGatePass * (kHeadDim / 4) / 256;  // float4 per thread per pass
+
 __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem p) {
   __shared__ float qs[kHeadDim];
   __shared__ float sc[kMaxBlocksPerSeq];
+  __shared__ float kt[kGateChunk * kGateRow];
+  __shared__ float ps[4][kGateChunk];
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t row = blockIdx.x;  // s * Hq + h
   const int s = (int)(row / p.Hq), h = (int)(row % p.Hq);
@@ -83,24 +95,42 @@ __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem 
     qs[2 * tid] = bf16_lo(w);
     qs[2 * tid + 1] = bf16_hi(w);
   }
-  __syncthreads();
   const int c = (int)((sq.len - 1) / p.B);  // current block; candidates j < c
-  // scores, one block per thread, dims in order
-  for (int j = tid; j < c; j += 256) {
-    const float4* kb = reinterpret_cast<const float4*>(
-        a.kbar + ((int64_t)(sq.blk_off + j) * p.Hkv + g) * kHeadDim);
-    float4 kv[kHeadDim / 4];
+  const int jb = tid % kGateChunk, quarter = tid / kGateChunk;
+  for (int j0 = 0; j0 < c; j0 += kGatePass) {
+    // float4 e = tid + 256 i of the pass: block e / 32, piece e % 32
+    float4 kv[kGateLoads];
 #pragma unroll
-    for (int d4 = 0; d4 < kHeadDim / 4; d4++) kv[d4] = kb[d4];
-    float acc = 0.0f;
-#pragma unroll
-    for (int d4 = 0; d4 < kHeadDim / 4; d4++) {
-      acc = fmaf(qs[4 * d4], kv[d4].x, acc);
-      acc = fmaf(qs[4 * d4 + 1], kv[d4].y, acc);
-      acc = fmaf(qs[4 * d4 + 2], kv[d4].z, acc);
-      acc = fmaf(qs[4 * d4 + 3], kv[d4].w, acc);
+    for (int i = 0; i < kGateLoads; i++) {
+      const int e = tid + 256 * i;
+      const int j = min(j0 + e / (kHeadDim / 4), c - 1);  // past the candidates: re-read, unused
+      kv[i] = reinterpret_cast<const float4*>(
+          a.kbar + ((int64_t)(sq.blk_off + j) * p.Hkv + g) * kHeadDim)[e % (kHeadDim / 4)];
     }
-    sc[j] = acc;
+#pragma unroll
+    for (int ch = 0; ch < kGatePass / kGateChunk; ch++) {
+      if (j0 + ch * kGateChunk >= c) break;  // uniform over the work-group
+      __syncthreads();  // the previous tile (and qs, first time) is done with
+#pragma unroll
+      for (int i = 0; i < kGateLoads / (kGatePass / kGateChunk); i++) {
+        const int ii = ch * (kGateLoads / (kGatePass / kGateChunk)) + i;
+        const int e = tid + 256 * ii - ch * kGateChunk * (kHeadDim / 4);
+        float* dst = kt + (e / (kHeadDim / 4)) * kGateRow + 4 * (e % (kHeadDim / 4));
+        dst[0] = kv[ii].x;
+        dst[1] = kv[ii].y;
+        dst[2] = kv[ii].z;
+        dst[3] = kv[ii].w;
+      }
+      __syncthreads();
+      float acc = 0.0f;
+      const float* kr = kt + jb * kGateRow + 32 * quarter;
+#pragma unroll
+      for (int d = 0; d < 32; d++) acc = fmaf(qs[32 * quarter + d], kr[d], acc);
+      ps[quarter][jb] = acc;
+      __syncthreads();
+      const int j = j0 + ch * kGateChunk + tid;
+      if (tid < kGateChunk && j < c) sc[j] = ((ps[0][tid] + ps[1][tid]) + ps[2][tid]) + ps[3][tid];
+    }
   }
   __syncthreads();
   if (tid >= 64) return;

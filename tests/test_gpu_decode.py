@@ -7,7 +7,7 @@ attention for the rows (cu[s+1] - 1, h), reading only those rows' query
 vectors.  MoBA mode with the block means passed in and computed on the fly,
 and full-attention mode (what the paper uses for generation).
 
-The decode gate sums scores in fp32 in dim order; a row whose k-th and
+The decode gate sums scores in fp32 in its own fixed order; a row whose k-th and
 (k+1)-th best oracle scores are closer than the gate's rounding bound
 (tau of tests/parity.py) has two correct selections, so its output is not
 compared (the count is reported; the selection invariants still hold there).
