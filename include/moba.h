@@ -183,8 +183,8 @@ moba_status moba_dense_backward(const moba_tensor* q, const moba_tensor* k, cons
  * kbar and recomputes it only when a block completes.
  * out [S, Hq, D] bf16 and lse [Hq, S] f32 (natural log) as for moba_forward.
  * Hq / Hkv must not exceed 16.  Gate scores are fp32 sums in a fixed order
- * (four sequential 32-dim partial sums, added in order); near-ties may be broken differently from moba_select's matrix-core
- * gate.  A call whose cu_seqlens differs from those of recent calls (every
+ * (four sequential 32-dim partial sums, added in order); near-ties may be
+ * broken differently from moba_select's matrix-core gate.  A call whose cu_seqlens differs from those of recent calls (every
  * step of a growing cache) builds new per-shape tables on the host and copies
  * them on `stream`; it does not synchronize the device.
  */
