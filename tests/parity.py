@@ -296,3 +296,89 @@ def decode_ambiguous_rows(q_rows, rows, T, Hq, kn, cu, B, topk):
         tau = TAU_SCALE * (qf[i] @ kabs[boff[s] + ja, h // G] + qf[i] @ kabs[boff[s] + jb, h // G])
         amb[i] = cand[ja] - cand[jb] <= tau
     return osel, amb
+
+
+def admissible_selections(q_rows, rows, T, Hq, kn, cu, B, topk, max_swap=3):
+    """Every selection a correct fp32 gate may return for each listed row
+    (query vectors q_rows [nrows, D] in list order).  Eq. 5 orders the past
+    blocks by exact score; the gate's rounding may reorder two blocks a, b
+    whose exact scores differ by at most tau_a + tau_b (the bound of
+    check_selection).  So a selection is admissible iff every block it keeps
+    and every past block it drops are in Eq. 5's order up to that bound.
+    Returns one list per row, the oracle's selection first, then the
+    admissible ones reached by exchanging up to max_swap kept blocks with
+    dropped ones near the boundary."""
+    import itertools
+
+    cu = np.asarray(cu)
+    kbar, kabs = oracle.pool(kn, cu, B, with_abs=True)
+    osel = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows)
+    boff = block_offsets(cu, B)
+    G = Hq // kn.shape[1]
+    cs = []
+    for r in rows:
+        t = int(r) // Hq
+        s = int(seq_of_tokens(cu, t))
+        cs.append((t - int(cu[s])) // B)
+    nmax = max(cs) + 1 if len(cs) else 1
+    _, sc = oracle.select_rows(q_rows, T, Hq, kbar, cu, B, topk, rows, nmax=nmax)
+    qf = np.abs(_widen(np.asarray(q_rows).reshape(len(rows), -1)))
+    result = []
+    for i, r in enumerate(rows):
+        t, h = int(r) // Hq, int(r) % Hq
+        s = int(seq_of_tokens(cu, t))
+        c = cs[i]
+        alts = [osel[i].copy()]
+        nh = min(topk - 1, c)
+        if 0 < nh < c:
+            tau = TAU_SCALE * (kabs[boff[s]:boff[s] + c, h // G] @ qf[i])
+            score = sc[i, :c]
+            kept = [int(x) for x in osel[i][:nh]]
+            dropped = [j for j in range(c) if j not in set(kept)]
+
+            def near(a, b):
+                return score[b] - score[a] <= tau[a] + tau[b] and score[a] - score[b] <= tau[a] + tau[b]
+
+            kin = [a for a in kept if any(near(a, b) for b in dropped)]
+            kout = [b for b in dropped if any(near(a, b) for a in kept)]
+            for n in range(1, min(max_swap, len(kin), len(kout)) + 1):
+                for xs in itertools.combinations(kin, n):
+                    for ys in itertools.combinations(kout, n):
+                        keep = sorted((set(kept) - set(xs)) | set(ys))
+                        drop = [j for j in range(c) if j not in set(keep)]
+                        if all(score[b] - score[a] <= tau[a] + tau[b] for a in keep for b in drop):
+                            alt = np.full(topk, -1, np.int32)
+                            alt[:nh] = keep
+                            alt[nh] = c
+                            alts.append(alt)
+        result.append(alts)
+    return result
+
+
+def check_rows_any_selection(gout, glse, q_rows, rows, T, Hq, kn, vn, cu, B, topk, what=""):
+    """Outputs of rows whose selection is not returned (decode): each row must
+    match the oracle's attention over one of its admissible selections
+    (admissible_selections); the row's closest one is used for the
+    tolerances of compare_outputs.  Returns (max-abs, mean-abs, lse max-abs,
+    rows with several admissible selections, rows matched by one other than
+    the oracle's)."""
+    alts = admissible_selections(q_rows, rows, T, Hq, kn, cu, B, topk)
+    idx = np.array([i for i, a in enumerate(alts) for _ in a], np.int64)
+    sels = np.stack([x for a in alts for x in a]) if len(idx) else np.zeros((0, topk), np.int32)
+    qr = np.asarray(q_rows).reshape(len(rows), -1)
+    oo, ol = oracle.attend_rows(qr[idx], T, Hq, kn, vn, np.asarray(cu), B, sels, np.asarray(rows)[idx])
+    gout = np.asarray(gout, np.float64).reshape(len(rows), -1)
+    glse = np.asarray(glse, np.float64).reshape(len(rows))
+    best_o = np.empty_like(gout)
+    best_l = np.empty_like(glse)
+    pos, multi, other = 0, 0, 0
+    for i, a in enumerate(alts):
+        n = len(a)
+        err = [np.abs(gout[i] - oo[pos + x]).max() + np.abs(glse[i] - ol[pos + x]) for x in range(n)]
+        x = int(np.argmin(err))
+        best_o[i], best_l[i] = oo[pos + x], ol[pos + x]
+        multi += n > 1
+        other += x > 0
+        pos += n
+    mx, mean, lmx = compare_outputs(gout, glse, best_o, best_l, "bf16", what)
+    return mx, mean, lmx, multi, other

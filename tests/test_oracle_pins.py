@@ -446,3 +446,92 @@ def test_compact_query_rows_match_full_arrays():
     o_full, l_full = oracle.attend(qn, kn, vn, cun, 64, s_full, rows=rows)
     o_rows, l_rows = oracle.attend_rows(q_rows, q.shape[0], 8, kn, vn, cun, 64, s_rows, rows)
     assert np.array_equal(o_full, o_rows) and np.array_equal(l_full, l_rows)
+
+
+# ----------------------------------------------------------------------------
+# the gate's score output (read by the tie rule of the GPU comparisons)
+# ----------------------------------------------------------------------------
+def exact_scores(qn, kn, cu, B, rows):
+    """Eq. 6 in exact rational arithmetic: for each listed row (t*Hq + h) the
+    map {j: <q_t,h, mean of block j's keys>} over its past blocks j < c
+    (Sec. 2.2: blocks from the current one on are never scored).  Also the
+    sum over i of |q_i| * |mean_i|, the scale of the fp64 rounding."""
+    T, Hq, D = qn.shape
+    G = Hq // kn.shape[1]
+    Q = _frac_inputs(qn)
+    K = _frac_inputs(kn)
+    out = []
+    for r in rows:
+        t, h = int(r) // Hq, int(r) % Hq
+        g = h // G
+        s = int(np.searchsorted(cu, t, side="right")) - 1
+        a, b = int(cu[s]), int(cu[s + 1])
+        c = (t - a) // B
+        sc = {}
+        for j in range(c):
+            toks = range(a + j * B, min(a + (j + 1) * B, b))
+            mean = [sum(K[u][g][d] for u in toks) / len(toks) for d in range(D)]
+            sc[j] = (sum(Q[t][h][d] * mean[d] for d in range(D)),
+                     sum(abs(Q[t][h][d]) * abs(mean[d]) for d in range(D)))
+        out.append(sc)
+    return out
+
+
+def assert_scores(sc, ref, nmax, exact):
+    assert sc.shape == (len(ref), nmax)
+    for i, row in enumerate(ref):
+        for j in range(nmax):
+            if j in row:
+                val, mag = row[j]
+                if exact:
+                    assert Fraction(float(sc[i, j])) == val, (i, j, sc[i, j], float(val))
+                else:
+                    assert abs(Fraction(float(sc[i, j])) - val) <= Fraction(2 ** -45) * mag, (i, j)
+            else:
+                assert np.isnan(sc[i, j]), (i, j, sc[i, j])
+
+
+def test_gate_scores_exact_integer_inputs():
+    """The score output of the gate (Eq. 6) for every listed row and every
+    past block is the exact inner product of the query with the block mean;
+    with small-integer inputs and a power-of-two block size every such value
+    is exact in fp64, so any wrong row, block, head or stride changes it.
+    Blocks from the current one on are NaN (masked, Sec. 2.2), and so is
+    every place past the last block."""
+    rng = np.random.default_rng(31)
+    seqlens = (23, 0, 17, 9)
+    T = sum(seqlens)
+    qn = rng.integers(-3, 4, size=(T, 4, 5)).astype(np.float32)
+    kn = rng.integers(-3, 4, size=(T, 2, 5)).astype(np.float32)
+    cu = inputs.cu_seqlens(seqlens).numpy()
+    B, nmax = 4, 7
+    kbar = oracle.pool(kn, cu, B)
+    rows = np.arange(T * 4, dtype=np.int64)
+    sel, sc = oracle.select(qn, kbar, cu, B, 3, nmax=nmax)
+    ref = exact_scores(qn, kn, cu, B, rows)
+    assert_scores(sc, ref, nmax, exact=True)
+    # a subset of rows, in a scrambled order
+    sub = rng.permutation(rows)[:50]
+    _, sc2 = oracle.select(qn, kbar, cu, B, 3, rows=sub, nmax=nmax)
+    assert_scores(sc2, [ref[int(r)] for r in sub], nmax, exact=True)
+    _, sc3 = oracle.select_rows(qn.reshape(-1, 5)[sub], T, 4, kbar, cu, B, 3, sub, nmax=nmax)
+    assert_scores(sc3, [ref[int(r)] for r in sub], nmax, exact=True)
+
+
+@pytest.mark.parametrize("B", [3, 5])
+def test_gate_scores_gaussian_ragged_gqa(B):
+    """The same pin on Gaussian bf16 inputs with ragged blocks and GQA
+    groups of 3, where the block means are not exact: every score must equal
+    the exact rational value to the fp64 rounding of the mean and the dot
+    product (far below the 2^-14 tie tolerance the GPU comparisons use)."""
+    qn, kn, _, cu = rand_case((26, 3, 19), 6, 2, 6, B, torch.bfloat16, seed=40 + B)
+    T = qn.shape[0]
+    kbar = oracle.pool(kn, cu, B)
+    rng = np.random.default_rng(B)
+    rows = np.sort(rng.choice(T * 6, size=90, replace=False)).astype(np.int64)
+    nmax = 9
+    ref = exact_scores(qn, kn, cu, B, rows)
+    _, sc = oracle.select(qn, kbar, cu, B, 2, rows=rows, nmax=nmax)
+    assert_scores(sc, ref, nmax, exact=False)
+    _, sc2 = oracle.select_rows(qn.reshape(-1, 6)[rows], T, 6, kbar, cu, B, 2, rows, nmax=nmax)
+    assert_scores(sc2, ref, nmax, exact=False)
