@@ -45,12 +45,13 @@ def seq_of_tokens(cu, t):
     return np.searchsorted(cu, t, side="right") - 1
 
 
-def check_selection(gpu_sel, rows, qn, kn, cu, B, topk, exact):
+def check_selection(gpu_sel, rows, qn, kn, cu, B, topk, exact, pooled=None):
     """Compare GPU selections (for `rows`) with the oracle's.  Returns
     (oracle_sel, mismatch_rows).  Raises AssertionError on a mismatch that is
-    not allowed."""
+    not allowed.  pooled: the oracle's (block means, mean |K|) of kn, if
+    already computed."""
     cu = np.asarray(cu)
-    kbar, kabs = oracle.pool(kn, cu, B, with_abs=True)
+    kbar, kabs = pooled if pooled is not None else oracle.pool(kn, cu, B, with_abs=True)
     osel = oracle.select(qn, kbar, cu, B, topk, rows=rows)
     gsel = np.asarray(gpu_sel).reshape(len(rows), topk)
     bad = np.nonzero((gsel != osel).any(axis=1))[0]

@@ -6,10 +6,11 @@ one in MoBA mode.
 
 Every decode row is checked (S * Hq rows): the oracle computes the last
 prefill row of each sequence from that row's query vector alone, over up to
-the whole 1M-token cache in full mode.  MoBA rows whose k-th and (k+1)-th
-oracle gate scores lie within the gate's rounding bound have two correct
-selections and are skipped (counted); the tolerances are those of
-tests/parity.py.
+the whole 1M-token cache in full mode.  A MoBA row whose (k-1)-th and k-th
+oracle gate scores lie within the gate's rounding bound has more than one
+correct selection; it is compared with the oracle's attention over the
+admissible selection closest to it (parity.check_rows_any_selection), so no
+row is left out.  The tolerances are those of tests/parity.py.
 """
 import numpy as np
 import pytest
@@ -63,13 +64,9 @@ def test_decode_workload(name):
     fmx, fmean, flmx = parity.compare_outputs(gout, glse, oout, olse, "bf16", "full")
 
     print("[dec] %s: oracle, MoBA gate and attention" % name, flush=True)
-    osel, amb = parity.decode_ambiguous_rows(q_rows, rows, T, Hq, kn, cun, w.block_size, w.topk)
-    oout, olse = oracle.attend_rows(q_rows, T, Hq, kn, vn, cun, w.block_size, osel, rows)
-    keep = ~amb
-    gout, glse = got["moba"]
-    mmx, mmean, mlmx = parity.compare_outputs(gout[keep], glse[keep], oout[keep], olse[keep], "bf16",
-                                              "moba")
-    print("%s: %d decode rows; full out max-abs %.2e mean-abs %.2e lse %.2e; MoBA (near-tie rows "
-          "skipped %d) out max-abs %.2e mean-abs %.2e lse %.2e"
-          % (name, len(rows), fmx, fmean, flmx, int(amb.sum()), mmx, mmean, mlmx))
-    assert keep.sum() >= len(rows) // 2, "most rows must be unambiguous"
+    mmx, mmean, mlmx, multi, other = parity.check_rows_any_selection(
+        got["moba"][0], got["moba"][1], q_rows, rows, T, Hq, kn, vn, cun, w.block_size, w.topk,
+        "moba")
+    print("%s: %d decode rows; full out max-abs %.2e mean-abs %.2e lse %.2e; MoBA (rows with "
+          "several admissible selections %d, matched another %d) out max-abs %.2e mean-abs %.2e "
+          "lse %.2e" % (name, len(rows), fmx, fmean, flmx, multi, other, mmx, mmean, mlmx))
