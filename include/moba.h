@@ -27,8 +27,10 @@
  *                      non-decreasing, cu[S] = T.  Sequence s holds tokens
  *                      [cu[s], cu[s+1]); blocks restart at every sequence and
  *                      nothing is attended across sequences.  A device
- *                      cu_seqlens costs one device-to-host copy and a sync;
- *                      pass it in host memory to keep the call asynchronous.
+ *                      cu_seqlens is copied to the host on `stream` (after
+ *                      the work enqueued there before the call) and the
+ *                      stream is waited for; pass it in host memory to keep
+ *                      the call asynchronous.
  *
  * Head dimension D must be 128.  Hq must be a multiple of Hkv (GQA: query head
  * h uses kv-head h / (Hq / Hkv)) and Hq / Hkv <= 128.  Logits are scaled by
@@ -230,17 +232,65 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
  *            e = r * (topk - 1) + x, where x is the selection slot (position
  *            in sel) and r = g * (T * G) + t * G + (h - g * G) with G = Hq/Hkv;
  *            ascending within a bin.  E must equal the number of history
- *            selections, sum over rows of min(topk - 1, c).
+ *            selections, sum over rows of min(topk - 1, c) (moba_route_size
+ *            reports it).
  * num_kv_heads gives Hkv.  The current block is not routed.
  */
 moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, int32_t block_size,
                        int32_t num_kv_heads, moba_tensor* counts, moba_tensor* offsets,
                        moba_tensor* entries, hipStream_t stream);
 
-/* Bytes of device workspace the library currently holds on the current device. */
-size_t moba_workspace_bytes(void);
+/*
+ * Workspace sizing query: the device workspace bytes moba_forward needs to
+ * run in one pass (no kv-head chunking) for any batch of T tokens in
+ * nblk_total blocks (sum over sequences of ceil(len / block_size)), with
+ * Hq / Hkv heads, head dimension D and topk, for either input dtype.  It is
+ * an upper bound over every cu_seqlens with these totals; moba_dense_forward,
+ * moba_select and moba_route need no more.  With MOBA_WORKSPACE_LIMIT_BYTES
+ * below it the forward runs in more kv-head chunks instead.  The backward
+ * needs more (fp32 dQ partials).  Returns 0 for invalid or empty arguments
+ * (T < 0, Hq or Hkv < 1, Hq % Hkv != 0, Hq / Hkv > 128, D != 128,
+ * topk < 1; T == 0 or nblk_total == 0).  Host-only arithmetic: no HIP call.
+ */
+size_t moba_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv, int32_t D, int64_t nblk_total,
+                            int32_t topk);
 
-/* Free the cached workspace of the current device (synchronizes the device). */
+/* Bytes of device workspace the library currently holds on the current device. */
+size_t moba_workspace_held_bytes(void);
+
+/*
+ * Sizes of moba_route's outputs for a batch (Algorithm 1,
+ * index_select_moba_attn_block):
+ *   *nblk_total = sum over sequences of ceil(len / block_size), so counts has
+ *                 Hkv * *nblk_total entries and offsets one more;
+ *   *entries    = E, the number of history selections: num_q_heads times the
+ *                 sum over tokens of min(topk - 1, c), c the token's block
+ *                 (Eq. 5 keeps min(topk - 1, c) past blocks besides the
+ *                 current one; Sec. 3.1 footnote).
+ * cu_seqlens as for moba_forward (host or device; a device copy is read on
+ * `stream`, which is then waited for).  Errors: MOBA_ERR_NULL,
+ * MOBA_ERR_SEQLENS, MOBA_ERR_BLOCK_SIZE, MOBA_ERR_TOPK, MOBA_ERR_SHAPE
+ * (num_q_heads < 1).  No device work besides that copy.
+ */
+moba_status moba_route_size(const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                            int32_t num_q_heads, int64_t* nblk_total, int64_t* entries,
+                            hipStream_t stream);
+
+/*
+ * The dK/dV kernel of moba_backward hands each 32-row subtile's softmax
+ * weights from one wave to another through a flag, with a bounded wait (so
+ * that the kernel always ends).  A wait that gives up leaves that subtile's
+ * dK wrong; every give-up is counted on the device.  This call waits for the
+ * current device, stores the count since the last call in *count and resets
+ * it.  With MOBA_DEBUG_SYNC set (non-zero), moba_backward checks the count
+ * itself and returns MOBA_ERR_HIP if it is not zero.  Testing aid: with
+ * MOBA_FORCE_WAIT_TIMEOUT set (non-zero) every such wait gives up after a
+ * few polls.
+ */
+moba_status moba_take_wait_timeouts(uint64_t* count);
+
+/* Free the cached workspace, tables and counters of the current device
+ * (synchronizes the device). */
 moba_status moba_release_workspace(void);
 
 /* Static, human-readable name of a status. */

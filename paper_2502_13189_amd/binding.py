@@ -71,8 +71,15 @@ def load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    i64 = ctypes.c_int64
     lib.moba_workspace_bytes.restype = ctypes.c_size_t
-    lib.moba_workspace_bytes.argtypes = []
+    lib.moba_workspace_bytes.argtypes = [i64, i32, i32, i32, i64, i32]
+    lib.moba_workspace_held_bytes.restype = ctypes.c_size_t
+    lib.moba_workspace_held_bytes.argtypes = []
+    lib.moba_route_size.restype = ctypes.c_int
+    lib.moba_route_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(i64), ctypes.POINTER(i64), vp]
+    lib.moba_take_wait_timeouts.restype = ctypes.c_int
+    lib.moba_take_wait_timeouts.argtypes = [ctypes.POINTER(ctypes.c_uint64)]
     lib.moba_release_workspace.restype = ctypes.c_int
     lib.moba_release_workspace.argtypes = []
     lib.moba_status_string.restype = ctypes.c_char_p
@@ -218,9 +225,21 @@ def dense_forward(q, k, v, cu_seqlens, out=None, lse=None, stream=None):
     return out, lse
 
 
+def route_size(cu_seqlens, block_size: int, topk: int, num_q_heads: int, stream=None):
+    """(nblk_total, E) as the library reports them: the batch's block count
+    and its number of history selections (moba_route's entries)."""
+    lib = load()
+    cu = _cu(cu_seqlens)
+    nb, e = ctypes.c_int64(), ctypes.c_int64()
+    dc = describe(cu)
+    _check("moba_route_size", lib.moba_route_size(_ref(dc), int(block_size), int(topk),
+                                                  int(num_q_heads), ctypes.byref(nb),
+                                                  ctypes.byref(e), _stream(cu, stream)))
+    return int(nb.value), int(e.value)
+
+
 def num_blocks(cu_seqlens, block_size: int) -> int:
-    cu = _cu(cu_seqlens).tolist()
-    return sum((cu[i + 1] - cu[i] + block_size - 1) // block_size for i in range(len(cu) - 1))
+    return route_size(cu_seqlens, block_size, 1, 1)[0]
 
 
 def pool(k, cu_seqlens, block_size: int, stream=None):
@@ -249,25 +268,13 @@ def select(q, k, cu_seqlens, block_size: int, topk: int, nmax: int = 0, stream=N
     return (sel, scores) if nmax > 0 else sel
 
 
-def history_entries(cu_seqlens, block_size: int, topk: int, num_q_heads: int) -> int:
-    """Number of history selections: sum over rows of min(topk-1, c)."""
-    cu = _cu(cu_seqlens).tolist()
-    e = 0
-    for i in range(len(cu) - 1):
-        L = cu[i + 1] - cu[i]
-        for c in range((L + block_size - 1) // block_size):
-            m = min(L, (c + 1) * block_size) - c * block_size
-            e += m * min(topk - 1, c)
-    return e * num_q_heads
-
-
 def route(sel, cu_seqlens, block_size: int, num_kv_heads: int, stream=None):
     """(counts [Hkv*nblk] int32, offsets [Hkv*nblk+1] int64, entries [E] int32)."""
     lib = load()
     cu = _cu(cu_seqlens)
     T, Hq, topk = sel.shape
-    nbins = num_blocks(cu, block_size) * num_kv_heads
-    E = history_entries(cu, block_size, topk, Hq)
+    nb, E = route_size(cu, block_size, topk, Hq, stream)
+    nbins = nb * num_kv_heads
     counts = torch.empty((nbins,), dtype=torch.int32, device=sel.device)
     offsets = torch.empty((nbins + 1,), dtype=torch.int64, device=sel.device)
     entries = torch.empty((E,), dtype=torch.int32, device=sel.device)
@@ -277,8 +284,24 @@ def route(sel, cu_seqlens, block_size: int, num_kv_heads: int, stream=None):
     return counts, offsets, entries
 
 
-def workspace_bytes() -> int:
-    return int(load().moba_workspace_bytes())
+def workspace_bytes(T: int, num_q_heads: int, num_kv_heads: int, nblk_total: int, topk: int,
+                    head_dim: int = 128) -> int:
+    """Device workspace bytes a one-pass moba_forward needs (an upper bound)."""
+    return int(load().moba_workspace_bytes(int(T), int(num_q_heads), int(num_kv_heads),
+                                           int(head_dim), int(nblk_total), int(topk)))
+
+
+def workspace_held_bytes() -> int:
+    """Bytes of device workspace the library holds on the current device."""
+    return int(load().moba_workspace_held_bytes())
+
+
+def take_wait_timeouts() -> int:
+    """Give-ups of the backward's hand-over wait since the last call (waits
+    for the device)."""
+    n = ctypes.c_uint64()
+    _check("moba_take_wait_timeouts", load().moba_take_wait_timeouts(ctypes.byref(n)))
+    return int(n.value)
 
 
 def release_workspace() -> None:

@@ -393,7 +393,6 @@ constexpr int kChunk = 64;          // rows per chunk
 constexpr int kBufR = kChunk * 16;  // one row-major Q or dO chunk: 64 rows x 16 16-byte chunks
 constexpr int kDmaR = kBufR / 64;   // DMA instructions per chunk and tensor (16)
 constexpr int kSlots = 3;           // row tables in flight
-constexpr int kSpinLimit = 1 << 20; // polls of a hand-over flag before giving up
 // s_waitcnt operand that waits for LDS operations only (lgkmcnt 0, vmcnt and
 // expcnt at their maxima)
 constexpr int kWaitLds = 0xC07F;
@@ -772,10 +771,13 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
         if (!live) continue;
         const f32x16 sd = sd_product(dr, st, offa, kv);  // dP
         if (have_prev) g_product(acc, q_prev, st_prev, offt, wb_prev);  // dK^T += Q^T dS
-        // wait (bounded, so it always ends) for the P-wave's P(st)
-        const int seq = 2 * i + st + 1;
+        // wait (bounded, so it always ends) for the P-wave's P(st); a wait
+        // that gives up goes on with a stale P and is counted, so the host
+        // can report it (the flag is in LDS: n is wave-uniform)
+        const int seq = 2 * i + st + 1 + a.wait_bias;
         int n = 0;
-        while (*flag < seq && ++n < kSpinLimit) __builtin_amdgcn_s_sleep(1);
+        while (*flag < seq && ++n < a.spin_limit) __builtin_amdgcn_s_sleep(1);
+        if (n >= a.spin_limit && lane == 0) atomicAdd(a.wait_timeouts, 1u);
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         ds_weights(sd, R, slot, st, hh, lane, X.p[st][pair], wb_prev);
         have_prev = true;

@@ -45,6 +45,12 @@ struct BwdArgs {
   int g0, g1;        // kv-heads of this chunk (dQ kernels)
   float scale_log2;  // log2(e) / sqrt(D)
   float scale;       // 1 / sqrt(D)
+  // dK/dV hand-over wait: polls before a wave gives up, and an offset added
+  // to the awaited flag value (0; a test sets it out of reach so that every
+  // wait gives up).  Each give-up adds one to *wait_timeouts.
+  int spin_limit;
+  int wait_bias;
+  uint32_t* wait_timeouts;
 };
 
 // Every launcher enqueues on `st` and returns the launch status.

@@ -32,6 +32,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr size_t kDefaultWorkspaceLimit = size_t(64) << 30;
+constexpr int kSpinLimit = 1 << 20;  // polls of a dK/dV hand-over flag before a wave gives up
 
 // ------------------------------------------------------------- profiling
 struct PhaseRec {
@@ -62,13 +63,13 @@ struct Phase {
   }
 };
 
-bool debug_sync() {
-  static const bool on = [] {
-    const char* e = std::getenv("MOBA_DEBUG_SYNC");
-    return e && e[0] && e[0] != '0';
-  }();
-  return on;
+bool env_flag(const char* name) {
+  const char* e = std::getenv(name);
+  return e && e[0] && e[0] != '0';
 }
+
+// Read at every launch, so a process can switch it on and off.
+bool debug_sync() { return env_flag("MOBA_DEBUG_SYNC"); }
 
 #define MOBA_LAUNCH(expr)                                         \
   do {                                                            \
@@ -146,8 +147,15 @@ moba_status check_cu_desc(const moba_tensor* cu) {
   return MOBA_OK;
 }
 
-// Copy cu_seqlens to the host (one sync if it lives on the device) and check it.
-moba_status read_cu(const moba_tensor* cu, int64_t T, std::vector<int32_t>* out) {
+// Pinned staging buffer for cu_seqlens that live on the device.
+std::mutex g_cu_mu;
+int32_t* g_cu_stage = nullptr;
+int64_t g_cu_cap = 0;
+
+// Copy cu_seqlens to the host.  Device-resident offsets are copied on the
+// caller's stream, after the work that may have written them, and the
+// stream is waited for (the one synchronization of such a call).
+moba_status fetch_cu(const moba_tensor* cu, hipStream_t stream, std::vector<int32_t>* out) {
   const int64_t n = cu->shape[0];
   out->resize(n);
   hipPointerAttribute_t attr;
@@ -157,17 +165,44 @@ moba_status read_cu(const moba_tensor* cu, int64_t T, std::vector<int32_t>* out)
   else
     (void)hipGetLastError();  // plain host memory: clear the lookup error
   if (on_device) {
-    if (hipMemcpy(out->data(), cu->data, n * sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+    std::lock_guard<std::mutex> lk(g_cu_mu);
+    if (g_cu_cap < n) {
+      if (g_cu_stage) (void)hipHostFree(g_cu_stage);
+      g_cu_stage = nullptr;
+      g_cu_cap = 0;
+      if (hipHostMalloc(reinterpret_cast<void**>(&g_cu_stage), n * sizeof(int32_t),
+                        hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        g_cu_stage = nullptr;
+        return MOBA_ERR_NO_MEMORY;
+      }
+      g_cu_cap = n;
+    }
+    if (hipMemcpyAsync(g_cu_stage, cu->data, n * sizeof(int32_t), hipMemcpyDeviceToHost,
+                       stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
       return MOBA_ERR_HIP;
+    std::memcpy(out->data(), g_cu_stage, n * sizeof(int32_t));
   } else {
     std::memcpy(out->data(), cu->data, n * sizeof(int32_t));
   }
-  const std::vector<int32_t>& c = *out;
+  return MOBA_OK;
+}
+
+// cu[0] = 0, non-decreasing, cu[S] = T.
+moba_status check_cu(const std::vector<int32_t>& c, int64_t T) {
+  const int64_t n = (int64_t)c.size();
   if (c[0] != 0) return MOBA_ERR_SEQLENS;
   for (int64_t s = 0; s + 1 < n; s++)
     if (c[s + 1] < c[s]) return MOBA_ERR_SEQLENS;
   if (c[n - 1] != T) return MOBA_ERR_SEQLENS;
   return MOBA_OK;
+}
+
+moba_status read_cu(const moba_tensor* cu, int64_t T, hipStream_t stream,
+                    std::vector<int32_t>* out) {
+  moba_status st = fetch_cu(cu, stream, out);
+  return st != MOBA_OK ? st : check_cu(*out, T);
 }
 
 // ------------------------------------------------------------- planning
@@ -334,6 +369,7 @@ struct DevCache {
   size_t ws_bytes = 0;
   PlanSlot slots[kPlanSlots];
   uint64_t clock = 0;
+  uint32_t* wait_timeouts = nullptr;  // device counter of dK/dV hand-over give-ups
 };
 std::mutex g_mu;
 std::map<int, DevCache> g_dev;
@@ -359,6 +395,35 @@ moba_status ensure_workspace(DevCache* dc, size_t bytes) {
     return MOBA_ERR_NO_MEMORY;
   }
   dc->ws_bytes = sz;
+  return MOBA_OK;
+}
+
+// The device's give-up counter of the dK/dV hand-over wait, zeroed when made.
+moba_status ensure_wait_counter(DevCache* dc) {
+  if (dc->wait_timeouts) return MOBA_OK;
+  void* p = nullptr;
+  if (hipMalloc(&p, kAlign) != hipSuccess) {
+    (void)hipGetLastError();
+    return MOBA_ERR_NO_MEMORY;
+  }
+  if (hipMemset(p, 0, kAlign) != hipSuccess) {
+    (void)hipFree(p);
+    return MOBA_ERR_HIP;
+  }
+  dc->wait_timeouts = static_cast<uint32_t*>(p);
+  return MOBA_OK;
+}
+
+// Reads and clears the give-up counter (synchronous).
+moba_status take_wait_counter(DevCache* dc, uint64_t* count) {
+  *count = 0;
+  if (!dc->wait_timeouts) return MOBA_OK;
+  uint32_t v = 0;
+  if (hipDeviceSynchronize() != hipSuccess ||
+      hipMemcpy(&v, dc->wait_timeouts, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemset(dc->wait_timeouts, 0, sizeof(v)) != hipSuccess)
+    return MOBA_ERR_HIP;
+  *count = v;
   return MOBA_OK;
 }
 
@@ -510,6 +575,53 @@ AttnArgs make_args(const Inputs& in, const View& vo, float* lse) {
 moba_status dense_forward_impl(const Inputs& in, const View& vo, moba_tensor* lse,
                                hipStream_t stream);
 
+// The forward's workspace: a fixed part (block keys, packed V^T, selection,
+// routing lists) and a part per chunk of `nch` kv-heads (the history
+// partials and their lse).
+struct FwdBufs {
+  float* kbar;
+  __hip_bfloat16* vt;
+  int32_t* sel;
+  RouteBuffers rb;
+  void* o_part;
+  float* lse_part;
+};
+
+void forward_layout(const Problem& p, bool bf16, int kk, int nch, Bump* bp, FwdBufs* b) {
+  const int64_t kh = kk - 1;
+  const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;
+  b->kbar = bp->take<float>((int64_t)p.nblk_total * p.Hkv * kHeadDim);
+  b->vt = bf16 ? bp->take<__hip_bfloat16>((int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim) : nullptr;
+  b->sel = bp->take<int32_t>(p.T * p.Hq * kk);
+  b->rb.hist = bp->take<int32_t>((int64_t)p.Hkv * p.hist_words);
+  b->rb.bin_count = bp->take<int32_t>(nbins);
+  b->rb.bin_start = bp->take<int64_t>(nbins + 1);
+  b->rb.bin_tile_start = bp->take<int32_t>(nbins + 1);
+  b->rb.entries = bp->take<uint32_t>(p.hist_entries);
+  const int64_t rows = (int64_t)nch * p.T * p.G;
+  b->o_part = bf16 ? (void*)bp->take<__hip_bfloat16>(rows * kh * kHeadDim)
+                   : (void*)bp->take<float>(rows * kh * kHeadDim);
+  b->lse_part = bp->take<float>(rows * kh);
+}
+
+// Number of blocks and of history selections (route entries) of a batch:
+// sum over sequences of ceil(L / B), and Hq times the sum over tokens of
+// min(topk - 1, c), c the token's block (Eq. 5 keeps min(k - 1, c) past
+// blocks besides the current one).
+void batch_sizes(const std::vector<int32_t>& cu, int B, int topk, int Hq, int64_t* nblk,
+                 int64_t* entries) {
+  int64_t nb = 0, e = 0;
+  for (size_t s = 0; s + 1 < cu.size(); s++) {
+    const int64_t L = (int64_t)cu[s + 1] - cu[s];
+    const int64_t n = ceil_div(L, B);
+    nb += n;
+    for (int64_t c = 0; c < n; c++)
+      e += (std::min<int64_t>(L, (c + 1) * B) - c * B) * std::min<int64_t>(topk - 1, c);
+  }
+  *nblk = nb;
+  *entries = e * Hq;
+}
+
 }  // namespace
 
 // ======================================================================= ABI
@@ -524,7 +636,7 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   if (st != MOBA_OK) return st;
   if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (topk < 1) return MOBA_ERR_TOPK;
-  if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, in.T, stream, &in.cu)) != MOBA_OK) return st;
   if (in.T == 0) return MOBA_OK;
 
   // blocks per sequence and the effective top-k (more than #blocks changes nothing)
@@ -552,37 +664,15 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
     return st;
   const Problem& p = pl->p;
   const int64_t kh = kk - 1;
-  const int64_t TG = p.T * p.G;
-  const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;
 
   // workspace: fixed part, then per-kv-head chunk part
-  auto layout = [&](void* base, int nch, Bump* bp, AttnArgs* a, RouteBuffers* rb, float** kbar,
-                    __hip_bfloat16** vt, int32_t** sel) {
-    *kbar = bp->take<float>((int64_t)p.nblk_total * p.Hkv * kHeadDim);
-    *vt = in.bf16 ? bp->take<__hip_bfloat16>((int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim) : nullptr;
-    *sel = bp->take<int32_t>(p.T * p.Hq * kk);
-    rb->hist = bp->take<int32_t>((int64_t)p.Hkv * p.hist_words);
-    rb->bin_count = bp->take<int32_t>(nbins);
-    rb->bin_start = bp->take<int64_t>(nbins + 1);
-    rb->bin_tile_start = bp->take<int32_t>(nbins + 1);
-    rb->entries = bp->take<uint32_t>(p.hist_entries);
-    const int64_t rows = (int64_t)nch * TG;
-    a->o_part = in.bf16 ? (void*)bp->take<__hip_bfloat16>(rows * kh * kHeadDim)
-                        : (void*)bp->take<float>(rows * kh * kHeadDim);
-    a->lse_part = bp->take<float>(rows * kh);
-    (void)base;
-  };
   const size_t limit = workspace_limit();
   int nch = 0;
   size_t need = 0;
   for (int n = p.Hkv; n >= 1; n--) {
     Bump bp(nullptr);
-    AttnArgs a{};
-    RouteBuffers rb{};
-    float* kb;
-    __hip_bfloat16* vt;
-    int32_t* sel;
-    layout(nullptr, n, &bp, &a, &rb, &kb, &vt, &sel);
+    FwdBufs b{};
+    forward_layout(p, in.bf16, kk, n, &bp, &b);
     if (bp.off + kAlign <= limit) { nch = n; need = bp.off + kAlign; break; }
   }
   if (nch == 0) return MOBA_ERR_NO_MEMORY;
@@ -592,11 +682,14 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
 
   Bump bp(dc->ws);
   AttnArgs a = make_args(in, vo, static_cast<float*>(lse->data));
-  RouteBuffers rb{};
-  float* kbar;
-  __hip_bfloat16* vt;
-  int32_t* sel;
-  layout(dc->ws, nch, &bp, &a, &rb, &kbar, &vt, &sel);
+  FwdBufs fb{};
+  forward_layout(p, in.bf16, kk, nch, &bp, &fb);
+  RouteBuffers rb = fb.rb;
+  float* kbar = fb.kbar;
+  __hip_bfloat16* vt = fb.vt;
+  int32_t* sel = fb.sel;
+  a.o_part = fb.o_part;
+  a.lse_part = fb.lse_part;
   a.vt = vt;
   a.seqs = d_seqs;
   a.bin_tile_start = rb.bin_tile_start;
@@ -672,7 +765,7 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   if (vdo.H != in.Hq || vdq.H != in.Hq || vdk.H != in.Hkv || vdv.H != in.Hkv) return MOBA_ERR_SHAPE;
   if (!dense && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (!dense && topk < 1) return MOBA_ERR_TOPK;
-  if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, in.T, stream, &in.cu)) != MOBA_OK) return st;
   if (in.T == 0) return MOBA_OK;
   if (!dense) {
     // as in the forward: top-k covering every block is full attention
@@ -774,6 +867,16 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   a.nktiles = (int64_t)pl->ktiles.size();
   a.scale = (float)(1.0 / std::sqrt((double)kHeadDim));
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)kHeadDim));
+  if ((st = ensure_wait_counter(dc)) != MOBA_OK) return st;
+  a.wait_timeouts = dc->wait_timeouts;
+  a.spin_limit = kSpinLimit;
+  a.wait_bias = 0;
+  if (env_flag("MOBA_FORCE_WAIT_TIMEOUT")) {
+    // testing aid: every hand-over wait gives up after a few polls (the
+    // kernel still runs to its end; the gradients are then wrong)
+    a.spin_limit = 64;
+    a.wait_bias = 1 << 30;
+  }
 
   // the forward's selection and routing, recomputed
   { Phase ph("pool", stream);
@@ -796,6 +899,12 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   }
   { Phase ph("bwd_dkdv", stream);
     MOBA_LAUNCH(launch_bwd_dkdv(a, p, stream)); }
+  if (debug_sync()) {
+    // the launch above has completed: report a hand-over wait that gave up
+    uint64_t n = 0;
+    if ((st = take_wait_counter(dc, &n)) != MOBA_OK) return st;
+    if (n != 0) return MOBA_ERR_HIP;
+  }
   for (int g0 = 0; g0 < p.Hkv; g0 += nch) {
     a.g0 = g0;
     a.g1 = std::min(p.Hkv, g0 + nch);
@@ -837,7 +946,7 @@ moba_status moba_dense_forward(const moba_tensor* q, const moba_tensor* k, const
   View vo;
   moba_status st = check_inputs(q, k, v, cu_seqlens, out, lse, &in, &vo);
   if (st != MOBA_OK) return st;
-  if ((st = read_cu(cu_seqlens, in.T, &in.cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, in.T, stream, &in.cu)) != MOBA_OK) return st;
   if (in.T == 0) return MOBA_OK;
   return dense_forward_impl(in, vo, lse, stream);
 }
@@ -918,7 +1027,7 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   if (!want_full && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (T >= (int64_t(1) << 31)) return MOBA_ERR_UNSUPPORTED;
   std::vector<int32_t> cu;
-  if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, T, stream, &cu)) != MOBA_OK) return st;
   if (S == 0) return MOBA_OK;
   int64_t lmax = 0;
   for (int64_t s = 0; s < S; s++) {
@@ -1026,7 +1135,7 @@ moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32
   if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
   if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   std::vector<int32_t> cu;
-  if ((st = read_cu(cu_seqlens, k->shape[0], &cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, k->shape[0], stream, &cu)) != MOBA_OK) return st;
   const int Hkv = (int)k->shape[1];
   int64_t nb = 0;
   for (size_t s = 0; s + 1 < cu.size(); s++) nb += ceil_div((int64_t)cu[s + 1] - cu[s], block_size);
@@ -1077,7 +1186,7 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
     nmax = (int)scores->shape[2];
   }
   std::vector<int32_t> cu;
-  if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, T, stream, &cu)) != MOBA_OK) return st;
   if (T == 0) return MOBA_OK;
   int64_t nbmax = 0;
   for (size_t s = 0; s + 1 < cu.size(); s++)
@@ -1128,7 +1237,7 @@ moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, in
   if (topk < 1) return MOBA_ERR_TOPK;
   if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
   std::vector<int32_t> cu;
-  if ((st = read_cu(cu_seqlens, T, &cu)) != MOBA_OK) return st;
+  if ((st = read_cu(cu_seqlens, T, stream, &cu)) != MOBA_OK) return st;
   int64_t nbmax = 0, nb = 0;
   for (size_t s = 0; s + 1 < cu.size(); s++) {
     const int64_t n = ceil_div((int64_t)cu[s + 1] - cu[s], block_size);
@@ -1178,7 +1287,59 @@ moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, in
   return MOBA_OK;
 }
 
-size_t moba_workspace_bytes(void) {
+size_t moba_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv, int32_t D, int64_t nblk_total,
+                            int32_t topk) {
+  if (T < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || Hq / Hkv > kMaxGroup || D != kHeadDim ||
+      nblk_total < 0 || topk < 1)
+    return 0;
+  if (T == 0 || nblk_total == 0) return 0;
+  // bounds over every cu_seqlens with these totals (each non-empty sequence
+  // holds at least one block, and no sequence more than nblk_total)
+  Problem p{};
+  p.T = T;
+  p.Hq = Hq;
+  p.Hkv = Hkv;
+  p.G = Hq / Hkv;
+  p.nblk_total = (int)std::min<int64_t>(nblk_total, INT32_MAX);
+  p.vt_tiles = ceil_div(T, kKeyTile) + nblk_total;
+  p.hist_words = (ceil_div(T, std::max(1, kRouteRows / p.G)) + 1) * nblk_total;
+  const int kk = (int)std::min<int64_t>(topk, nblk_total);
+  p.hist_entries = T * Hq * (int64_t)(kk - 1);
+  size_t need = 0;
+  for (int bf16 = 0; bf16 < 2; bf16++) {
+    Bump bp(nullptr);
+    FwdBufs b{};
+    forward_layout(p, bf16 != 0, kk, Hkv, &bp, &b);
+    need = std::max(need, bp.off + kAlign);
+  }
+  return need;
+}
+
+moba_status moba_route_size(const moba_tensor* cu_seqlens, int32_t block_size, int32_t topk,
+                            int32_t num_q_heads, int64_t* nblk_total, int64_t* entries,
+                            hipStream_t stream) {
+  if (!nblk_total || !entries) return MOBA_ERR_NULL;
+  moba_status st;
+  if ((st = check_cu_desc(cu_seqlens)) != MOBA_OK) return st;
+  if (block_size < 1) return MOBA_ERR_BLOCK_SIZE;
+  if (topk < 1) return MOBA_ERR_TOPK;
+  if (num_q_heads < 1) return MOBA_ERR_SHAPE;
+  std::vector<int32_t> cu;
+  if ((st = fetch_cu(cu_seqlens, stream, &cu)) != MOBA_OK) return st;
+  if ((st = check_cu(cu, cu.back())) != MOBA_OK) return st;  // the batch holds T = cu[S] tokens
+  batch_sizes(cu, block_size, topk, num_q_heads, nblk_total, entries);
+  return MOBA_OK;
+}
+
+moba_status moba_take_wait_timeouts(uint64_t* count) {
+  if (!count) return MOBA_ERR_NULL;
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevCache* dc = cache_for_current_device();
+  if (!dc) return MOBA_ERR_HIP;
+  return take_wait_counter(dc, count);
+}
+
+size_t moba_workspace_held_bytes(void) {
   std::lock_guard<std::mutex> lk(g_mu);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
@@ -1194,6 +1355,7 @@ moba_status moba_release_workspace(void) {
   if (it == g_dev.end()) return MOBA_OK;
   if (hipDeviceSynchronize() != hipSuccess) return MOBA_ERR_HIP;
   if (it->second.ws) (void)hipFree(it->second.ws);
+  if (it->second.wait_timeouts) (void)hipFree(it->second.wait_timeouts);
   for (PlanSlot& sl : it->second.slots) {
     if (sl.tab) (void)hipFree(sl.tab);
     if (sl.stage) (void)hipHostFree(sl.stage);

@@ -31,7 +31,8 @@ def declared_functions():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ["moba_forward", "moba_dense_forward", "moba_pool", "moba_select", "moba_route",
-              "moba_workspace_bytes", "moba_release_workspace", "moba_status_string",
+              "moba_route_size", "moba_workspace_bytes", "moba_workspace_held_bytes",
+              "moba_take_wait_timeouts", "moba_release_workspace", "moba_status_string",
               "moba_profile_enable", "moba_profile_read"]:
         assert n in names
 
@@ -276,3 +277,73 @@ def test_decode_validation(lib):
         t.data = None
     assert c.decode(lib) == "MOBA_OK"  # no sequences: nothing to do
     assert DecCase(S=0, cu=(0,)).decode(lib) == "MOBA_ERR_SEQLENS"  # cache rows no sequence owns
+
+
+# ---------------------------------------------------------------- sizing queries
+def py_route_size(cu, B, topk, hq):
+    nb = e = 0
+    for s in range(len(cu) - 1):
+        L = cu[s + 1] - cu[s]
+        n = (L + B - 1) // B
+        nb += n
+        for c in range(n):
+            e += (min(L, (c + 1) * B) - c * B) * min(topk - 1, c)
+    return nb, e * hq
+
+
+@pytest.mark.parametrize("cu,B,topk,hq", [
+    ((0, 1000, 1000, 1517), 128, 3, 4),
+    ((0, 4096, 16384, 46384, 111920), 1024, 4, 32),
+    ((0, 1048576), 4096, 12, 32),
+    ((0, 7, 9), 1, 5, 2),
+    ((0,), 16, 2, 8),
+    ((0, 300), 64, 40, 1),
+])
+def test_route_size_counts_blocks_and_entries(lib, cu, B, topk, hq):
+    """The number of blocks and of history selections (Eq. 5 keeps min(k-1, c)
+    past blocks besides the current one) as moba_route_size reports them."""
+    nb, e = binding.route_size(torch_cu(cu), B, topk, hq)
+    assert (nb, e) == py_route_size(cu, B, topk, hq)
+
+
+def torch_cu(cu):
+    import torch
+    return torch.tensor(cu, dtype=torch.int32)
+
+
+def test_route_size_validation(lib):
+    r = ctypes.byref
+    nb, e = ctypes.c_int64(), ctypes.c_int64()
+    good = np.array([0, 10, 30], np.int32)
+    dc = desc([3], binding.MOBA_I32, data=good.ctypes.data)
+    assert lib.moba_route_size(r(dc), 4, 2, 1, r(nb), r(e), None) == 0
+    assert lib.moba_route_size(None, 4, 2, 1, r(nb), r(e), None) == 1
+    assert lib.moba_route_size(r(dc), 4, 2, 1, None, r(e), None) == 1
+    assert lib.moba_route_size(r(dc), 0, 2, 1, r(nb), r(e), None) == 5
+    assert lib.moba_route_size(r(dc), 4, 0, 1, r(nb), r(e), None) == 6
+    assert lib.moba_route_size(r(dc), 4, 2, 0, r(nb), r(e), None) == 3
+    bad = np.array([0, 10, 5], np.int32)
+    assert lib.moba_route_size(r(desc([3], binding.MOBA_I32, data=bad.ctypes.data)), 4, 2, 1,
+                               r(nb), r(e), None) == 7
+    assert lib.moba_route_size(r(desc([3], binding.MOBA_F32, data=good.ctypes.data)), 4, 2, 1,
+                               r(nb), r(e), None) == 2
+
+
+def test_workspace_bytes_bounds_the_forward_buffers(lib):
+    """moba_workspace_bytes covers the buffers a one-pass forward must hold:
+    fp32 block keys, the selection, the routing entries, and (f32 inputs)
+    fp32 history partials with their lse, one per history selection; the
+    rest (packed V^T, histograms, bin tables) is small beside them."""
+    for T, hq, hkv, nb, topk in [(1048576, 32, 8, 256, 12), (111920, 32, 32, 110, 4),
+                                 (32768, 32, 8, 16, 3), (1024, 1, 1, 8, 3), (300, 4, 2, 300, 9)]:
+        kk = min(topk, nb)
+        E = T * hq * (kk - 1)
+        core = nb * hkv * 128 * 4 + T * hq * kk * 4 + E * 4 + E * 128 * 4 + E * 4
+        got = lib.moba_workspace_bytes(T, hq, hkv, 128, nb, topk)
+        assert core <= got <= core + T * hkv * 128 * 2 + 4 * (T // 64 + nb) * hkv * 128 * 64 \
+            + 8 * nb * hkv * (T // 128 + 2) + (1 << 20), (T, got, core)
+    assert lib.moba_workspace_bytes(1024, 4, 2, 64, 8, 3) == 0   # D must be 128
+    assert lib.moba_workspace_bytes(1024, 3, 2, 128, 8, 3) == 0  # Hq % Hkv
+    assert lib.moba_workspace_bytes(1024, 4, 2, 128, 8, 0) == 0  # topk < 1
+    assert lib.moba_workspace_bytes(-1, 4, 2, 128, 8, 3) == 0
+    assert lib.moba_workspace_bytes(0, 4, 2, 128, 0, 3) == 0

@@ -105,3 +105,28 @@ def test_dense_backward(seqlens, hq, hkv):
         mean_rel = float(err.mean() / np.abs(ref).mean())
         print("%s: %.2e of (|ref| + c), mean %.2e" % (name, ratio, mean_rel))
         assert ratio <= parity.BWD_ELEM_U and mean_rel <= parity.BWD_MEAN_REL, name
+
+
+def test_wait_give_up_is_reported(monkeypatch):
+    """The dK/dV kernel's bounded hand-over wait, forced from the host to
+    give up on every subtile (every kernel still runs to its end): the
+    give-ups are counted and reported, as MOBA_ERR_HIP under MOBA_DEBUG_SYNC;
+    a normal call afterwards counts none and is correct again."""
+    q, k, v, cu = inputs.make((700, 300), 4, 2, 128, torch.bfloat16, 128, 0.5, 91, device=DEV)
+    out, lse = binding.forward(q, k, v, cu, 128, 3)
+    dout = inputs.make_dout(q.shape, torch.bfloat16, 91, device=DEV)
+    ref = binding.backward(q, k, v, cu, 128, 3, out, lse, dout)
+    assert binding.take_wait_timeouts() == 0
+    monkeypatch.setenv("MOBA_FORCE_WAIT_TIMEOUT", "1")
+    binding.backward(q, k, v, cu, 128, 3, out, lse, dout)
+    assert binding.take_wait_timeouts() > 0
+    monkeypatch.setenv("MOBA_DEBUG_SYNC", "1")
+    with pytest.raises(binding.MobaError) as e:
+        binding.backward(q, k, v, cu, 128, 3, out, lse, dout)
+    assert e.value.name == "MOBA_ERR_HIP"
+    monkeypatch.delenv("MOBA_FORCE_WAIT_TIMEOUT")
+    again = binding.backward(q, k, v, cu, 128, 3, out, lse, dout)
+    monkeypatch.delenv("MOBA_DEBUG_SYNC")
+    assert binding.take_wait_timeouts() == 0
+    for x, y in zip(ref, again):
+        assert torch.equal(x, y)

@@ -221,6 +221,50 @@ def test_device_cu_seqlens():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_device_cu_seqlens_written_on_a_side_stream():
+    """A device cu_seqlens written by work on the caller's (non-default)
+    stream is read after that work: the library copies it on that stream.
+    The offsets are first set to another valid batch, then overwritten on the
+    side stream behind a long matrix product, and the call is made on the
+    side stream without any host synchronization in between."""
+    q, k, v, cu = make((500, 300), 4, 2, torch.bfloat16, 64, seed=31)
+    o1, l1 = binding.forward(q, k, v, cu, 64, 3)
+    decoy = torch.tensor([0, 100, 800], dtype=torch.int32, device=DEV)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        a = torch.randn(8192, 8192, device=DEV)
+        for _ in range(4):
+            a = a @ a * 1e-4
+        decoy.copy_(cu.to(DEV, non_blocking=True) + (a[0, 0] * 0).to(torch.int32))
+        o2, l2 = binding.forward(q, k, v, decoy, 64, 3, stream=side)
+    side.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_workspace_bytes_is_enough_for_one_pass(monkeypatch):
+    """With the workspace cap at moba_workspace_bytes' figure the forward
+    runs its history attention in one pass (one launch per call), and the
+    workspace it holds is within the figure."""
+    seqlens, hq, hkv, B, topk = (3000, 0, 1700), 8, 2, 128, 4
+    q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, seed=43)
+    nb, _ = binding.route_size(cu, B, topk, hq)
+    need = binding.workspace_bytes(q.shape[0], hq, hkv, nb, topk)
+    binding.release_workspace()
+    monkeypatch.setenv("MOBA_WORKSPACE_LIMIT_BYTES", str(need))
+    binding.profile_enable(True)
+    binding.profile_read()
+    o1, l1 = binding.forward(q, k, v, cu, B, topk)
+    ph = binding.profile_read()
+    binding.profile_enable(False)
+    monkeypatch.delenv("MOBA_WORKSPACE_LIMIT_BYTES")
+    assert ph["attn_hist"][0] == 1, ph
+    assert binding.workspace_held_bytes() <= need
+    o2, l2 = binding.forward(q, k, v, cu, B, topk)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
 def test_empty_batch():
     q = torch.empty((0, 4, 128), dtype=torch.bfloat16, device=DEV)
     k = torch.empty((0, 2, 128), dtype=torch.bfloat16, device=DEV)
