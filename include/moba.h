@@ -196,6 +196,33 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
                         moba_tensor* lse, hipStream_t stream);
 
 /*
+ * moba_decode without any allocation, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  Same arguments, conventions and results
+ * as moba_decode (the same kernels; the outputs are bit-identical), except:
+ *   - cu_seqlens must be in host memory (a device pointer returns
+ *     MOBA_ERR_UNSUPPORTED);
+ *   - every intermediate buffer (the per-sequence table, block means when
+ *     kbar is NULL, selections, block lists, partial results) lives in one
+ *     static device array of MOBA_DECODE_NOALLOC_MAX_BYTES bytes, which each
+ *     GPU the library runs on holds from module load until the process ends;
+ *     a call needing more returns MOBA_ERR_NO_MEMORY before enqueueing
+ *     anything (full attention needs about S * Hq * ceil(L_max / 256) * 516
+ *     bytes: a 1M-token cache with 32 query heads fits for one sequence);
+ *   - no library call allocates memory, device or pinned, and no profiling
+ *     events are recorded.
+ * All calls on one GPU share that array and the last call's contents stay
+ * in it: calls whose execution overlaps on one GPU (different streams, or
+ * host threads) race and give wrong results.  Calls on one stream are
+ * ordered and safe.
+ */
+#define MOBA_DECODE_NOALLOC_MAX_BYTES ((size_t)96 << 20)
+moba_status moba_decode_noalloc(const moba_tensor* q, const moba_tensor* k_cache,
+                                const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
+                                const moba_tensor* kbar, int32_t block_size, int32_t topk,
+                                moba_tensor* out, moba_tensor* lse, hipStream_t stream);
+
+/*
  * Block mean-pool of the keys (Eq. 6; Algorithm 1, mean_pool).
  * kbar [nblk_total, Hkv, D] f32 contiguous, device: row b = blk_off[s] + j
  * holds the mean of k over the tokens of block j of sequence s (a short last

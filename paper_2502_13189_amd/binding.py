@@ -62,6 +62,7 @@ def load() -> ctypes.CDLL:
         "moba_backward": [P, P, P, P, i32, i32, P, P, P, P, P, P, vp],
         "moba_dense_backward": [P, P, P, P, P, P, P, P, P, P, vp],
         "moba_decode": [P, P, P, P, P, i32, i32, P, P, vp],
+        "moba_decode_noalloc": [P, P, P, P, P, i32, i32, P, P, vp],
         "moba_dense_forward": [P, P, P, P, P, P, vp],
         "moba_pool": [P, P, i32, P, vp],
         "moba_select": [P, P, P, i32, i32, P, P, vp],
@@ -207,6 +208,23 @@ def decode(q, k_cache, v_cache, cu_seqlens, block_size: int, topk: int, kbar=Non
     _check("moba_decode", lib.moba_decode(_ref(d[0]), _ref(d[1]), _ref(d[2]), _ref(d[3]),
                                           _ref(dkb), int(block_size), int(topk), _ref(do),
                                           _ref(dl), _stream(q, stream)))
+    return out, lse
+
+
+def decode_noalloc(q, k_cache, v_cache, cu_seqlens, block_size: int, topk: int, out, lse,
+                   kbar=None, stream=None):
+    """decode() through moba_decode_noalloc: the library allocates nothing;
+    the caller passes out [S, Hq, 128] bf16 and lse [Hq, S] fp32, and
+    cu_seqlens must be a host tensor."""
+    lib = load()
+    cu = _cu(cu_seqlens)
+    d = [describe(t) for t in (q, k_cache, v_cache, cu)]
+    dkb = describe(kbar) if kbar is not None else None
+    do, dl = describe(out), describe(lse)
+    _check("moba_decode_noalloc", lib.moba_decode_noalloc(_ref(d[0]), _ref(d[1]), _ref(d[2]),
+                                                          _ref(d[3]), _ref(dkb), int(block_size),
+                                                          int(topk), _ref(do), _ref(dl),
+                                                          _stream(q, stream)))
     return out, lse
 
 

@@ -48,7 +48,7 @@ struct Phase {
   PhaseRec rec{};
   bool on = false;
   Phase(const char* name, hipStream_t s) : st(s) {
-    if (!g_prof) return;
+    if (!g_prof || !name) return;
     rec.name = name;
     if (hipEventCreate(&rec.a) != hipSuccess) return;
     if (hipEventCreate(&rec.b) != hipSuccess) { (void)hipEventDestroy(rec.a); return; }
@@ -147,6 +147,15 @@ moba_status check_cu_desc(const moba_tensor* cu) {
   return MOBA_OK;
 }
 
+bool on_device(const void* ptr) {
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
+    (void)hipGetLastError();  // plain host memory
+    return false;
+  }
+  return attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged;
+}
+
 // Pinned staging buffer for cu_seqlens that live on the device.
 std::mutex g_cu_mu;
 int32_t* g_cu_stage = nullptr;
@@ -158,13 +167,7 @@ int64_t g_cu_cap = 0;
 moba_status fetch_cu(const moba_tensor* cu, hipStream_t stream, std::vector<int32_t>* out) {
   const int64_t n = cu->shape[0];
   out->resize(n);
-  hipPointerAttribute_t attr;
-  bool on_device = false;
-  if (hipPointerGetAttributes(&attr, cu->data) == hipSuccess)
-    on_device = attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged;
-  else
-    (void)hipGetLastError();  // plain host memory: clear the lookup error
-  if (on_device) {
+  if (on_device(cu->data)) {
     std::lock_guard<std::mutex> lk(g_cu_mu);
     if (g_cu_cap < n) {
       if (g_cu_stage) (void)hipHostFree(g_cu_stage);
@@ -396,6 +399,50 @@ moba_status ensure_workspace(DevCache* dc, size_t bytes) {
   }
   dc->ws_bytes = sz;
   return MOBA_OK;
+}
+
+// ------------------------------------------------------------- no-alloc scratch
+// moba_decode_noalloc's buffers: a static device array per GPU (held from
+// module load until the process ends).  Host code never passes the array's
+// name to a kernel: its device address is looked up once per device.
+constexpr size_t kNoAllocScratchBytes = MOBA_DECODE_NOALLOC_MAX_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+std::mutex g_na_mu;
+std::map<int, char*> g_na_ptr;  // device -> address of `scratch` on it
+
+moba_status noalloc_scratch(char** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MOBA_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_na_mu);
+  auto it = g_na_ptr.find(dev);
+  if (it == g_na_ptr.end()) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return MOBA_ERR_HIP;
+    }
+    it = g_na_ptr.emplace(dev, static_cast<char*>(p)).first;
+  }
+  *out = it->second;
+  return MOBA_OK;
+}
+
+// Per-sequence tables passed to the device by value (kernel arguments).
+constexpr int kSeqsPerCopy = 32;
+struct SeqBatch {
+  SeqInfo s[kSeqsPerCopy];
+  int32_t n;
+};
+
+__global__ void seq_table_kernel(SeqBatch b, SeqInfo* dst) {
+  const int i = threadIdx.x;
+  if (i < b.n) dst[i] = b.s[i];
+}
+
+hipError_t launch_seq_table(const SeqBatch& b, SeqInfo* dst, hipStream_t st) {
+  seq_table_kernel<<<1, kSeqsPerCopy, 0, st>>>(b, dst);
+  return hipGetLastError();
 }
 
 // The device's give-up counter of the dK/dV hand-over wait, zeroed when made.
@@ -994,14 +1041,14 @@ moba_status dense_forward_impl(const Inputs& in, const View& vo, moba_tensor* ls
   return MOBA_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
+// moba_decode; with `noalloc`, moba_decode_noalloc: the per-shape tables are
+// built on the host and written into the device's static scratch array by
+// kernels that take them as arguments, and the buffers are carved from that
+// array, so nothing is allocated.
+moba_status decode_impl(const moba_tensor* q, const moba_tensor* k_cache,
                         const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
                         const moba_tensor* kbar, int32_t block_size, int32_t topk, moba_tensor* out,
-                        moba_tensor* lse, hipStream_t stream) {
+                        moba_tensor* lse, hipStream_t stream, bool noalloc) {
   if (missing(q) || missing(k_cache) || missing(v_cache) || missing(out) || missing(lse) ||
       !cu_seqlens || !cu_seqlens->data)
     return MOBA_ERR_NULL;
@@ -1027,6 +1074,7 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   if (!want_full && block_size < 1) return MOBA_ERR_BLOCK_SIZE;
   if (T >= (int64_t(1) << 31)) return MOBA_ERR_UNSUPPORTED;
   std::vector<int32_t> cu;
+  if (noalloc && on_device(cu_seqlens->data)) return MOBA_ERR_UNSUPPORTED;
   if ((st = read_cu(cu_seqlens, T, stream, &cu)) != MOBA_OK) return st;
   if (S == 0) return MOBA_OK;
   int64_t lmax = 0;
@@ -1048,15 +1096,25 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
     if ((st = check_contig(kbar, MOBA_F32, 3, ks)) != MOBA_OK) return st;
   }
 
-  std::lock_guard<std::mutex> lk(g_mu);
-  DevCache* dc = cache_for_current_device();
-  if (!dc) return MOBA_ERR_HIP;
+  std::unique_lock<std::mutex> lk(g_mu, std::defer_lock);
+  DevCache* dc = nullptr;
   const Plan* pl;
-  const SeqInfo* d_seqs;
-  const CausalTile* d_tiles;
-  if ((st = get_plan(dc, stream, cu, Hkv, Hkv, B, kk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
-                     &d_tiles)) != MOBA_OK)
-    return st;
+  Plan own_plan;
+  const SeqInfo* d_seqs = nullptr;
+  char* scratch_base = nullptr;
+  if (noalloc) {
+    if ((st = noalloc_scratch(&scratch_base)) != MOBA_OK) return st;
+    build_plan(cu, Hkv, Hkv, B, kk, kTilesNone, kTileRowsMfma, &own_plan);
+    pl = &own_plan;
+  } else {
+    lk.lock();
+    dc = cache_for_current_device();
+    if (!dc) return MOBA_ERR_HIP;
+    const CausalTile* d_tiles;
+    if ((st = get_plan(dc, stream, cu, Hkv, Hkv, B, kk, kTilesNone, kTileRowsMfma, &pl, &d_seqs,
+                       &d_tiles)) != MOBA_OK)
+      return st;
+  }
   Problem p = pl->p;
   p.S = (int)S;
   p.Hq = Hq;
@@ -1074,6 +1132,7 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   const int split_len = (int)ceil_div(nslot, nsplit);
   auto layout = [&](Bump* bp, float** kb, int32_t** sel, int32_t** blk, float** po, float** pls,
                     float** mid) {
+    if (noalloc) d_seqs = bp->take<SeqInfo>(S);  // the tables, first
     *kb = bp->take<float>(own_kbar ? (int64_t)p.nblk_total * Hkv * kHeadDim : 0);
     *sel = bp->take<int32_t>(full ? 0 : S * Hq * kk);
     *blk = bp->take<int32_t>(S * Hkv * nunion);
@@ -1086,13 +1145,27 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
     float *a0, *a2, *a3, *a5;
     int32_t *a1, *a4;
     layout(&sz, &a0, &a1, &a4, &a2, &a3, &a5);
-    if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
-    if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
+    if (noalloc) {
+      if (sz.off > kNoAllocScratchBytes) return MOBA_ERR_NO_MEMORY;
+    } else {
+      if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
+      if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
+    }
   }
-  Bump bp(dc->ws);
+  Bump bp(noalloc ? static_cast<void*>(scratch_base) : dc->ws);
   DecodeArgs a{};
   float* kb_ws;
   layout(&bp, &kb_ws, &a.sel, &a.blocks, &a.part_o, &a.part_lse, &a.mid);
+  if (noalloc) {
+    // the per-sequence table, written by kernels that receive it by value
+    SeqInfo* dst = const_cast<SeqInfo*>(d_seqs);
+    for (int64_t s0 = 0; s0 < S; s0 += kSeqsPerCopy) {
+      SeqBatch b{};
+      b.n = (int32_t)std::min<int64_t>(kSeqsPerCopy, S - s0);
+      for (int i = 0; i < b.n; i++) b.s[i] = pl->seqs[s0 + i];
+      MOBA_LAUNCH(launch_seq_table(b, dst + s0, stream));
+    }
+  }
   a.nsplit = nsplit;
   a.split_len = split_len;
   a.nunion = nunion;
@@ -1108,21 +1181,43 @@ moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
   a.chunk_block = B;
   a.full = full ? 1 : 0;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)kHeadDim));
+  // (the no-alloc path records no profiling events)
   if (own_kbar) {
-    Phase ph("pool", stream);
+    Phase ph(noalloc ? nullptr : "pool", stream);
     MOBA_LAUNCH(launch_pool(vk.data, true, vk.st, vk.sh, d_seqs, p, kb_ws, stream));
   }
   if (!full) {
-    { Phase ph("decode_gate", stream);
+    { Phase ph(noalloc ? nullptr : "decode_gate", stream);
       MOBA_LAUNCH(launch_decode_gate(a, p, stream)); }
-    Phase ph("decode_plan", stream);
+    Phase ph(noalloc ? nullptr : "decode_plan", stream);
     MOBA_LAUNCH(launch_decode_plan(a, p, stream));
   }
-  { Phase ph("decode_attend", stream);
+  { Phase ph(noalloc ? nullptr : "decode_attend", stream);
     MOBA_LAUNCH(launch_decode_attend(a, p, stream)); }
-  { Phase ph("decode_combine", stream);
+  { Phase ph(noalloc ? nullptr : "decode_combine", stream);
     MOBA_LAUNCH(launch_decode_combine(a, p, stream)); }
   return MOBA_OK;
+}
+
+
+}  // namespace
+
+extern "C" {
+
+moba_status moba_decode(const moba_tensor* q, const moba_tensor* k_cache,
+                        const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
+                        const moba_tensor* kbar, int32_t block_size, int32_t topk, moba_tensor* out,
+                        moba_tensor* lse, hipStream_t stream) {
+  return decode_impl(q, k_cache, v_cache, cu_seqlens, kbar, block_size, topk, out, lse, stream,
+                     false);
+}
+
+moba_status moba_decode_noalloc(const moba_tensor* q, const moba_tensor* k_cache,
+                                const moba_tensor* v_cache, const moba_tensor* cu_seqlens,
+                                const moba_tensor* kbar, int32_t block_size, int32_t topk,
+                                moba_tensor* out, moba_tensor* lse, hipStream_t stream) {
+  return decode_impl(q, k_cache, v_cache, cu_seqlens, kbar, block_size, topk, out, lse, stream,
+                     true);
 }
 
 moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32_t block_size,
