@@ -13,12 +13,15 @@
 // bf16 queries: the scores come from the matrix cores.  Each fp32 block key
 // is split exactly into three bf16 terms, kbar = hi + mid + lo (each term
 // takes the next 8 significant bits, so the sum carries at least 24 and the
-// remainder is below 2^-26 |kbar|); a bf16 query element times a term is exact
-// in fp32, so s_j = <q, hi> + <q, mid> + <q, lo> is an fp32-accumulated dot
-// product of the exact operands.  Per chunk of 32 blocks a wave computes
-// S^T (blocks x queries) for its 64 rows with v_mfma_f32_32x32x16_bf16
-// (3 terms x 8 k-steps per 32 rows), passes the tile through LDS so that each
-// lane holds its own row's 32 scores, and inserts them in block order.
+// remainder is below 2^-26 |kbar|; the pool kernel writes the three planes);
+// a bf16 query element times a term is exact in fp32, so
+// s_j = <q, hi> + <q, mid> + <q, lo> is an fp32-accumulated dot product of
+// the exact operands.  Per chunk of 32 blocks a wave computes S^T (blocks x
+// queries) for its 64 rows with v_mfma_f32_32x32x16_bf16 (3 terms x 8
+// k-steps per 32 rows; the next chunk's terms are fetched meanwhile),
+// passes the tile through LDS so that each lane holds its own row's 32
+// scores, and inserts them in block order, compared as orderable integer
+// keys of the fp32 scores.
 //
 // fp32 queries: s_j = <q, kbar_j> on the VALU in fp32 with four interleaved
 // partial sums combined pairwise, block keys broadcast from LDS.
@@ -175,10 +178,39 @@ constexpr int kChunk = 32;               // blocks per matrix tile
 constexpr int kTermRow = kHeadDim + 8;   // bf16 per LDS row of a block-key term (272 B)
 constexpr int kScoreRow = kChunk + 4;    // floats per LDS score row (144 B)
 
+// Orderable integer key of an fp32 score: k(a) < k(b) iff a < b (ties only
+// for equal values; -0 is first made +0).
+__device__ __forceinline__ int32_t score_key(float f) {
+  const int32_t b = __float_as_int(f + 0.0f);
+  return b ^ ((b >> 31) & 0x7fffffff);
+}
+
+// Sorted insertion of block j with key kj into (lk, li) (see the header).
+// The newcomer goes below every entry with a key >= its own (an equal key
+// stays below the earlier, lower-index entry): with gt[x] = kj > lk[x] (a
+// suffix of the list), place x takes place x-1's entry where gt[x-1], the
+// newcomer where only gt[x], and keeps its own entry otherwise; the bottom
+// entry drops out.  Places are rewritten from the bottom up, in place.
+template <int KM>
+__device__ __forceinline__ void insert_key(int32_t (&lk)[KM], int (&li)[KM], int32_t kj, int j) {
+  bool gt[KM];
+#pragma unroll
+  for (int x = 0; x < KM; x++) gt[x] = kj > lk[x];
+#pragma unroll
+  for (int x = KM - 1; x >= 1; x--) {
+    const int32_t ak = gt[x - 1] ? lk[x - 1] : kj;
+    const int ai = gt[x - 1] ? li[x - 1] : j;
+    lk[x] = gt[x] ? ak : lk[x];
+    li[x] = gt[x] ? ai : li[x];
+  }
+  lk[0] = gt[0] ? kj : lk[0];
+  li[0] = gt[0] ? j : li[0];
+}
+
 template <int KM>
 __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __restrict__ q,
                                                         int64_t q_st, int64_t q_sh,
-                                                        const float* __restrict__ kbar,
+                                                        const __hip_bfloat16* __restrict__ kterm,
                                                         const SeqInfo* __restrict__ seqs, Problem p,
                                                         int32_t* __restrict__ sel,
                                                         float* __restrict__ scores, int nmax) {
@@ -206,14 +238,13 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
     for (int j = 0; j < nmax; j++) scores[row * nmax + j] = j < c ? 0.0f : NAN;
   }
 
-  float sc[KM > 0 ? KM : 1];
-  int id[KM > 0 ? KM : 1];
+  int32_t lk[KM > 0 ? KM : 1];
+  int li[KM > 0 ? KM : 1];
   if constexpr (KM > 0) {
 #pragma unroll
     for (int x = 0; x < KM; x++) {
-      const bool blocked = x < KM - (K - 1);
-      sc[x] = blocked ? INFINITY : -INFINITY;
-      id[x] = 0x7fffffff;
+      lk[x] = x < KM - (K - 1) ? INT32_MAX : INT32_MIN;
+      li[x] = 0x7fffffff;
     }
   }
   const bool need_scores = KM > 0 || scores != nullptr;
@@ -233,42 +264,31 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
         qf[set][kk] = vb ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qr + 16 * kk))
                          : bf16x8{};
     }
-    const float4* kb4 = reinterpret_cast<const float4*>(kbar);
-    // staging: thread -> block jb of the chunk, dims d0 .. d0 + 15
+    // staging: thread -> block jb of the chunk, dims d0 .. d0 + 15 of each of
+    // the three terms (two 16-byte pieces per term), fetched one chunk ahead
     const int jb = threadIdx.x >> 3, d0 = 16 * (threadIdx.x & 7);
+    const int64_t plane = (int64_t)p.nblk_total * p.Hkv * kHeadDim;
+    u32x4 pf[3][2];
+    auto fetch = [&](int jc) {
+      const int j = jc + jb;
+      const bool in = j < sq.nblk;
+      const __hip_bfloat16* src =
+          kterm + (((int64_t)sq.blk_off + (in ? j : 0)) * p.Hkv + g) * kHeadDim + d0;
+#pragma unroll
+      for (int m = 0; m < 3; m++)
+#pragma unroll
+        for (int h2 = 0; h2 < 2; h2++)
+          pf[m][h2] = in ? *reinterpret_cast<const u32x4*>(src + m * plane + 8 * h2) : u32x4{};
+    };
+    fetch(0);
     for (int jc = 0; jc < cmax; jc += kChunk) {
       __syncthreads();  // previous chunk's terms are no longer read
-      {
-        float x[16];
-        const int j = jc + jb;
-        if (j < sq.nblk) {
-          const float4* src = kb4 + (((int64_t)sq.blk_off + j) * p.Hkv + g) * (kHeadDim / 4) + d0 / 4;
 #pragma unroll
-          for (int v = 0; v < 4; v++) {
-            const float4 f = src[v];
-            x[4 * v] = f.x; x[4 * v + 1] = f.y; x[4 * v + 2] = f.z; x[4 * v + 3] = f.w;
-          }
-        } else {
+      for (int m = 0; m < 3; m++)
 #pragma unroll
-          for (int e = 0; e < 16; e++) x[e] = 0.0f;
-        }
-        bf16x8 t[3][2];
-#pragma unroll
-        for (int e = 0; e < 16; e++) {
-          const __bf16 hi = (__bf16)x[e];
-          const float r1 = x[e] - (float)hi;
-          const __bf16 mid = (__bf16)r1;
-          const __bf16 lo = (__bf16)(r1 - (float)mid);
-          t[0][e >> 3][e & 7] = hi;
-          t[1][e >> 3][e & 7] = mid;
-          t[2][e >> 3][e & 7] = lo;
-        }
-#pragma unroll
-        for (int m = 0; m < 3; m++)
-#pragma unroll
-          for (int h2 = 0; h2 < 2; h2++)
-            *reinterpret_cast<bf16x8*>(&terms[m][jb][d0 + 8 * h2]) = t[m][h2];
-      }
+        for (int h2 = 0; h2 < 2; h2++)
+          *reinterpret_cast<u32x4*>(&terms[m][jb][d0 + 8 * h2]) = pf[m][h2];
+      if (jc + kChunk < cmax) fetch(jc + kChunk);  // lands during this chunk's products
       __syncthreads();
 #pragma unroll
       for (int set = 0; set < 2; set++) {
@@ -296,47 +316,49 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
         }
       }
       __builtin_amdgcn_wave_barrier();
-      // this lane's row: 32 scores in block order.  Only scores above the
+      // this lane's row: 32 scores in block order.  Only keys above the
       // list's last entry at the chunk start can enter it (the last entry
-      // only rises, and an equal later score never displaces an earlier
-      // one), so those are marked and inserted in block order; the other
+      // only rises, and an equal later key never displaces an earlier one),
+      // so those are marked and inserted in block order; the other
       // insertions would leave the list unchanged.
       const int jend = min(kChunk, c - jc);  // blocks from c on never enter
+      const uint32_t live = jend >= kChunk ? ~0u : (jend <= 0 ? 0u : (1u << jend) - 1u);
       uint32_t msk = 0;
-      const float thr = KM > 0 ? sc[KM > 0 ? KM - 1 : 0] : INFINITY;
+      const int32_t thr = KM > 0 ? lk[KM > 0 ? KM - 1 : 0] : INT32_MAX;
 #pragma unroll
       for (int b4 = 0; b4 < kChunk / 4; b4++) {
         const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
         const float f[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int e = 0; e < 4; e++) {
-          const int b = 4 * b4 + e;
-          if (scores && b < jend && jc + b < nmax) scores[row * nmax + jc + b] = f[e];
-          if (b < jend && f[e] > thr) msk |= 1u << b;
-        }
+        for (int e = 0; e < 4; e++)
+          if (KM > 0) msk |= (uint32_t)(score_key(f[e]) > thr) << (4 * b4 + e);
+      }
+      msk &= live;
+      if (scores) {  // debugging aid: the fp32 scores of this row's past blocks
+        for (int b = 0; b < jend && jc + b < nmax; b++) scores[row * nmax + jc + b] = st[wave][lane][b];
       }
       if constexpr (KM > 0) {
         while (msk) {
           const int b = __builtin_ctz(msk);
           msk &= msk - 1;
-          insert_top<KM>(sc, id, st[wave][lane][b], jc + b);
+          insert_key<KM>(lk, li, score_key(st[wave][lane][b]), jc + b);
         }
       }
       __builtin_amdgcn_wave_barrier();
     }
   }
   if (!valid) return;
-  write_sel<KM>(sel + row * K, id, c, K);
+  write_sel<KM>(sel + row * K, li, c, K);
 }
 
 template <typename T, int KM>
 hipError_t launch_km(const void* q, int64_t q_st, int64_t q_sh, const float* kbar,
-                     const SeqInfo* seqs, const Problem& p, int32_t* sel, float* scores, int nmax,
-                     hipStream_t st) {
+                     const __hip_bfloat16* kterm, const SeqInfo* seqs, const Problem& p,
+                     int32_t* sel, float* scores, int nmax, hipStream_t st) {
   dim3 grid((unsigned)p.gate_groups, p.Hkv);
   if constexpr (std::is_same<T, __hip_bfloat16>::value)
-    gate_mfma_kernel<KM><<<grid, 256, 0, st>>>(static_cast<const T*>(q), q_st, q_sh, kbar, seqs, p,
-                                               sel, scores, nmax);
+    gate_mfma_kernel<KM><<<grid, 256, 0, st>>>(static_cast<const T*>(q), q_st, q_sh, kterm, seqs,
+                                               p, sel, scores, nmax);
   else
     gate_kernel<T, KM><<<grid, 256, 0, st>>>(static_cast<const T*>(q), q_st, q_sh, kbar, seqs, p,
                                              sel, scores, nmax);
@@ -345,10 +367,10 @@ hipError_t launch_km(const void* q, int64_t q_st, int64_t q_sh, const float* kba
 
 template <typename T>
 hipError_t launch_typed(const void* q, int64_t q_st, int64_t q_sh, const float* kbar,
-                        const SeqInfo* seqs, const Problem& p, int32_t* sel, float* scores,
-                        int nmax, hipStream_t st) {
+                        const __hip_bfloat16* kterm, const SeqInfo* seqs, const Problem& p,
+                        int32_t* sel, float* scores, int nmax, hipStream_t st) {
   const int kh = p.topk - 1;
-#define MOBA_GATE_KM(n) launch_km<T, n>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st)
+#define MOBA_GATE_KM(n) launch_km<T, n>(q, q_st, q_sh, kbar, kterm, seqs, p, sel, scores, nmax, st)
   if (kh >= p.nblk_max - 1) return MOBA_GATE_KM(0);
   if (kh <= 1) return MOBA_GATE_KM(1);
   if (kh <= 3) return MOBA_GATE_KM(3);
@@ -363,11 +385,12 @@ hipError_t launch_typed(const void* q, int64_t q_st, int64_t q_sh, const float* 
 }  // namespace
 
 hipError_t launch_gate(const void* q, bool bf16, int64_t q_st, int64_t q_sh, const float* kbar,
-                       const SeqInfo* seqs, const Problem& p, int32_t* sel, float* scores,
-                       int nmax, hipStream_t st) {
+                       const __hip_bfloat16* kterm, const SeqInfo* seqs, const Problem& p,
+                       int32_t* sel, float* scores, int nmax, hipStream_t st) {
   if (p.gate_groups == 0) return hipSuccess;
-  if (bf16) return launch_typed<__hip_bfloat16>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
-  return launch_typed<float>(q, q_st, q_sh, kbar, seqs, p, sel, scores, nmax, st);
+  if (bf16)
+    return launch_typed<__hip_bfloat16>(q, q_st, q_sh, kbar, kterm, seqs, p, sel, scores, nmax, st);
+  return launch_typed<float>(q, q_st, q_sh, kbar, nullptr, seqs, p, sel, scores, nmax, st);
 }
 
 }  // namespace moba

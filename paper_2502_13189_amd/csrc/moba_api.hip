@@ -627,6 +627,7 @@ moba_status dense_forward_impl(const Inputs& in, const View& vo, moba_tensor* ls
 // partials and their lse).
 struct FwdBufs {
   float* kbar;
+  __hip_bfloat16* kterm;  // bf16 path: the three exact bf16 planes of kbar
   __hip_bfloat16* vt;
   int32_t* sel;
   RouteBuffers rb;
@@ -638,6 +639,7 @@ void forward_layout(const Problem& p, bool bf16, int kk, int nch, Bump* bp, FwdB
   const int64_t kh = kk - 1;
   const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;
   b->kbar = bp->take<float>((int64_t)p.nblk_total * p.Hkv * kHeadDim);
+  b->kterm = bf16 ? bp->take<__hip_bfloat16>((int64_t)3 * p.nblk_total * p.Hkv * kHeadDim) : nullptr;
   b->vt = bf16 ? bp->take<__hip_bfloat16>((int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim) : nullptr;
   b->sel = bp->take<int32_t>(p.T * p.Hq * kk);
   b->rb.hist = bp->take<int32_t>((int64_t)p.Hkv * p.hist_words);
@@ -747,14 +749,16 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   a.ntiles = (int64_t)pl->tiles.size();
 
   { Phase ph("pool", stream);
-    MOBA_LAUNCH(launch_pool(in.k.data, in.bf16, in.k.st, in.k.sh, d_seqs, p, kbar, stream)); }
+    MOBA_LAUNCH(launch_pool(in.k.data, in.bf16, in.k.st, in.k.sh, d_seqs, p, kbar, fb.kterm,
+                            stream)); }
   if (in.bf16) {
     Phase ph("vt_pack", stream);
     MOBA_LAUNCH(launch_vt_pack(static_cast<const __hip_bfloat16*>(in.v.data), in.v.st, in.v.sh,
                                d_seqs, p, vt, stream));
   }
   { Phase ph("gate", stream);
-    MOBA_LAUNCH(launch_gate(in.q.data, in.bf16, in.q.st, in.q.sh, kbar, d_seqs, p, sel, nullptr, 0,
+    MOBA_LAUNCH(launch_gate(in.q.data, in.bf16, in.q.st, in.q.sh, kbar, fb.kterm, d_seqs, p, sel,
+                            nullptr, 0,
                             stream)); }
   if (kh > 0 && p.hist_entries > 0) {
     Phase ph("route", stream);
@@ -855,11 +859,13 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   const bool routed = kh > 0 && p.hist_entries > 0;
 
   struct Bufs {
-    float* kbar; __hip_bfloat16* kt; int32_t* sel; RouteBuffers rb; float2* ld; int4* rec;
+    float* kbar; __hip_bfloat16* kterm; __hip_bfloat16* kt; int32_t* sel; RouteBuffers rb;
+    float2* ld; int4* rec;
     float* dq_part;
   };
   auto layout = [&](int nch, Bump* bp, Bufs* b) {
     b->kbar = bp->take<float>((int64_t)p.nblk_total * p.Hkv * kHeadDim);
+    b->kterm = bp->take<__hip_bfloat16>((int64_t)3 * p.nblk_total * p.Hkv * kHeadDim);
     b->kt = bp->take<__hip_bfloat16>((int64_t)p.Hkv * p.vt_tiles * kKeyTile * kHeadDim);
     b->sel = bp->take<int32_t>(p.T * p.Hq * kk);
     b->rb.hist = bp->take<int32_t>((int64_t)p.Hkv * p.hist_words);
@@ -927,12 +933,14 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
 
   // the forward's selection and routing, recomputed
   { Phase ph("pool", stream);
-    MOBA_LAUNCH(launch_pool(in.k.data, true, in.k.st, in.k.sh, d_seqs, p, b.kbar, stream)); }
+    MOBA_LAUNCH(launch_pool(in.k.data, true, in.k.st, in.k.sh, d_seqs, p, b.kbar, b.kterm,
+                            stream)); }
   { Phase ph("kt_pack", stream);
     MOBA_LAUNCH(launch_vt_pack(static_cast<const __hip_bfloat16*>(in.k.data), in.k.st, in.k.sh,
                                d_seqs, p, b.kt, stream)); }
   { Phase ph("gate", stream);
-    MOBA_LAUNCH(launch_gate(in.q.data, true, in.q.st, in.q.sh, b.kbar, d_seqs, p, b.sel, nullptr, 0,
+    MOBA_LAUNCH(launch_gate(in.q.data, true, in.q.st, in.q.sh, b.kbar, b.kterm, d_seqs, p, b.sel,
+                            nullptr, 0,
                             stream)); }
   if (routed) {
     Phase ph("route", stream);
@@ -1184,7 +1192,7 @@ moba_status decode_impl(const moba_tensor* q, const moba_tensor* k_cache,
   // (the no-alloc path records no profiling events)
   if (own_kbar) {
     Phase ph(noalloc ? nullptr : "pool", stream);
-    MOBA_LAUNCH(launch_pool(vk.data, true, vk.st, vk.sh, d_seqs, p, kb_ws, stream));
+    MOBA_LAUNCH(launch_pool(vk.data, true, vk.st, vk.sh, d_seqs, p, kb_ws, nullptr, stream));
   }
   if (!full) {
     { Phase ph(noalloc ? nullptr : "decode_gate", stream);
@@ -1248,7 +1256,7 @@ moba_status moba_pool(const moba_tensor* k, const moba_tensor* cu_seqlens, int32
     return st;
   Phase ph("pool", stream);
   MOBA_LAUNCH(launch_pool(vk.data, k->dtype == MOBA_BF16, vk.st, vk.sh, d_seqs, pl->p,
-                          static_cast<float*>(kbar->data), stream));
+                          static_cast<float*>(kbar->data), nullptr, stream));
   return MOBA_OK;
 }
 
@@ -1297,16 +1305,20 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
                       &d_tiles)) != MOBA_OK)
     return st;
   const Problem& p = pl->p;
+  const bool bf16 = q->dtype == MOBA_BF16;
+  const int64_t nkb = (int64_t)p.nblk_total * Hkv * kHeadDim;
   Bump sz(nullptr);
-  sz.take<float>((int64_t)p.nblk_total * Hkv * kHeadDim);
+  sz.take<float>(nkb);
+  sz.take<__hip_bfloat16>(bf16 ? 3 * nkb : 0);
   if (sz.off + kAlign > workspace_limit()) return MOBA_ERR_NO_MEMORY;
   if ((st = ensure_workspace(dc, sz.off + kAlign)) != MOBA_OK) return st;
   Bump bp(dc->ws);
-  float* kbar = bp.take<float>((int64_t)p.nblk_total * Hkv * kHeadDim);
+  float* kbar = bp.take<float>(nkb);
+  __hip_bfloat16* kterm = bf16 ? bp.take<__hip_bfloat16>(3 * nkb) : nullptr;
   { Phase ph("pool", stream);
-    MOBA_LAUNCH(launch_pool(vk.data, q->dtype == MOBA_BF16, vk.st, vk.sh, d_seqs, p, kbar, stream)); }
+    MOBA_LAUNCH(launch_pool(vk.data, bf16, vk.st, vk.sh, d_seqs, p, kbar, kterm, stream)); }
   { Phase ph("gate", stream);
-    MOBA_LAUNCH(launch_gate(vq.data, q->dtype == MOBA_BF16, vq.st, vq.sh, kbar, d_seqs, p,
+    MOBA_LAUNCH(launch_gate(vq.data, bf16, vq.st, vq.sh, kbar, kterm, d_seqs, p,
                             static_cast<int32_t*>(sel->data),
                             scores ? static_cast<float*>(scores->data) : nullptr, nmax, stream)); }
   return MOBA_OK;
@@ -1397,8 +1409,8 @@ size_t moba_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv, int32_t D, int64
   p.G = Hq / Hkv;
   p.nblk_total = (int)std::min<int64_t>(nblk_total, INT32_MAX);
   p.vt_tiles = ceil_div(T, kKeyTile) + nblk_total;
-  p.hist_words = (ceil_div(T, std::max(1, kRouteRows / p.G)) + 1) * nblk_total;
   const int kk = (int)std::min<int64_t>(topk, nblk_total);
+  p.hist_words = (ceil_div(T, std::max(1, kRouteRows / p.G)) + 1) * nblk_total;
   p.hist_entries = T * Hq * (int64_t)(kk - 1);
   size_t need = 0;
   for (int bf16 = 0; bf16 < 2; bf16++) {

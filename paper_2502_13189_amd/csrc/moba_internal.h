@@ -13,7 +13,7 @@ constexpr int kTileRowsMfma = 256;  // query rows per bf16 (matrix-core) attenti
 constexpr int kTileRowsF32 = 128;   // query rows per fp32 attention work-group
 constexpr int kMaxGroup = 128;      // largest Hq / Hkv
 constexpr int kMaxBlocksPerSeq = 4096;  // limit of the routing kernels' LDS tables
-constexpr int kRouteRows = 4096;  // rows handled by one routing work-group
+constexpr int kRouteRows = 1024;  // rows (tokens x query heads of a group) per routing chunk
 
 // Per-sequence bookkeeping, built on the host and uploaded once per shape.
 struct SeqInfo {
@@ -53,18 +53,22 @@ struct Problem {
 
 // ---------------------------------------------------------------- launches
 // Every launcher enqueues on `st` and returns the launch status.
+// kterm (nullable): also the three exact bf16 planes of kbar (hi, mid, lo;
+// each [nblk_total, Hkv, D]) that the bf16 gate reads.
 hipError_t launch_pool(const void* k, bool bf16, int64_t k_st, int64_t k_sh, const SeqInfo* seqs,
-                       const Problem& p, float* kbar, hipStream_t st);
+                       const Problem& p, float* kbar, __hip_bfloat16* kterm, hipStream_t st);
 
 hipError_t launch_vt_pack(const __hip_bfloat16* v, int64_t v_st, int64_t v_sh, const SeqInfo* seqs,
                           const Problem& p, __hip_bfloat16* vt, hipStream_t st);
 
+// bf16 queries read kterm (from launch_pool), fp32 queries kbar.
 hipError_t launch_gate(const void* q, bool bf16, int64_t q_st, int64_t q_sh, const float* kbar,
-                       const SeqInfo* seqs, const Problem& p, int32_t* sel, float* scores,
-                       int nmax, hipStream_t st);
+                       const __hip_bfloat16* kterm, const SeqInfo* seqs, const Problem& p,
+                       int32_t* sel, float* scores, int nmax, hipStream_t st);
 
 struct RouteBuffers {
-  int32_t* hist;            // [Hkv * hist_words] per-chunk counts, then per-chunk exclusive offsets
+  int32_t* hist;            // [Hkv * hist_words]: per sequence, per block a column over the
+                            // sequence's chunks: counts, then exclusive offsets
   int32_t* bin_count;       // [Hkv * nblk_total]
   int64_t* bin_start;       // [Hkv * nblk_total + 1]
   int32_t* bin_tile_start;  // [Hkv * nblk_total + 1] tiles of tile_rows entries

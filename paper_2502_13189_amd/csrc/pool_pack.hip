@@ -45,10 +45,14 @@ struct Load8<float> {
   }
 };
 
+// kterm (nullable): the block keys split exactly into three bf16 planes,
+// kbar = hi + mid + lo, each plane [nblk_total, Hkv, D] (read by the
+// matrix-core gate).
 template <typename T>
 __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ k, int64_t k_st, int64_t k_sh,
                                                    const SeqInfo* __restrict__ seqs, int S, int B,
-                                                   int Hkv, float* __restrict__ kbar) {
+                                                   int Hkv, int nblk_total, float* __restrict__ kbar,
+                                                   __hip_bfloat16* __restrict__ kterm) {
   __shared__ double red[16][kHeadDim];
   const int b = blockIdx.x;
   const int g = blockIdx.y;
@@ -75,7 +79,18 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ k, int6
     double sum = 0.0;
 #pragma unroll
     for (int r = 0; r < 16; r++) sum += red[r][threadIdx.x];
-    kbar[((int64_t)b * Hkv + g) * kHeadDim + threadIdx.x] = (float)(sum / (double)(t1 - t0));
+    const float m = (float)(sum / (double)(t1 - t0));
+    const int64_t o = ((int64_t)b * Hkv + g) * kHeadDim + threadIdx.x;
+    kbar[o] = m;
+    if (kterm) {
+      const int64_t plane = (int64_t)nblk_total * Hkv * kHeadDim;
+      const __hip_bfloat16 hi = __float2bfloat16(m);
+      const float r1 = m - __bfloat162float(hi);
+      const __hip_bfloat16 mid = __float2bfloat16(r1);
+      kterm[o] = hi;
+      kterm[o + plane] = mid;
+      kterm[o + 2 * plane] = __float2bfloat16(r1 - __bfloat162float(mid));
+    }
   }
 }
 
@@ -134,15 +149,16 @@ __global__ __launch_bounds__(256) void vt_pack_kernel(const __hip_bfloat16* __re
 }  // namespace
 
 hipError_t launch_pool(const void* k, bool bf16, int64_t k_st, int64_t k_sh, const SeqInfo* seqs,
-                       const Problem& p, float* kbar, hipStream_t st) {
+                       const Problem& p, float* kbar, __hip_bfloat16* kterm, hipStream_t st) {
   if (p.nblk_total == 0) return hipSuccess;
   dim3 grid(p.nblk_total, p.Hkv);
   if (bf16)
     pool_kernel<__hip_bfloat16><<<grid, 256, 0, st>>>(
-        static_cast<const __hip_bfloat16*>(k), k_st, k_sh, seqs, p.S, p.B, p.Hkv, kbar);
+        static_cast<const __hip_bfloat16*>(k), k_st, k_sh, seqs, p.S, p.B, p.Hkv, p.nblk_total,
+        kbar, kterm);
   else
     pool_kernel<float><<<grid, 256, 0, st>>>(static_cast<const float*>(k), k_st, k_sh, seqs, p.S,
-                                             p.B, p.Hkv, kbar);
+                                             p.B, p.Hkv, p.nblk_total, kbar, kterm);
   return hipGetLastError();
 }
 

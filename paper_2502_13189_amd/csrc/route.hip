@@ -7,17 +7,24 @@
 //
 // Rows of kv-head g are ordered r = g*T*G + t*G + hl (hl = query head within
 // the GQA group).  Rows are cut into chunks of `route_rt` tokens x G heads
-// within one sequence.  Four kernels:
-//   count      per chunk: LDS histogram of the chunk's history selections
-//              over the sequence's blocks;
-//   scan_cols  per bin: exclusive prefix over the chunks of its sequence (in
+// (at most kRouteRows rows) within one sequence.  Per sequence and kv-head
+// the histogram holds one column per block over the sequence's chunks.
+// Four kernels:
+//   count      per chunk: the chunk's selections, read once and coalesced
+//              (each token's G * topk entries are contiguous), counted per
+//              block in LDS and written to the blocks' columns;
+//   scan_cols  one wave per bin: exclusive prefix over its column (in
 //              place), and the bin total;
 //   scan_bins  one work-group: exclusive scans of bin totals (entry offsets)
 //              and of ceil(total / tile_rows) (attention tile offsets);
-//   scatter    per chunk, 256 rows at a time: every row ORs its bit into an
-//              LDS bitmask per selected block; a row's rank among the round's
+//   scatter    per chunk, one thread per row: every row ORs its bit into an
+//              LDS bitmask per selected block; a row's rank among the chunk's
 //              rows that chose the same block is the popcount of the lower
-//              bits, which keeps the order of rows (a stable sort).
+//              bits, which keeps the order of rows (a stable sort).  The
+//              chunk's entries are gathered in LDS, grouped by block, and
+//              each block's run is then written out contiguously.  When that
+//              does not fit in LDS, rounds of 256 rows write their entries
+//              one by one.
 // Entry value: r * (topk - 1) + slot, where slot is the position of the block
 // in the row's ascending selection.
 #include "moba_internal.h"
@@ -43,6 +50,13 @@ __device__ __forceinline__ ChunkPos chunk_pos(const SeqInfo* seqs, const Problem
   return c;
 }
 
+// Column of block j of sequence sq (kv-head g) in the histogram.
+__device__ __forceinline__ int32_t* hist_col(int32_t* hist, const Problem& p, int g,
+                                             const SeqInfo& sq, int j) {
+  const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
+  return hist + (int64_t)g * p.hist_words + sq.hist_off + (int64_t)j * nchunks;
+}
+
 __global__ __launch_bounds__(256) void route_count_kernel(const int32_t* __restrict__ sel,
                                                           const SeqInfo* __restrict__ seqs,
                                                           Problem p, int32_t* __restrict__ hist) {
@@ -53,39 +67,52 @@ __global__ __launch_bounds__(256) void route_count_kernel(const int32_t* __restr
   const int kh = p.topk - 1;
   for (int j = threadIdx.x; j < sq.nblk; j += 256) cnt[j] = 0;
   __syncthreads();
-  const int nrow = cp.ntok * p.G;
-  for (int i = threadIdx.x; i < nrow; i += 256) {
-    const int tl = cp.tl0 + i / p.G, hl = i % p.G;
-    const int c = tl / p.B;
-    const int nh = min(kh, c);
-    const int64_t row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;
-    for (int x = 0; x < nh; x++) atomicAdd(&cnt[sel[row * p.topk + x]], 1);
+  // element e of the chunk: token cp.tl0 + e / (G topk), entry e % (G topk)
+  // of the token's group of rows (head hl = entry / topk, slot x = entry % topk)
+  const int per_tok = p.G * p.topk;
+  const int n = cp.ntok * per_tok;  // at most kRouteRows * topk
+  const int32_t* base = sel + ((int64_t)(sq.tok_start + cp.tl0) * p.Hq + (int64_t)g * p.G) * p.topk;
+  const int64_t tok_stride = (int64_t)p.Hq * p.topk;
+  for (int e = threadIdx.x; e < n; e += 256) {
+    const int tk = e / per_tok, w = e - tk * per_tok;
+    const int x = w % p.topk;
+    const int nh = min(kh, (cp.tl0 + tk) / p.B);
+    if (x < nh) atomicAdd(&cnt[base[tk * tok_stride + w]], 1);
   }
   __syncthreads();
-  int32_t* dst = hist + (int64_t)g * p.hist_words + sq.hist_off + (int64_t)cp.r * sq.nblk;
-  for (int j = threadIdx.x; j < sq.nblk; j += 256) dst[j] = cnt[j];
+  const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
+  int32_t* col0 = hist + (int64_t)g * p.hist_words + sq.hist_off + cp.r;
+  for (int j = threadIdx.x; j < sq.nblk; j += 256) col0[(int64_t)j * nchunks] = cnt[j];
 }
 
+// One wave per bin: exclusive scan of the bin's column, and its total.
 __global__ __launch_bounds__(256) void route_scan_cols_kernel(const SeqInfo* __restrict__ seqs,
                                                               Problem p, int32_t* __restrict__ hist,
                                                               int32_t* __restrict__ bin_count) {
-  const int64_t bin = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t bin = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;
   if (bin >= nbins) return;
   const int g = (int)(bin / p.nblk_total);
   const int b = (int)(bin % p.nblk_total);
   const int s = find_seq(seqs, p.S, b, [](const SeqInfo& x) { return x.blk_off; });
   const SeqInfo sq = seqs[s];
-  const int j = b - sq.blk_off;
   const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
-  int32_t* col = hist + (int64_t)g * p.hist_words + sq.hist_off + j;
+  int32_t* col = hist_col(hist, p, g, sq, b - sq.blk_off);
   int32_t run = 0;
-  for (int r = 0; r < nchunks; r++) {
-    const int32_t v = col[(int64_t)r * sq.nblk];
-    col[(int64_t)r * sq.nblk] = run;
-    run += v;
+  for (int r0 = 0; r0 < nchunks; r0 += 64) {
+    const int r = r0 + lane;
+    const int32_t v = r < nchunks ? col[r] : 0;
+    int32_t inc = v;  // inclusive prefix over the 64 lanes
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int32_t o = __shfl_up(inc, d, 64);
+      if (lane >= d) inc += o;
+    }
+    if (r < nchunks) col[r] = run + inc - v;
+    run += __shfl(inc, 63, 64);
   }
-  bin_count[bin] = run;
+  if (lane == 0) bin_count[bin] = run;
 }
 
 __global__ __launch_bounds__(1024) void route_scan_bins_kernel(const int32_t* __restrict__ bin_count,
@@ -127,6 +154,7 @@ __global__ __launch_bounds__(1024) void route_scan_bins_kernel(const int32_t* __
   }
 }
 
+// Entries written one by one (chunks whose entries do not fit in LDS).
 __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __restrict__ sel,
                                                             const SeqInfo* __restrict__ seqs,
                                                             Problem p,
@@ -139,13 +167,14 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
   const ChunkPos cp = chunk_pos(seqs, p, blockIdx.x);
   const SeqInfo sq = seqs[cp.s];
   const int nb = sq.nblk;
-  uint32_t* mask = lds;            // [nb][8]
+  uint32_t* mask = lds;            // [8][nb], word-major
   uint32_t* running = lds + 8 * nb;  // [nb]
-  // with use_pre: [nb][8] bytes, the set bits of each block's words below a word
+  // with use_pre: [8][nb] bytes, the set bits of each block's words below a word
   uint8_t* pre = reinterpret_cast<uint8_t*>(lds + 9 * nb);
   const int kh = p.topk - 1;
   const int tid = threadIdx.x, word = tid >> 5, bit = tid & 31;
-  const int32_t* chunk_off = hist + (int64_t)g * p.hist_words + sq.hist_off + (int64_t)cp.r * nb;
+  const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
+  const int32_t* chunk_off = hist + (int64_t)g * p.hist_words + sq.hist_off + cp.r;
   const int64_t* bstart = bin_start + (int64_t)g * p.nblk_total + sq.blk_off;
   const uint64_t TG = (uint64_t)p.T * p.G;
   for (int j = tid; j < nb; j += 256) running[j] = 0;
@@ -162,7 +191,7 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
       hl = i % p.G;
       nh = min(kh, tl / p.B);
       row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;
-      for (int x = 0; x < nh; x++) atomicOr(&mask[sel[row * p.topk + x] * 8 + word], 1u << bit);
+      for (int x = 0; x < nh; x++) atomicOr(&mask[word * nb + sel[row * p.topk + x]], 1u << bit);
     }
     __syncthreads();
     if (use_pre) {
@@ -170,8 +199,8 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
         uint32_t acc = 0;  // at most 7 * 32
 #pragma unroll
         for (int w = 0; w < 8; w++) {
-          pre[j * 8 + w] = (uint8_t)acc;
-          acc += __popc(mask[j * 8 + w]);
+          pre[w * nb + j] = (uint8_t)acc;
+          acc += __popc(mask[w * nb + j]);
         }
       }
       __syncthreads();
@@ -180,14 +209,13 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
       const uint64_t r = (uint64_t)g * TG + (uint64_t)(sq.tok_start + tl) * p.G + hl;
       for (int x = 0; x < nh; x++) {
         const int j = sel[row * p.topk + x];
-        const uint32_t* m = mask + j * 8;
-        uint32_t rank = running[j] + __popc(m[word] & ((1u << bit) - 1u));
+        uint32_t rank = running[j] + __popc(mask[word * nb + j] & ((1u << bit) - 1u));
         if (use_pre) {
-          rank += pre[j * 8 + word];
+          rank += pre[word * nb + j];
         } else {
-          for (int w = 0; w < word; w++) rank += __popc(m[w]);
+          for (int w = 0; w < word; w++) rank += __popc(mask[w * nb + j]);
         }
-        const int64_t pos = bstart[j] + chunk_off[j] + rank;
+        const int64_t pos = bstart[j] + chunk_off[(int64_t)j * nchunks] + rank;
         entries[pos] = (uint32_t)(r * (uint64_t)kh + (uint64_t)x);
       }
     }
@@ -195,11 +223,129 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
     for (int j = tid; j < nb; j += 256) {
       uint32_t c = 0;
 #pragma unroll
-      for (int w = 0; w < 8; w++) c += __popc(mask[j * 8 + w]);
+      for (int w = 0; w < 8; w++) c += __popc(mask[w * nb + j]);
       running[j] += c;
     }
     __syncthreads();
   }
+}
+
+// LDS of the staged scatter for nb blocks and kh selections per row: masks
+// [32][nb] words (one bit per row of the chunk), their prefix counts [32][nb]
+// (u16), per-block segment start and chunk count [nb] each, and the chunk's
+// entries [kRouteRows * kh].
+__host__ __device__ inline size_t staged_lds_bytes(int nb, int kh) {
+  return (size_t)nb * (128 + 64 + 8) + (size_t)kRouteRows * kh * 4;
+}
+
+// KH: largest number of history selections per row (register array).
+template <int KH>
+__global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
+    const int32_t* __restrict__ sel, const SeqInfo* __restrict__ seqs, Problem p,
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ bin_count,
+    const int64_t* __restrict__ bin_start, uint32_t* __restrict__ entries) {
+  extern __shared__ uint32_t lds[];
+  constexpr int kWords = kRouteRows / 32;
+  const int g = blockIdx.y;
+  const ChunkPos cp = chunk_pos(seqs, p, blockIdx.x);
+  const SeqInfo sq = seqs[cp.s];
+  const int nb = sq.nblk;
+  const int kh = p.topk - 1;
+  uint32_t* mask = lds;                                  // [32][nb] (word-major: no bank
+                                                         // conflicts among a word's lanes)
+  uint32_t* seg = mask + kWords * nb;                    // [nb] segment start of block j in ent
+  uint32_t* ccnt = seg + nb;                             // [nb] entries of block j in this chunk
+  uint32_t* ent = ccnt + nb;                             // [rows * kh]
+  uint16_t* pre = reinterpret_cast<uint16_t*>(ent + kRouteRows * kh);  // [32][nb]
+  const int tid = threadIdx.x, word = tid >> 5, bit = tid & 31;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
+  const int32_t* col0 = hist + (int64_t)g * p.hist_words + sq.hist_off;
+  const int64_t bin0 = (int64_t)g * p.nblk_total + sq.blk_off;
+
+  for (int j = tid; j < nb; j += kRouteRows) {
+    const int32_t* col = col0 + (int64_t)j * nchunks;
+    const int32_t a = col[cp.r];
+    const int32_t b = cp.r + 1 < nchunks ? col[cp.r + 1] : bin_count[bin0 + j];
+    ccnt[j] = (uint32_t)(b - a);
+  }
+  for (int x = tid; x < kWords * nb; x += kRouteRows) mask[x] = 0;
+  // this thread's row and its selections
+  const int nrow = cp.ntok * p.G;
+  const bool valid = tid < nrow;
+  const int tl = cp.tl0 + tid / p.G, hl = tid % p.G;
+  const int nh = valid ? min(kh, tl / p.B) : 0;
+  int js[KH];
+  const int32_t* mine = sel + ((int64_t)(sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl) * p.topk;
+#pragma unroll
+  for (int x = 0; x < KH; x++) js[x] = x < nh ? mine[x] : 0;
+  __syncthreads();
+  // segment starts: exclusive scan of ccnt (wave 0, 64 blocks per step)
+  if (wave == 0) {
+    uint32_t run = 0;
+    for (int j0 = 0; j0 < nb; j0 += 64) {
+      const int j = j0 + lane;
+      const uint32_t v = j < nb ? ccnt[j] : 0;
+      uint32_t inc = v;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += o;
+      }
+      if (j < nb) seg[j] = run + inc - v;
+      run += __shfl(inc, 63, 64);
+    }
+  }
+#pragma unroll
+  for (int x = 0; x < KH; x++)
+    if (x < nh) atomicOr(&mask[word * nb + js[x]], 1u << bit);
+  __syncthreads();
+  // per block: rows of the chunk in the words below each word
+  for (int j = tid; j < nb; j += kRouteRows) {
+    uint32_t acc = 0;
+#pragma unroll
+    for (int w = 0; w < kWords; w++) {
+      pre[w * nb + j] = (uint16_t)acc;
+      acc += __popc(mask[w * nb + j]);
+    }
+  }
+  __syncthreads();
+  if (valid) {
+    const uint64_t r = (uint64_t)g * ((uint64_t)p.T * p.G) + (uint64_t)(sq.tok_start + tl) * p.G + hl;
+#pragma unroll
+    for (int x = 0; x < KH; x++) {
+      if (x < nh) {
+        const int j = js[x];
+        const uint32_t rank = pre[word * nb + j] +
+                              __popc(mask[word * nb + j] & ((1u << bit) - 1u));
+        ent[seg[j] + rank] = (uint32_t)(r * (uint64_t)kh + (uint64_t)x);
+      }
+    }
+  }
+  __syncthreads();
+  // each block's run, contiguous in LDS and in the bin's list: one wave per block
+  for (int j = wave; j < nb; j += kRouteRows / 64) {
+    const uint32_t n = ccnt[j];
+    if (n == 0) continue;
+    uint32_t* dst = entries + bin_start[bin0 + j] + col0[(int64_t)j * nchunks + cp.r];
+    const uint32_t* srcj = ent + seg[j];
+    for (uint32_t e = lane; e < n; e += 64) dst[e] = srcj[e];
+  }
+}
+
+template <int KH>
+hipError_t launch_staged(dim3 grid, size_t lds, const int32_t* sel, const SeqInfo* seqs,
+                         const Problem& p, const RouteBuffers& rb, hipStream_t st) {
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&route_scatter_staged_kernel<KH>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  route_scatter_staged_kernel<KH><<<grid, kRouteRows, lds, st>>>(sel, seqs, p, rb.hist,
+                                                                 rb.bin_count, rb.bin_start,
+                                                                 rb.entries);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -214,8 +360,8 @@ hipError_t launch_route(const int32_t* sel, const SeqInfo* seqs, const Problem& 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  route_scan_cols_kernel<<<(unsigned)((nbins + 255) / 256), 256, 0, st>>>(seqs, p, rb.hist,
-                                                                          rb.bin_count);
+  route_scan_cols_kernel<<<(unsigned)((nbins + 3) / 4), 256, 0, st>>>(seqs, p, rb.hist,
+                                                                      rb.bin_count);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   route_scan_bins_kernel<<<1, 1024, 0, st>>>(rb.bin_count, nbins, p.tile_rows, rb.bin_start,
@@ -224,6 +370,15 @@ hipError_t launch_route(const int32_t* sel, const SeqInfo* seqs, const Problem& 
   if (e != hipSuccess) return e;
   if (p.route_chunks > 0 && p.hist_entries > 0) {
     dim3 grid((unsigned)p.route_chunks, p.Hkv);
+    const int kh = p.topk - 1;
+    const size_t staged = staged_lds_bytes(p.nblk_max, kh);
+    if (staged <= kRouteLdsMax && kh <= 31) {
+      if (kh <= 3) return launch_staged<3>(grid, staged, sel, seqs, p, rb, st);
+      if (kh <= 7) return launch_staged<7>(grid, staged, sel, seqs, p, rb, st);
+      if (kh <= 11) return launch_staged<11>(grid, staged, sel, seqs, p, rb, st);
+      if (kh <= 15) return launch_staged<15>(grid, staged, sel, seqs, p, rb, st);
+      return launch_staged<31>(grid, staged, sel, seqs, p, rb, st);
+    }
     // the per-block prefix table when it fits beside the masks in LDS
     const size_t base = (size_t)p.nblk_max * 9 * sizeof(uint32_t);
     const bool use_pre = base + (size_t)p.nblk_max * 8 <= kRouteLdsMax;

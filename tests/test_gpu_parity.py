@@ -127,8 +127,21 @@ def test_select_scores_within_bound():
         assert np.all(np.abs(gsc[m, j] - osc[m, j]) <= tau)
 
 
-def test_route_matches_cpu_inversion():
-    seqlens, hq, hkv, B, topk = (1500, 0, 700, 33), 8, 2, 64, 4
+ROUTE_CASES = [
+    # seqlens, hq, hkv, B, topk
+    ((1500, 0, 700, 33), 8, 2, 64, 4),
+    ((9000, 0, 3000), 8, 2, 128, 12),  # several routing chunks per sequence, LDS-staged runs
+    ((2000, 1000), 6, 2, 32, 5),       # groups of 3 query heads: rounds of 255 rows
+    ((700,), 2, 1, 1, 64),             # 700 one-key blocks, 63 per row: entries written directly
+]
+
+
+@pytest.mark.parametrize("seqlens,hq,hkv,B,topk", ROUTE_CASES,
+                         ids=["-".join(map(str, c[0])) + "_h%dx%d_B%d_k%d" % c[1:]
+                              for c in ROUTE_CASES])
+def test_route_matches_cpu_inversion(seqlens, hq, hkv, B, topk):
+    """Algorithm 1's index_select step: every bin's list holds exactly the
+    history selections of its (kv-head, block), in row order."""
     q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, offset=0.5, seed=11)
     sel = binding.select(q, k, cu, B, topk)
     counts, offsets, entries = binding.route(sel, cu, B, hkv)
