@@ -253,6 +253,13 @@ def run_sweep(args):
         lse = torch.empty((w.hq, L), dtype=torch.float32, device=dev)
         step = lambda: binding.forward(q, k, v, cu, w.block_size, w.topk, out=out, lse=lse)
         ms = time_steps(step, args.sweep_steps, 1)
+        # one more step with per-phase events (not in the timing)
+        binding.profile_read()
+        binding.profile_enable(True)
+        step()
+        torch.cuda.synchronize()
+        binding.profile_enable(False)
+        phases = binding.profile_read()
         cur, hist, _ = attended_keys(w.seqlens, w.block_size, w.topk)
         flop = 4.0 * w.d * w.hq * (cur + hist)
         dflop = 4.0 * w.d * w.hq * dense_keys(w.seqlens)
@@ -274,6 +281,7 @@ def run_sweep(args):
             "dense_flop": dflop, "flop_ratio": round(dflop / flop, 3),
             "dense_ms": None if dense_ms is None else round(dense_ms, 2), "dense": dense_kind,
             "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 3),
+            "phases_ms": {n: round(t, 3) for n, (c, t) in phases.items()},
         }), flush=True)
         del q, k, v, out, lse
         torch.cuda.empty_cache()

@@ -210,12 +210,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
     const int64_t per = gridDim.x / 8;
     const int64_t tile = tbeg + (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
     if (tile >= tend) return;
-    int64_t lo = a.g0 * nb, hi = a.g1 * nb - 1;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (a.bin_tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    const int64_t bin = lo;
+    const int64_t bin = a.tile_bin[tile];
     g = (int)(bin / nb);
     const int b = (int)(bin % nb);
     const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kRows;

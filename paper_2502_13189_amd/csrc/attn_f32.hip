@@ -34,12 +34,7 @@ __global__ __launch_bounds__(128, 1) void attn_f32_kernel(AttnArgs a, Problem p)
     const int64_t tend = a.bin_tile_start[a.g1 * nb];
     const int64_t tile = tbeg + blockIdx.x;
     if (tile >= tend) return;
-    int64_t lo = a.g0 * nb, hi = a.g1 * nb - 1;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (a.bin_tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    const int64_t bin = lo;
+    const int64_t bin = a.tile_bin[tile];
     g = (int)(bin / nb);
     const int b = (int)(bin % nb);
     const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kTileRowsF32;

@@ -57,6 +57,7 @@ enum { kHist = 0, kCur = 1, kDense = 2 };
 constexpr int kRows = kTileRowsMfma;               // query rows per work-group (256)
 constexpr int kLdsChunks = 2 * kBufK + 2 * kBufV;  // 70 KiB: two K and two V^T buffers
 constexpr float kSumLimit = 256.0f;  // largest per-lane weight sum kept without a rescale
+constexpr int kPersistMaxBlock = 1024;  // blocks this short run on the persistent history kernel
 constexpr float kLn2 = 0.69314718055994531f;
 
 // Weights of S under the running max m as bf16 P^T operands pb[2*th + s2]
@@ -137,12 +138,7 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p
     const int64_t per = gridDim.x / 8;
     const int64_t tile = tbeg + (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
     if (tile >= tend) return;
-    int64_t lo = a.g0 * nb, hi = a.g1 * nb - 1;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (a.bin_tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    const int64_t bin = lo;
+    const int64_t bin = a.tile_bin[tile];
     g = (int)(bin / nb);
     const int b = (int)(bin % nb);
     const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kRows;
@@ -309,10 +305,207 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p
   }
 }
 
+// ----------------------------------------------------------------------
+// History tiles of short blocks, persistent: one work-group per CU walks a
+// run of tiles.  With few key tiles per history tile (B / 64), the per-tile
+// cost outside the key loop (work-group start, routed query rows, first K/V
+// tile, epilogue) would dominate; here the next tile's query rows and first
+// K/V tile are fetched during the current tile's last key tile.
+struct HistCtx {
+  int g, s;
+  int64_t kbeg, kend, tok0;
+  int i0, i1;
+  RowInfo ri;
+};
+
+__device__ __forceinline__ bool hist_setup(const AttnArgs& a, const Problem& p, int64_t tile,
+                                           int64_t tlim, int rloc, HistCtx& c) {
+  if (tile >= tlim) return false;
+  const int64_t nb = p.nblk_total;
+  const int64_t bin = a.tile_bin[tile];
+  const int g = (int)(bin / nb);
+  const int b = (int)(bin % nb);
+  const int64_t e0 = a.bin_start[bin] + (tile - a.bin_tile_start[bin]) * kRows;
+  const int n = (int)min((int64_t)kRows, a.bin_start[bin] + a.bin_count[bin] - e0);
+  const int s = find_seq(a.seqs, p.S, b, [](const SeqInfo& x) { return x.blk_off; });
+  const SeqInfo sq = a.seqs[s];
+  const int64_t kbeg = (int64_t)sq.tok_start + (int64_t)(b - sq.blk_off) * p.B;
+  const uint64_t kh = (uint64_t)(p.topk - 1);
+  const uint64_t TG = (uint64_t)p.T * p.G;
+  const uint64_t ev = a.entries[e0 + min(rloc, n - 1)];
+  const uint64_t rem = ev / kh - (uint64_t)g * TG;
+  const bool ok = rem < TG;
+  c.ri.valid = rloc < n && ok;
+  c.ri.t = ok ? (int64_t)(rem / p.G) : kbeg;
+  c.ri.h = g * p.G + (ok ? (int)(rem % p.G) : 0);
+  c.ri.dst = (int64_t)(ev - (uint64_t)a.g0 * TG * kh);
+  c.g = __builtin_amdgcn_readfirstlane(g);
+  c.s = __builtin_amdgcn_readfirstlane(s);
+  c.kbeg = uniform64(kbeg);
+  c.kend = uniform64(kbeg + p.B);
+  c.tok0 = uniform64(sq.tok_start);
+  c.i0 = (int)((c.kbeg - c.tok0) / kKeyTile);
+  c.i1 = (int)((c.kend - c.tok0 + kKeyTile - 1) / kKeyTile);
+  return true;
+}
+
+// The tile-dependent (wave-uniform) part of the DMA sources.
+__device__ __forceinline__ void dma_tile(Dma& D, const AttnArgs& a, const Problem& p,
+                                         const HistCtx& c) {
+  const SeqInfo sq = a.seqs[c.s];
+  const int64_t kst = a.k_st * 2;
+  D.kbase = reinterpret_cast<const char*>(static_cast<const __hip_bfloat16*>(a.k) +
+                                          (int64_t)c.g * a.k_sh) + c.tok0 * kst;
+  D.len = sq.len;
+  D.klast = D.kbase + (sq.len - 1) * kst;
+  D.vbase = reinterpret_cast<const char*>(
+      a.vt + ((int64_t)c.g * p.vt_tiles + sq.vt_tile_off) * (kKeyTile * kHeadDim));
+}
+
+__device__ __forceinline__ void load_q(bf16x8 (&qf)[8], const AttnArgs& a, const RowInfo& ri,
+                                       int hh) {
+  const __hip_bfloat16* qrow = static_cast<const __hip_bfloat16*>(a.q) + ri.t * a.q_st +
+                               (int64_t)ri.h * a.q_sh + 8 * hh;
+#pragma unroll
+  for (int kk = 0; kk < 8; kk++)
+    qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 16 * kk));
+}
+
+__global__ __launch_bounds__(512, 1) void attn_hist_persist_kernel(AttnArgs a, Problem p) {
+  __shared__ u32x4 lds[kLdsChunks];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int qc = lane & 31, hh = lane >> 5;
+  const int rloc = wave * 32 + qc;
+
+  // XCD-aware walk: work-groups go round-robin to the 8 XCDs; XCD x owns
+  // the contiguous run [x*per, (x+1)*per) of the tiles (tiles of one bin share
+  // its K/V block), and its work-groups take every nx-th tile of it.  Every
+  // work-group leaves the loop once its next tile is past the run.
+  const int64_t nb = p.nblk_total;
+  const int64_t tbeg = a.bin_tile_start[a.g0 * nb];
+  const int64_t tend = a.bin_tile_start[a.g1 * nb];
+  const int64_t nx = gridDim.x / 8;
+  const int64_t per = (tend - tbeg + 7) / 8;
+  const int64_t xs = tbeg + (int64_t)(blockIdx.x % 8) * per;
+  const int64_t tlim = min(tend, xs + per);
+  int64_t tile = xs + blockIdx.x / 8;
+
+  HistCtx c;
+  if (!hist_setup(a, p, tile, tlim, rloc, c)) return;
+  bf16x8 qf[8];
+  load_q(qf, a, c.ri, hh);
+  Dma D;
+  {
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    D.wave = wv;
+    const int64_t kst = a.k_st * 2;
+    D.k_tile = kKeyTile * kst;
+#pragma unroll
+    for (int x = 0; x < 3; x++) {
+      const int pk = 64 * (wv + 8 * x) + lane;
+      const int row = min(pk / kRowK, kKeyTile - 1), col = min(pk % kRowK, kRowK - 2);
+      D.krow[x] = row;
+      D.kcol[x] = (uint32_t)(col * 16);
+      D.koff[x] = (uint32_t)(row * kst) + D.kcol[x];
+      const int vrow = min(pk / kRowV, kHeadDim - 1), vc = min(pk % kRowV, kRowV - 2);
+      D.voff[x] = (uint32_t)(vrow * (kKeyTile * 2) + vc * 16);
+    }
+  }
+  dma_tile(D, a, p, c);
+  ReadOff ro;
+  ro.kq = qc * kRowK + hh;
+  ro.vq = qc * kRowV + hh;
+  const float c2 = a.scale_log2;
+
+  dma_k(D, c.i0, lds);
+  dma_v(D, c.i0, lds + 2 * kBufK);
+  dma_wait();
+  __syncthreads();
+
+  int par = 0;  // buffer holding the current key tile
+  for (;;) {
+    HistCtx n;
+    const bool more = hist_setup(a, p, tile + nx, tlim, rloc, n);
+    Dma Dn = D;
+    if (more) dma_tile(Dn, a, p, n);
+    f32x16 o[4];
+    float m = -INFINITY, l = 0.0f;
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) o[dt][r] = 0.0f;
+    f32x16 sc[2];
+    bf16x8 pb[4];
+    for (int i = c.i0; i < c.i1; i++) {
+      const int cur = par;
+      par ^= 1;
+      const bool last = i + 1 == c.i1;
+      if (!last) {
+        dma_k(D, i + 1, lds + (cur ^ 1) * kBufK);
+        dma_v(D, i + 1, lds + 2 * kBufK + (cur ^ 1) * kBufV);
+      } else if (more) {
+        dma_k(Dn, n.i0, lds + (cur ^ 1) * kBufK);
+        dma_v(Dn, n.i0, lds + 2 * kBufK + (cur ^ 1) * kBufV);
+      }
+      qk(sc, lds + cur * kBufK, ro, qf);
+      if (last && more) load_q(qf, a, n.ri, hh);  // this tile's products are issued
+      const int64_t u0 = c.tok0 + (int64_t)i * kKeyTile;
+      const bool edge = u0 < c.kbeg || u0 + kKeyTile > c.kend;
+      int lo = 0, hi = kKeyTile;
+      if (edge) {
+        lo = (int)max((int64_t)0, c.kbeg - u0) - 4 * hh;
+        hi = (int)min((int64_t)kKeyTile, c.kend - u0) - 4 * hh;
+      }
+      softmax<kHist>(sc, m, l, o, pb, edge, lo, hi, c2);
+      pv(o, lds + 2 * kBufK + cur * kBufV, ro, pb);
+      dma_wait();
+      __syncthreads();
+    }
+    // epilogue: the normalised partial (bf16) and its lse
+    const float l_tot = l + xor32(l);  // every lane takes part in the exchange
+    if (c.ri.valid) {
+      const float inv = 1.0f / l_tot;
+      const float lse = (m + __builtin_amdgcn_logf(l_tot)) * kLn2;
+      uint2* orow = reinterpret_cast<uint2*>(static_cast<__hip_bfloat16*>(a.o_part) +
+                                             c.ri.dst * kHeadDim);
+#pragma unroll
+      for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; r4++) {
+          uint2 w;
+          w.x = pack_bf16(o[dt][4 * r4 + 0] * inv, o[dt][4 * r4 + 1] * inv);
+          w.y = pack_bf16(o[dt][4 * r4 + 2] * inv, o[dt][4 * r4 + 3] * inv);
+          orow[(32 * dt + 8 * r4 + 4 * hh) >> 2] = w;
+        }
+      if (hh == 0) a.lse_part[c.ri.dst] = lse;
+    }
+    if (!more) break;
+    c = n;
+    D = Dn;
+    tile += nx;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_attn_hist_bf16(const AttnArgs& a, const Problem& p, int64_t grid, hipStream_t st) {
   if (grid <= 0) return hipSuccess;
+  if (p.B <= kPersistMaxBlock) {
+    // short blocks: one work-group per CU (a multiple of 8), walking the tiles
+    static int ncu = 0;
+    if (!ncu) {
+      int dev = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return hipErrorInvalidDevice;
+    }
+    int64_t g = ncu / 8 * 8;
+    if (g < 8) g = 8;
+    if (g > (grid + 7) / 8 * 8) g = (grid + 7) / 8 * 8;
+    attn_hist_persist_kernel<<<(unsigned)g, 512, 0, st>>>(a, p);
+    return hipGetLastError();
+  }
   grid = (grid + 7) / 8 * 8;
   attn_mfma_kernel<kHist><<<(unsigned)grid, 512, 0, st>>>(a, p);
   return hipGetLastError();

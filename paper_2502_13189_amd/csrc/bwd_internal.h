@@ -32,6 +32,7 @@ struct BwdArgs {
   const SeqInfo* seqs;
   // routing lists (null when no row has a history block)
   const int32_t* bin_tile_start;
+  const int32_t* tile_bin;  // the bin of every history tile
   const int64_t* bin_start;
   const int32_t* bin_count;
   const uint32_t* entries;

@@ -647,6 +647,7 @@ void forward_layout(const Problem& p, bool bf16, int kk, int nch, Bump* bp, FwdB
   b->rb.bin_start = bp->take<int64_t>(nbins + 1);
   b->rb.bin_tile_start = bp->take<int32_t>(nbins + 1);
   b->rb.entries = bp->take<uint32_t>(p.hist_entries);
+  b->rb.tile_bin = bp->take<int32_t>(route_tiles_bound(p.hist_entries, nbins, p.tile_rows));
   const int64_t rows = (int64_t)nch * p.T * p.G;
   b->o_part = bf16 ? (void*)bp->take<__hip_bfloat16>(rows * kh * kHeadDim)
                    : (void*)bp->take<float>(rows * kh * kHeadDim);
@@ -742,6 +743,7 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
   a.vt = vt;
   a.seqs = d_seqs;
   a.bin_tile_start = rb.bin_tile_start;
+  a.tile_bin = rb.tile_bin;
   a.bin_start = rb.bin_start;
   a.bin_count = rb.bin_count;
   a.entries = rb.entries;
@@ -873,6 +875,7 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
     b->rb.bin_start = bp->take<int64_t>(nbins + 1);
     b->rb.bin_tile_start = bp->take<int32_t>(nbins + 1);
     b->rb.entries = bp->take<uint32_t>(p.hist_entries);
+    b->rb.tile_bin = bp->take<int32_t>(route_tiles_bound(p.hist_entries, nbins, kTileRowsMfma));
     b->ld = bp->take<float2>(p.T * p.Hq);
     b->rec = bp->take<int4>(routed ? p.hist_entries : 0);
     b->dq_part = bp->take<float>(routed ? (int64_t)nch * TG * kh * kHeadDim : 0);
@@ -907,6 +910,7 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   a.seqs = d_seqs;
   if (routed) {
     a.bin_tile_start = b.rb.bin_tile_start;
+    a.tile_bin = b.rb.tile_bin;
     a.bin_start = b.rb.bin_start;
     a.bin_count = b.rb.bin_count;
     a.entries = b.rb.entries;
@@ -1409,6 +1413,7 @@ size_t moba_workspace_bytes(int64_t T, int32_t Hq, int32_t Hkv, int32_t D, int64
   p.G = Hq / Hkv;
   p.nblk_total = (int)std::min<int64_t>(nblk_total, INT32_MAX);
   p.vt_tiles = ceil_div(T, kKeyTile) + nblk_total;
+  p.tile_rows = std::min(kTileRowsMfma, kTileRowsF32);  // the smaller gives more tiles
   const int kk = (int)std::min<int64_t>(topk, nblk_total);
   p.hist_words = (ceil_div(T, std::max(1, kRouteRows / p.G)) + 1) * nblk_total;
   p.hist_entries = T * Hq * (int64_t)(kk - 1);

@@ -73,7 +73,14 @@ struct RouteBuffers {
   int64_t* bin_start;       // [Hkv * nblk_total + 1]
   int32_t* bin_tile_start;  // [Hkv * nblk_total + 1] tiles of tile_rows entries
   uint32_t* entries;        // [hist_entries]
+  int32_t* tile_bin;        // nullable: [tiles] the bin of every attention tile
 };
+
+// Attention tiles of the routing lists, at most: one per tile_rows entries
+// plus one partial tile per bin.
+inline int64_t route_tiles_bound(int64_t entries, int64_t nbins, int tile_rows) {
+  return (entries + tile_rows - 1) / tile_rows + nbins;
+}
 
 hipError_t launch_route(const int32_t* sel, const SeqInfo* seqs, const Problem& p,
                         const RouteBuffers& rb, hipStream_t st);
@@ -89,6 +96,7 @@ struct AttnArgs {
   const int64_t* bin_start;
   const int32_t* bin_count;
   const uint32_t* entries;
+  const int32_t* tile_bin;  // the bin of every history tile
   void* o_part;     // [rows_chunk * (topk-1), D], normalised; bf16 on the bf16
                     // path, fp32 on the fp32 path
   float* lse_part;  // [rows_chunk * (topk-1)]

@@ -154,6 +154,16 @@ __global__ __launch_bounds__(1024) void route_scan_bins_kernel(const int32_t* __
   }
 }
 
+// One wave per bin: the bin index of each of its attention tiles.
+__global__ __launch_bounds__(256) void route_tile_bins_kernel(const int32_t* __restrict__ bin_tile_start,
+                                                              int64_t nbins,
+                                                              int32_t* __restrict__ tile_bin) {
+  const int64_t bin = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (bin >= nbins) return;
+  const int32_t t1 = bin_tile_start[bin + 1];
+  for (int32_t t = bin_tile_start[bin] + (threadIdx.x & 63); t < t1; t += 64) tile_bin[t] = (int32_t)bin;
+}
+
 // Entries written one by one (chunks whose entries do not fit in LDS).
 __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __restrict__ sel,
                                                             const SeqInfo* __restrict__ seqs,
@@ -368,6 +378,12 @@ hipError_t launch_route(const int32_t* sel, const SeqInfo* seqs, const Problem& 
                                               rb.bin_tile_start);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (rb.tile_bin) {
+    route_tile_bins_kernel<<<(unsigned)((nbins + 3) / 4), 256, 0, st>>>(rb.bin_tile_start, nbins,
+                                                                        rb.tile_bin);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (p.route_chunks > 0 && p.hist_entries > 0) {
     dim3 grid((unsigned)p.route_chunks, p.Hkv);
     const int kh = p.topk - 1;
