@@ -116,6 +116,44 @@ __device__ __forceinline__ void softmax(f32x16 (&s)[2], float& m, float& l, f32x
   l += ts;
 }
 
+// History epilogues stage the tile's normalised bf16 rows in LDS (rows of 17
+// chunks, so the staging writes of 32 lanes on 32 rows spread over the
+// banks) and then write each row as 16 lanes x 16 bytes, four whole rows per
+// instruction: the scattered partial rows land in full 128-byte lines
+// instead of 16-byte pieces spread over 16 instructions.
+constexpr int kStageRow = kHeadDim / 8 + 1;  // 16-byte chunks per staged row
+
+// Stages this lane's row (normalised, bf16) and its partial index; the
+// caller then synchronizes and calls store_staged.
+__device__ __forceinline__ void stage_row(const f32x16 (&o)[4], float inv, u32x4* stage,
+                                          int64_t* sdst, int rloc, int hh, bool valid, int64_t dst) {
+  uint2* srow = reinterpret_cast<uint2*>(stage + rloc * kStageRow);
+#pragma unroll
+  for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; r4++) {
+      uint2 w;
+      w.x = pack_bf16(o[dt][4 * r4 + 0] * inv, o[dt][4 * r4 + 1] * inv);
+      w.y = pack_bf16(o[dt][4 * r4 + 2] * inv, o[dt][4 * r4 + 3] * inv);
+      srow[(32 * dt + 8 * r4 + 4 * hh) >> 2] = w;
+    }
+  if (hh == 0) sdst[rloc] = valid ? dst : -1;
+}
+
+// Wave w writes staged rows 32w .. 32w + 31, four per instruction.
+__device__ __forceinline__ void store_staged(const AttnArgs& a, const u32x4* stage,
+                                             const int64_t* sdst, int wave, int lane) {
+  const int rsub = lane >> 4, ch = lane & 15;
+#pragma unroll
+  for (int j = 0; j < 8; j++) {
+    const int rr = 32 * wave + 4 * j + rsub;
+    const int64_t d = sdst[rr];
+    if (d >= 0)
+      reinterpret_cast<u32x4*>(static_cast<__hip_bfloat16*>(a.o_part) + d * kHeadDim)[ch] =
+          stage[rr * kStageRow + ch];
+  }
+}
+
 template <int MODE>
 __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p) {
   __shared__ u32x4 lds[kLdsChunks];
@@ -269,21 +307,13 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p
     f32x16 (&og)[4] = o;
     const RowInfo& r = ri;
     if constexpr (MODE == kHist) {
-      if (r.valid) {
-        // 4 consecutive dims per (dt, r4): one 8-byte store of 4 bf16
-        uint2* orow = reinterpret_cast<uint2*>(static_cast<__hip_bfloat16*>(a.o_part) +
-                                               r.dst * kHeadDim);
-#pragma unroll
-        for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-          for (int r4 = 0; r4 < 4; r4++) {
-            uint2 w;
-            w.x = pack_bf16(og[dt][4 * r4 + 0] * inv, og[dt][4 * r4 + 1] * inv);
-            w.y = pack_bf16(og[dt][4 * r4 + 2] * inv, og[dt][4 * r4 + 3] * inv);
-            orow[(32 * dt + 8 * r4 + 4 * hh) >> 2] = w;
-          }
-        if (hh == 0) a.lse_part[r.dst] = lse;
-      }
+      // the K/V buffers are free after the last barrier: stage the rows there
+      u32x4* stage = lds;
+      int64_t* sdst = reinterpret_cast<int64_t*>(lds + kRows * kStageRow);
+      stage_row(og, inv, stage, sdst, rloc, hh, r.valid, r.dst);
+      if (r.valid && hh == 0) a.lse_part[r.dst] = lse;
+      __syncthreads();
+      store_staged(a, stage, sdst, wave, lane);
     } else {
       const float scale = inv, lse_out = lse;
       if (r.valid) {
@@ -373,6 +403,8 @@ __device__ __forceinline__ void load_q(bf16x8 (&qf)[8], const AttnArgs& a, const
 
 __global__ __launch_bounds__(512, 1) void attn_hist_persist_kernel(AttnArgs a, Problem p) {
   __shared__ u32x4 lds[kLdsChunks];
+  __shared__ u32x4 stage[kRows * kStageRow];  // the tile's partial rows (bf16)
+  __shared__ int64_t sdst[kRows];             // their partial indices (-1: no row)
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
@@ -464,22 +496,12 @@ __global__ __launch_bounds__(512, 1) void attn_hist_persist_kernel(AttnArgs a, P
     }
     // epilogue: the normalised partial (bf16) and its lse
     const float l_tot = l + xor32(l);  // every lane takes part in the exchange
-    if (c.ri.valid) {
-      const float inv = 1.0f / l_tot;
-      const float lse = (m + __builtin_amdgcn_logf(l_tot)) * kLn2;
-      uint2* orow = reinterpret_cast<uint2*>(static_cast<__hip_bfloat16*>(a.o_part) +
-                                             c.ri.dst * kHeadDim);
-#pragma unroll
-      for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; r4++) {
-          uint2 w;
-          w.x = pack_bf16(o[dt][4 * r4 + 0] * inv, o[dt][4 * r4 + 1] * inv);
-          w.y = pack_bf16(o[dt][4 * r4 + 2] * inv, o[dt][4 * r4 + 3] * inv);
-          orow[(32 * dt + 8 * r4 + 4 * hh) >> 2] = w;
-        }
-      if (hh == 0) a.lse_part[c.ri.dst] = lse;
-    }
+    stage_row(o, 1.0f / l_tot, stage, sdst, rloc, hh, c.ri.valid, c.ri.dst);
+    if (c.ri.valid && hh == 0) a.lse_part[c.ri.dst] = (m + __builtin_amdgcn_logf(l_tot)) * kLn2;
+    __syncthreads();
+    store_staged(a, stage, sdst, wave, lane);
+    // the staging area is rewritten only after the next tile's key loop,
+    // whose barriers order these reads before those writes
     if (!more) break;
     c = n;
     D = Dn;
