@@ -115,6 +115,7 @@ def cpu_baseline(w, q, k, v, cu, n_rows, seed=7):
     cores = len(os.sched_getaffinity(0))
     oracle.set_threads(cores)
     T, Hq = q.shape[0], q.shape[1]
+    n_rows = min(n_rows, T * Hq)
     rng = np.random.default_rng(seed)
     rows = np.sort(rng.choice(T * Hq, size=n_rows, replace=False)).astype(np.int64)
     t_copy = time.perf_counter()
@@ -252,14 +253,23 @@ def run_sweep(args):
         out = torch.empty_like(q)
         lse = torch.empty((w.hq, L), dtype=torch.float32, device=dev)
         step = lambda: binding.forward(q, k, v, cu, w.block_size, w.topk, out=out, lse=lse)
-        ms = time_steps(step, args.sweep_steps, 1)
-        # one more step with per-phase events (not in the timing)
-        binding.profile_read()
-        binding.profile_enable(True)
-        step()
-        torch.cuda.synchronize()
-        binding.profile_enable(False)
-        phases = binding.profile_read()
+        if L < (1 << 22):
+            ms = time_steps(step, args.sweep_steps, 1)
+            # one more step with per-phase events (not in the timing)
+            binding.profile_read()
+            binding.profile_enable(True)
+            step()
+            torch.cuda.synchronize()
+            binding.profile_enable(False)
+            phases = binding.profile_read()
+        else:
+            # steps of many seconds: the events of the timed steps give the
+            # phases (their cost is negligible at this scale), no warm-up
+            binding.profile_read()
+            binding.profile_enable(True)
+            ms = time_steps(step, args.sweep_steps, 0)
+            binding.profile_enable(False)
+            phases = {n: (c, t / args.sweep_steps) for n, (c, t) in binding.profile_read().items()}
         cur, hist, _ = attended_keys(w.seqlens, w.block_size, w.topk)
         flop = 4.0 * w.d * w.hq * (cur + hist)
         dflop = 4.0 * w.d * w.hq * dense_keys(w.seqlens)

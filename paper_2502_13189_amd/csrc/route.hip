@@ -70,14 +70,27 @@ __global__ __launch_bounds__(256) void route_count_kernel(const int32_t* __restr
   // element e of the chunk: token cp.tl0 + e / (G topk), entry e % (G topk)
   // of the token's group of rows (head hl = entry / topk, slot x = entry % topk)
   const int per_tok = p.G * p.topk;
-  const int n = cp.ntok * per_tok;  // at most kRouteRows * topk
   const int32_t* base = sel + ((int64_t)(sq.tok_start + cp.tl0) * p.Hq + (int64_t)g * p.G) * p.topk;
   const int64_t tok_stride = (int64_t)p.Hq * p.topk;
-  for (int e = threadIdx.x; e < n; e += 256) {
-    const int tk = e / per_tok, w = e - tk * per_tok;
+  if (per_tok <= 256) {
+    // thread -> entry w of token tk0 + k * tpb: the divisions once per thread
+    const int tpb = 256 / per_tok;
+    const int tk0 = threadIdx.x / per_tok, w = threadIdx.x - tk0 * per_tok;
     const int x = w % p.topk;
-    const int nh = min(kh, (cp.tl0 + tk) / p.B);
-    if (x < nh) atomicAdd(&cnt[base[tk * tok_stride + w]], 1);
+    if (tk0 < tpb) {
+      for (int tk = tk0; tk < cp.ntok; tk += tpb) {
+        const int nh = min(kh, (cp.tl0 + tk) / p.B);
+        if (x < nh) atomicAdd(&cnt[base[tk * tok_stride + w]], 1);
+      }
+    }
+  } else {
+    const int n = cp.ntok * per_tok;  // at most kRouteRows * topk
+    for (int e = threadIdx.x; e < n; e += 256) {
+      const int tk = e / per_tok, w = e - tk * per_tok;
+      const int x = w % p.topk;
+      const int nh = min(kh, (cp.tl0 + tk) / p.B);
+      if (x < nh) atomicAdd(&cnt[base[tk * tok_stride + w]], 1);
+    }
   }
   __syncthreads();
   const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
