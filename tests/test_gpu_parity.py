@@ -51,6 +51,11 @@ SMALL = [
     ((300, 45), 128, 1, 64, 3, torch.bfloat16),    # the largest group, 128 query heads per kv-head
     ((257, 3), 4, 2, 4096, 2, torch.bfloat16),     # block larger than every sequence
     ((4000,), 2, 1, 1, 3, torch.bfloat16),         # 4000 blocks: routing ranks without its LDS prefix table
+    # more than one 32-block gate chunk, for each list size the gate bounds
+    # from below (k-1 = 1, 11, 15) before inserting
+    ((1500,), 4, 4, 16, 2, torch.bfloat16),
+    ((3000, 70), 4, 2, 16, 12, torch.bfloat16),
+    ((2500,), 2, 1, 8, 16, torch.bfloat16),
     ((300,), 2, 2, 64, 3, torch.float32),
     ((600, 250), 4, 2, 128, 4, torch.float32),
     ((515,), 2, 1, 50, 3, torch.float32),
@@ -85,10 +90,11 @@ def test_pool_matches_oracle(dtype):
     assert np.all(np.abs(kbar - ref) <= tol)
 
 
-def test_select_constructed_ties():
+@pytest.mark.parametrize("B,L,topk", [(64, 900, 4), (16, 900, 4), (8, 1200, 12), (4, 1000, 16)])
+def test_select_constructed_ties(B, L, topk):
     """Every block holds the same keys: all scores tie exactly and the lower
-    block index must win on the GPU too."""
-    B, L, topk = 64, 900, 4
+    block index must win on the GPU too (also where rows have more than one
+    32-block gate chunk and the gate first bounds the list from below)."""
     q, k, v, cu = make((L,), 4, 2, torch.bfloat16, B, seed=5)
     blk = k[:B].clone()
     k = blk.repeat((L + B - 1) // B, 1, 1)[:L].contiguous()
