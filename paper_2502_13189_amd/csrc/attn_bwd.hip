@@ -182,7 +182,7 @@ __device__ __forceinline__ void dma_vrow(const Dma& D, const VDma& V, int i, u32
     if (x < 2 || D.wave + 16 < kDmaK) {
       const char* src = tile + (D.krow[x] * V.st + D.kcol[x]);
       if (tail && base + D.krow[x] >= D.len) src = V.last + D.kcol[x];
-      __builtin_amdgcn_global_load_lds(src, buf + 64 * (D.wave + 8 * x), 16, 0, 0);
+      dma16(src, buf + 64 * (D.wave + 8 * x));
     }
   }
 }
@@ -665,10 +665,8 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   auto dma_rows = [&](int slot, u32x4* qbuf, u32x4* dbuf) {
 #pragma unroll
     for (int x = 0; x < kDx; x++) {
-      __builtin_amdgcn_global_load_lds(qb + R.qoff[slot][drow[x]] + dcol[x],
-                                       qbuf + 64 * (wave + kW * x), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(db + R.doff[slot][drow[x]] + dcol[x],
-                                       dbuf + 64 * (wave + kW * x), 16, 0, 0);
+      dma16(qb + R.qoff[slot][drow[x]] + dcol[x], qbuf + 64 * (wave + kW * x));
+      dma16(db + R.doff[slot][drow[x]] + dcol[x], dbuf + 64 * (wave + kW * x));
     }
   };
 

@@ -9,7 +9,7 @@
 // the GQA group).  Rows are cut into chunks of `route_rt` tokens x G heads
 // (at most kRouteRows rows) within one sequence.  Per sequence and kv-head
 // the histogram holds one column per block over the sequence's chunks.
-// Four kernels:
+// Five kernels:
 //   count      per chunk: the chunk's selections, read once and coalesced
 //              (each token's G * topk entries are contiguous), counted per
 //              block in LDS and written to the blocks' columns;
@@ -17,6 +17,7 @@
 //              place), and the bin total;
 //   scan_bins  one work-group: exclusive scans of bin totals (entry offsets)
 //              and of ceil(total / tile_rows) (attention tile offsets);
+//   tile_bins  one wave per bin: the bin of each of its attention tiles;
 //   scatter    per chunk, one thread per row: every row ORs its bit into an
 //              LDS bitmask per selected block; a row's rank among the chunk's
 //              rows that chose the same block is the popcount of the lower
