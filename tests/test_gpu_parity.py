@@ -233,6 +233,37 @@ def test_workspace_chunking_is_invisible(monkeypatch):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_chunked_attention_matches_one_pass(monkeypatch):
+    """Caps below the one-pass workspace (moba_workspace_bytes) split the
+    attention into 2 to 8 chunks of kv-heads that reuse one partial buffer;
+    every split must give the one-pass result bit for bit (the merge count
+    shows the chunk count)."""
+    seqlens, hq, hkv, B, topk = (2100, 0, 1300), 16, 8, 64, 5
+    q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, offset=0.5, seed=33)
+    nblk, _ = binding.route_size(cu, B, topk, hq)
+    one = binding.workspace_bytes(q.shape[0], hq, hkv, nblk, topk)
+    o1, l1 = binding.forward(q, k, v, cu, B, topk)
+    torch.cuda.synchronize()
+    chunks = []
+    for frac in (1.0, 0.5, 0.4, 0.3, 0.25, 0.2, 0.15, 0.12):
+        monkeypatch.setenv("MOBA_WORKSPACE_LIMIT_BYTES", str(int(one * frac)))
+        binding.profile_read()
+        binding.profile_enable(True)
+        try:
+            o2, l2 = binding.forward(q, k, v, cu, B, topk)
+        except binding.MobaError as e:  # below the fixed part plus one kv-head
+            binding.profile_enable(False)
+            assert e.name == "MOBA_ERR_NO_MEMORY"
+            continue
+        torch.cuda.synchronize()
+        binding.profile_enable(False)
+        chunks.append(binding.profile_read().get("merge", (0, 0.0))[0])
+        assert torch.equal(o1, o2) and torch.equal(l1, l2), frac
+    monkeypatch.delenv("MOBA_WORKSPACE_LIMIT_BYTES")
+    print("merge launches per cap:", chunks)
+    assert len(chunks) >= 3 and chunks[0] == 1 and max(chunks) >= 4, chunks
+
+
 def test_device_cu_seqlens():
     q, k, v, cu = make((500, 300), 4, 2, torch.bfloat16, 64, seed=31)
     o1, l1 = binding.forward(q, k, v, cu, 64, 3)
