@@ -257,9 +257,11 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
 // LDS of the staged scatter for nb blocks and kh selections per row: masks
 // [32][nb] words (one bit per row of the chunk), their prefix counts [32][nb]
 // (u16), per-block segment start and chunk count [nb] each, and the chunk's
-// entries [kRouteRows * kh].
+// entries [kRouteRows * kh] as u16 codes (row within the chunk << 5 | slot;
+// the staged path takes kh <= 31): at top-12 two work-groups fit on a CU up
+// to ~290 blocks per sequence, one up to ~700.
 __host__ __device__ inline size_t staged_lds_bytes(int nb, int kh) {
-  return (size_t)nb * (128 + 64 + 8) + (size_t)kRouteRows * kh * 4;
+  return (size_t)nb * (128 + 64 + 8) + (size_t)kRouteRows * kh * 2;
 }
 
 // KH: largest number of history selections per row (register array).
@@ -279,8 +281,8 @@ __global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
                                                          // conflicts among a word's lanes)
   uint32_t* seg = mask + kWords * nb;                    // [nb] segment start of block j in ent
   uint32_t* ccnt = seg + nb;                             // [nb] entries of block j in this chunk
-  uint32_t* ent = ccnt + nb;                             // [rows * kh]
-  uint16_t* pre = reinterpret_cast<uint16_t*>(ent + kRouteRows * kh);  // [32][nb]
+  uint16_t* ent = reinterpret_cast<uint16_t*>(ccnt + nb);  // [rows * kh] codes
+  uint16_t* pre = ent + kRouteRows * kh;                    // [32][nb]
   const int tid = threadIdx.x, word = tid >> 5, bit = tid & 31;
   const int lane = tid & 63, wave = tid >> 6;
   const int nchunks = (sq.len + p.route_rt - 1) / p.route_rt;
@@ -335,25 +337,29 @@ __global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
   }
   __syncthreads();
   if (valid) {
-    const uint64_t r = (uint64_t)g * ((uint64_t)p.T * p.G) + (uint64_t)(sq.tok_start + tl) * p.G + hl;
 #pragma unroll
     for (int x = 0; x < KH; x++) {
       if (x < nh) {
         const int j = js[x];
         const uint32_t rank = pre[word * nb + j] +
                               __popc(mask[word * nb + j] & ((1u << bit) - 1u));
-        ent[seg[j] + rank] = (uint32_t)(r * (uint64_t)kh + (uint64_t)x);
+        ent[seg[j] + rank] = (uint16_t)((tid << 5) | x);
       }
     }
   }
   __syncthreads();
-  // each block's run, contiguous in LDS and in the bin's list: one wave per block
+  // each block's run, contiguous in LDS and in the bin's list: one wave per
+  // block; the chunk's rows are r0 + (row within the chunk)
+  const uint64_t r0 = (uint64_t)g * ((uint64_t)p.T * p.G) + (uint64_t)(sq.tok_start + cp.tl0) * p.G;
   for (int j = wave; j < nb; j += kRouteRows / 64) {
     const uint32_t n = ccnt[j];
     if (n == 0) continue;
     uint32_t* dst = entries + bin_start[bin0 + j] + col0[(int64_t)j * nchunks + cp.r];
-    const uint32_t* srcj = ent + seg[j];
-    for (uint32_t e = lane; e < n; e += 64) dst[e] = srcj[e];
+    const uint16_t* srcj = ent + seg[j];
+    for (uint32_t e = lane; e < n; e += 64) {
+      const uint32_t code = srcj[e];
+      dst[e] = (uint32_t)((r0 + (code >> 5)) * (uint64_t)kh + (code & 31u));
+    }
   }
 }
 
