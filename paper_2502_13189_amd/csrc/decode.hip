@@ -15,9 +15,11 @@
 //   gate     one work-group per (sequence, query head): fp32 scores of the
 //            query against the block means of the sequence's complete past
 //            blocks (coalesced loads staged through LDS; four partial sums
-//            over dim quarters, added in order), then top-(k-1) by
-//            k-1 rounds of a wave-wide argmax (ties: lower block index), and
-//            the selection written ascending with the current block last.
+//            over dim quarters, added in order), then top-(k-1) (ties:
+//            lower block index): up to 1024 candidates by rank, each thread
+//            counting the candidates that precede its own; beyond, by k-1
+//            rounds of a wave-wide argmax.  The selection is written
+//            ascending with the current block last.
 //   plan     (MoBA) one wave per (sequence, kv-head): the union of the
 //            blocks the group's query heads selected, ascending.
 //   attend   one work-group per (sequence, kv-head, 256-key chunk; chunks
@@ -78,6 +80,7 @@ constexpr int kGatePass = 256;              // blocks per pass
 constexpr int kGateChunk = 64;              // blocks per LDS tile
 constexpr int kGateRow = kHeadDim + 1;      // padded LDS row (floats)
 constexpr int kGateLoads = kGatePass * (kHeadDim / 4) / 256;  // float4 per thread per pass
+constexpr int kRankMax = 1024;              // candidates ranked in parallel (4 per thread)
 
 __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem p) {
   __shared__ float qs[kHeadDim];
@@ -133,11 +136,52 @@ __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem 
     }
   }
   __syncthreads();
-  if (tid >= 64) return;
-  // top-(k-1): rounds of a wave-wide argmax over (score desc, index asc);
-  // lane L owns candidates L, L + 64, ... and marks its taken ones in a mask
   const int kh = p.topk - 1;
   const int nh = min(kh, c);
+  if (c <= kRankMax) {
+    // top-(k-1) by rank: candidate j is kept iff fewer than nh candidates
+    // precede it in (score desc, index asc) order — the same set as the
+    // argmax rounds below.  Thread t ranks candidates t + 256 i against all
+    // (every lane reads the same score: broadcast), then the kept ones are
+    // written ascending: a kept candidate's place is the number of kept ones
+    // in the earlier 64-candidate groups plus those below it in its own.
+    __shared__ int gcnt[kRankMax / 64];
+    const int wave = tid >> 6;
+    uint64_t bal[kRankMax / 256];
+#pragma unroll
+    for (int i = 0; i < kRankMax / 256; i++) {
+      const int j = tid + 256 * i;
+      bool keep = false;
+      if (j < c) {
+        const float sj = sc[j];
+        int above = 0;
+        for (int u = 0; u < c; u++) {
+          const float su = sc[u];
+          above += (su > sj || (su == sj && u < j)) ? 1 : 0;
+        }
+        keep = above < nh;
+      }
+      bal[i] = __ballot(keep);
+      if (lane == 0) gcnt[4 * i + wave] = __popcll(bal[i]);
+    }
+    __syncthreads();
+    int32_t* out = a.sel + row * p.topk;
+#pragma unroll
+    for (int i = 0; i < kRankMax / 256; i++) {
+      if ((bal[i] >> lane) & 1) {
+        int pos = __popcll(bal[i] & ((uint64_t(1) << lane) - 1));
+        for (int x = 0; x < 4 * i + wave; x++) pos += gcnt[x];
+        out[pos] = tid + 256 * i;
+      }
+    }
+    if (tid == 0) out[nh] = c;
+    for (int x = nh + 1 + tid; x < p.topk; x += 256) out[x] = -1;
+    return;
+  }
+  if (tid >= 64) return;
+  // top-(k-1) for longer sequences: rounds of a wave-wide argmax over (score
+  // desc, index asc); lane L owns candidates L, L + 64, ... and marks its
+  // taken ones in a mask
   uint64_t taken = 0;
   for (int r = 0; r < nh; r++) {
     float best = -INFINITY;

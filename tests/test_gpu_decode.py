@@ -46,6 +46,8 @@ CASES = [
     ((600, 45), 16, 1, 64, 3),   # the largest group decode takes
     ((50, 2), 2, 1, 1, 5),       # one-key blocks
     ((24000, 300), 4, 1, 4096, 5),  # combine in two shares per row (80 MoBA / 94 full slots)
+    ((1025, 1026), 2, 1, 1, 4),  # 1024 past blocks (the most the gate ranks in parallel), then 1025
+    ((2600,), 2, 1, 2, 6),       # 1299 past blocks: the gate's argmax rounds
 ]
 
 
