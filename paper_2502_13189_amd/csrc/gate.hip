@@ -185,6 +185,14 @@ __device__ __forceinline__ int32_t score_key(float f) {
   return b ^ ((b >> 31) & 0x7fffffff);
 }
 
+// The fp32 score whose key is k (k from score_key, or INT32_MAX, which gives
+// a NaN that no score exceeds); INT32_MIN, the placeholder below every key,
+// gives -inf.  For a score f and such a k, score_key(f) > k iff f > the
+// result (-0 and +0 share key 0 and compare equal).
+__device__ __forceinline__ float key_floor(int32_t k) {
+  return k == INT32_MIN ? -INFINITY : __int_as_float(k ^ ((k >> 31) & 0x7fffffff));
+}
+
 // Sorted insertion of block j with key kj into (lk, li) (see the header).
 // The newcomer goes below every entry with a key >= its own (an equal key
 // stays below the earlier, lower-index entry): with gt[x] = kj > lk[x] (a
@@ -324,14 +332,15 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
       const int jend = min(kChunk, c - jc);  // blocks from c on never enter
       const uint32_t live = jend >= kChunk ? ~0u : (jend <= 0 ? 0u : (1u << jend) - 1u);
       uint32_t msk = 0;
-      const int32_t thr = KM > 0 ? lk[KM > 0 ? KM - 1 : 0] : INT32_MAX;
+      // compared as floats: key(f) > thr iff f > key_floor(thr)
+      const float thr = key_floor(KM > 0 ? lk[KM > 0 ? KM - 1 : 0] : INT32_MAX);
 #pragma unroll
       for (int b4 = 0; b4 < kChunk / 4; b4++) {
         const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
         const float f[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int e = 0; e < 4; e++)
-          if (KM > 0) msk |= (uint32_t)(score_key(f[e]) > thr) << (4 * b4 + e);
+          if (KM > 0) msk |= (uint32_t)(f[e] > thr) << (4 * b4 + e);
       }
       msk &= live;
       if (scores) {  // debugging aid: the fp32 scores of this row's past blocks
