@@ -56,6 +56,7 @@ SMALL = [
     ((1500,), 4, 4, 16, 2, torch.bfloat16),
     ((3000, 70), 4, 2, 16, 12, torch.bfloat16),
     ((2500,), 2, 1, 8, 16, torch.bfloat16),
+    ((1500, 300), 4, 2, 16, 40, torch.bfloat16),  # k-1 = 39: the 63-place gate list, entries routed one by one
     ((300,), 2, 2, 64, 3, torch.float32),
     ((600, 250), 4, 2, 128, 4, torch.float32),
     ((515,), 2, 1, 50, 3, torch.float32),
