@@ -73,7 +73,7 @@ __device__ __forceinline__ void insert_top(float (&sc)[KM], int (&id)[KM], float
 template <int KM>
 __device__ __forceinline__ void write_sel(int32_t* out, const int* id, int c, int K) {
   int nh = 0;
-  if constexpr (KM > 0) {
+  if (KM > 0 && c >= K) {
 #pragma unroll
     for (int x = 0; x < KM; x++) {
       if (id[x] < c) {
@@ -342,7 +342,9 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
         for (int e = 0; e < 4; e++)
           if (KM > 0) msk |= (uint32_t)(f[e] > thr) << (4 * b4 + e);
       }
-      msk &= live;
+      // a row with at most k - 1 past blocks keeps all of them (written
+      // without the list)
+      msk &= c >= K ? live : 0u;
       if (scores) {  // debugging aid: the fp32 scores of this row's past blocks
         for (int b = 0; b < jend && jc + b < nmax; b++) scores[row * nmax + jc + b] = st[wave][lane][b];
       }
