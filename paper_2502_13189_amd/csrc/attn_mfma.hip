@@ -401,10 +401,6 @@ __device__ __forceinline__ void load_q(bf16x8 (&qf)[8], const AttnArgs& a, const
     qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 16 * kk));
 }
 
-// kAsm: LDS DMA as inline assembly (no compiler wait after each key tile's
-// DMA issue); the compiler's form is kept for blocks of up to 256 keys, where
-// the other register allocation it gives measured faster.
-template <bool kAsm>
 __global__ __launch_bounds__(512, 1) void attn_hist_persist_kernel(AttnArgs a, Problem p) {
   __shared__ u32x4 lds[kLdsChunks];
   __shared__ u32x4 stage[kRows * kStageRow];  // the tile's partial rows (bf16)
@@ -454,8 +450,8 @@ __global__ __launch_bounds__(512, 1) void attn_hist_persist_kernel(AttnArgs a, P
   ro.vq = qc * kRowV + hh;
   const float c2 = a.scale_log2;
 
-  dma_k<kAsm>(D, c.i0, lds);
-  dma_v<kAsm>(D, c.i0, lds + 2 * kBufK);
+  dma_k(D, c.i0, lds);
+  dma_v(D, c.i0, lds + 2 * kBufK);
   dma_wait();
   __syncthreads();
 
@@ -478,11 +474,11 @@ __global__ __launch_bounds__(512, 1) void attn_hist_persist_kernel(AttnArgs a, P
       par ^= 1;
       const bool last = i + 1 == c.i1;
       if (!last) {
-        dma_k<kAsm>(D, i + 1, lds + (cur ^ 1) * kBufK);
-        dma_v<kAsm>(D, i + 1, lds + 2 * kBufK + (cur ^ 1) * kBufV);
+        dma_k(D, i + 1, lds + (cur ^ 1) * kBufK);
+        dma_v(D, i + 1, lds + 2 * kBufK + (cur ^ 1) * kBufV);
       } else if (more) {
-        dma_k<kAsm>(Dn, n.i0, lds + (cur ^ 1) * kBufK);
-        dma_v<kAsm>(Dn, n.i0, lds + 2 * kBufK + (cur ^ 1) * kBufV);
+        dma_k(Dn, n.i0, lds + (cur ^ 1) * kBufK);
+        dma_v(Dn, n.i0, lds + 2 * kBufK + (cur ^ 1) * kBufV);
       }
       qk(sc, lds + cur * kBufK, ro, qf);
       if (last && more) load_q(qf, a, n.ri, hh);  // this tile's products are issued
@@ -529,10 +525,7 @@ hipError_t launch_attn_hist_bf16(const AttnArgs& a, const Problem& p, int64_t gr
     int64_t g = ncu / 8 * 8;
     if (g < 8) g = 8;
     if (g > (grid + 7) / 8 * 8) g = (grid + 7) / 8 * 8;
-    if (p.B <= 4 * kKeyTile)
-      attn_hist_persist_kernel<false><<<(unsigned)g, 512, 0, st>>>(a, p);
-    else
-      attn_hist_persist_kernel<true><<<(unsigned)g, 512, 0, st>>>(a, p);
+    attn_hist_persist_kernel<<<(unsigned)g, 512, 0, st>>>(a, p);
     return hipGetLastError();
   }
   grid = (grid + 7) / 8 * 8;

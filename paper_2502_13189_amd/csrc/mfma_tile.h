@@ -82,55 +82,57 @@ struct Dma {
 // before any later LDS read it cannot prove disjoint from the DMA's target
 // (which it cannot for buffers chosen at run time), defeating the prefetch.
 // Every caller therefore waits for its DMA explicitly (dma_wait) before the
-// barrier that publishes the data.  kAsm = false issues the compiler's own
-// form (same instruction; its register allocation differs, see the
-// short-block history kernel).
-template <bool kAsm = true>
-__device__ __forceinline__ void dma16(const void* gsrc, u32x4* ldst) {
-  if constexpr (kAsm) {
-    const uint32_t m0 = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)ldst);
-    asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gsrc), "{m0}"(m0) : "memory");
-  } else {
-    __builtin_amdgcn_global_load_lds(gsrc, ldst, 16, 0, 0);
-  }
+// barrier that publishes the data.
+__device__ __forceinline__ uint32_t lds_addr(const u32x4* p) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
 }
 
-template <bool kAsm = true>
+// A per-lane 64-bit source address (gathered rows).
+__device__ __forceinline__ void dma16(const void* gsrc, u32x4* ldst) {
+  asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gsrc), "{m0}"(lds_addr(ldst)) : "memory");
+}
+
+// A wave-uniform base (scalar registers) plus a 32-bit per-lane byte offset:
+// one vector register per address instead of two, which keeps the attention
+// kernels' register allocation free of spills.
+__device__ __forceinline__ void dma16_at(const char* base, uint32_t off, u32x4* ldst) {
+  asm volatile("global_load_lds_dwordx4 %0, %1"
+               : : "v"(off), "s"(base), "{m0}"(lds_addr(ldst)) : "memory");
+}
+
 __device__ __forceinline__ void dma_k1(const Dma& D, const char* tile, bool tail, int64_t base,
                                        u32x4* buf, int x) {
-  const char* src = tile + D.koff[x];
+  uint32_t off = D.koff[x];
   // rows past the sequence end repeat its last key; they are always masked
-  if (tail && base + D.krow[x] >= D.len) src = D.klast + D.kcol[x];
-  dma16<kAsm>(src, buf + 64 * (D.wave + 8 * x));
+  // (the tile starts at or before the last key, so the offset stays >= 0)
+  if (tail && base + D.krow[x] >= D.len) off = (uint32_t)(D.klast - tile) + D.kcol[x];
+  dma16_at(tile, off, buf + 64 * (D.wave + 8 * x));
 }
 
-template <bool kAsm = true>
 __device__ __forceinline__ void dma_k(const Dma& D, int i, u32x4* buf) {
   const int64_t base = (int64_t)i * kKeyTile;
   const char* tile = D.kbase + (int64_t)i * D.k_tile;
   if (base + kKeyTile <= D.len) {
-    dma_k1<kAsm>(D, tile, false, base, buf, 0);
-    dma_k1<kAsm>(D, tile, false, base, buf, 1);
-    if (D.wave + 16 < kDmaK) dma_k1<kAsm>(D, tile, false, base, buf, 2);
+    dma_k1(D, tile, false, base, buf, 0);
+    dma_k1(D, tile, false, base, buf, 1);
+    if (D.wave + 16 < kDmaK) dma_k1(D, tile, false, base, buf, 2);
   } else {
-    dma_k1<kAsm>(D, tile, true, base, buf, 0);
-    dma_k1<kAsm>(D, tile, true, base, buf, 1);
-    if (D.wave + 16 < kDmaK) dma_k1<kAsm>(D, tile, true, base, buf, 2);
+    dma_k1(D, tile, true, base, buf, 0);
+    dma_k1(D, tile, true, base, buf, 1);
+    if (D.wave + 16 < kDmaK) dma_k1(D, tile, true, base, buf, 2);
   }
 }
 
-template <bool kAsm = true>
 __device__ __forceinline__ void dma_v1(const Dma& D, const char* tile, u32x4* buf, int x) {
-  dma16<kAsm>(tile + D.voff[x], buf + 64 * (D.wave + 8 * x));
+  dma16_at(tile, D.voff[x], buf + 64 * (D.wave + 8 * x));
 }
 
-template <bool kAsm = true>
 __device__ __forceinline__ void dma_v(const Dma& D, int i, u32x4* buf) {
   const char* tile = D.vbase + (int64_t)i * (kChunksV * 16);
-  dma_v1<kAsm>(D, tile, buf, 0);
-  dma_v1<kAsm>(D, tile, buf, 1);
-  if (D.wave + 16 < kDmaV) dma_v1<kAsm>(D, tile, buf, 2);
+  dma_v1(D, tile, buf, 0);
+  dma_v1(D, tile, buf, 1);
+  if (D.wave + 16 < kDmaV) dma_v1(D, tile, buf, 2);
 }
 
 // Wait for this wave's LDS DMA (and everything else) before a barrier.
