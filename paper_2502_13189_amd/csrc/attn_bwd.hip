@@ -180,9 +180,10 @@ __device__ __forceinline__ void dma_vrow(const Dma& D, const VDma& V, int i, u32
 #pragma unroll
   for (int x = 0; x < 3; x++) {
     if (x < 2 || D.wave + 16 < kDmaK) {
-      const char* src = tile + (D.krow[x] * V.st + D.kcol[x]);
-      if (tail && base + D.krow[x] >= D.len) src = V.last + D.kcol[x];
-      dma16(src, buf + 64 * (D.wave + 8 * x));
+      uint32_t off = D.krow[x] * V.st + D.kcol[x];
+      // (the tile starts at or before the last row, so the offset stays >= 0)
+      if (tail && base + D.krow[x] >= D.len) off = (uint32_t)(V.last - tile) + D.kcol[x];
+      dma16_at(tile, off, buf + 64 * (D.wave + 8 * x));
     }
   }
 }
