@@ -18,10 +18,13 @@
 // s_j = <q, hi> + <q, mid> + <q, lo> is an fp32-accumulated dot product of
 // the exact operands.  Per chunk of 32 blocks a wave computes S^T (blocks x
 // queries) for its 64 rows with v_mfma_f32_32x32x16_bf16 (3 terms x 8
-// k-steps per 32 rows; the next chunk's terms are fetched meanwhile),
-// passes the tile through LDS so that each lane holds its own row's 32
-// scores, and inserts them in block order, compared as orderable integer
-// keys of the fp32 scores.
+// k-steps per 32 rows, each block-key operand feeding both 32-row sets; the
+// next chunk's terms are fetched meanwhile), passes the tile through LDS so
+// that each lane holds its own row's 32 scores, and inserts them in block
+// order (fp32 compares; a list place's new score is one median-of-three).
+// Only scores that can still enter the list are inserted: those above its
+// last entry, or, in the first chunks, those at or above the last entry the
+// list will have after the chunk, found first from the scores alone.
 //
 // fp32 queries: s_j = <q, kbar_j> on the VALU in fp32 with four interleaved
 // partial sums combined pairwise, block keys broadcast from LDS.
@@ -178,50 +181,53 @@ constexpr int kChunk = 32;               // blocks per matrix tile
 constexpr int kTermRow = kHeadDim + 8;   // bf16 per LDS row of a block-key term (272 B)
 constexpr int kScoreRow = kChunk + 4;    // floats per LDS score row (144 B)
 
-// Orderable integer key of an fp32 score: k(a) < k(b) iff a < b (ties only
-// for equal values; -0 is first made +0).
-__device__ __forceinline__ int32_t score_key(float f) {
-  const int32_t b = __float_as_int(f + 0.0f);
-  return b ^ ((b >> 31) & 0x7fffffff);
+// a = median(a, b, c), in place.  Issued as assembly in program order, so a
+// list rewritten from the bottom up keeps every value in its own register
+// (the compiler would otherwise reorder the medians and copy the list back
+// at the end of each insertion).
+__device__ __forceinline__ void med3_into(float& a, float b, float c) {
+  asm volatile("v_med3_f32 %0, %0, %1, %2" : "+v"(a) : "v"(b), "v"(c));
 }
 
-// The fp32 score whose key is k (k from score_key, or INT32_MAX, which gives
-// a NaN that no score exceeds); INT32_MIN, the placeholder below every key,
-// gives -inf.  For a score f and such a k, score_key(f) > k iff f > the
-// result (-0 and +0 share key 0 and compare equal).
-__device__ __forceinline__ float key_floor(int32_t k) {
-  return k == INT32_MIN ? -INFINITY : __int_as_float(k ^ ((k >> 31) & 0x7fffffff));
-}
-
-// Sorted insertion of block j with key kj into (lk, li) (see the header).
-// The newcomer goes below every entry with a key >= its own (an equal key
-// stays below the earlier, lower-index entry): with gt[x] = kj > lk[x] (a
+// Sorted insertion of block j with score sj into (lf, li) (see the header).
+// The newcomer goes below every entry with a score >= its own (an equal score
+// stays below the earlier, lower-index entry): with gt[x] = sj > lf[x] (a
 // suffix of the list), place x takes place x-1's entry where gt[x-1], the
 // newcomer where only gt[x], and keeps its own entry otherwise; the bottom
-// entry drops out.  Places are rewritten from the bottom up, in place.
+// entry drops out.  Places are rewritten from the bottom up, in place.  As
+// the list is sorted, the new score of place x is the median of its own, its
+// upper neighbour's and sj (one v_med3_f32).  Scores are finite; -0 and +0
+// compare equal, as the selection rule treats them.
 template <int KM>
-__device__ __forceinline__ void insert_key(int32_t (&lk)[KM], int (&li)[KM], int32_t kj, int j) {
+__device__ __forceinline__ void insert_f(float (&lf)[KM], int (&li)[KM], float sj, int j) {
   bool gt[KM];
 #pragma unroll
-  for (int x = 0; x < KM; x++) gt[x] = kj > lk[x];
+  for (int x = 0; x < KM; x++) gt[x] = sj > lf[x];
 #pragma unroll
   for (int x = KM - 1; x >= 1; x--) {
-    const int32_t ak = gt[x - 1] ? lk[x - 1] : kj;
     const int ai = gt[x - 1] ? li[x - 1] : j;
-    lk[x] = gt[x] ? ak : lk[x];
     li[x] = gt[x] ? ai : li[x];
+    med3_into(lf[x], lf[x - 1], sj);
   }
-  lk[0] = gt[0] ? kj : lk[0];
+  lf[0] = gt[0] ? sj : lf[0];
   li[0] = gt[0] ? j : li[0];
 }
 
+// The scores of a sorted list of KM places after inserting sj, values only.
 template <int KM>
-__global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __restrict__ q,
-                                                        int64_t q_st, int64_t q_sh,
-                                                        const __hip_bfloat16* __restrict__ kterm,
-                                                        const SeqInfo* __restrict__ seqs, Problem p,
-                                                        int32_t* __restrict__ sel,
-                                                        float* __restrict__ scores, int nmax) {
+__device__ __forceinline__ void insert_value(float (&lc)[KM], float sj) {
+#pragma unroll
+  for (int x = KM - 1; x >= 1; x--) med3_into(lc[x], lc[x - 1], sj);
+  lc[0] = fmaxf(lc[0], sj);
+}
+
+// Lists of up to 15 places fit two waves per SIMD (256 registers), so one
+// wave's loads and products overlap the other's selection work.
+template <int KM>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KM <= 15 ? 2 : 1)))
+void gate_mfma_kernel(const __hip_bfloat16* __restrict__ q, int64_t q_st, int64_t q_sh,
+                      const __hip_bfloat16* __restrict__ kterm, const SeqInfo* __restrict__ seqs,
+                      Problem p, int32_t* __restrict__ sel, float* __restrict__ scores, int nmax) {
   __shared__ __attribute__((aligned(16))) __bf16 terms[3][kChunk][kTermRow];
   __shared__ __attribute__((aligned(16))) float st[4][64][kScoreRow];
   const int g = blockIdx.y;
@@ -234,6 +240,8 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
   const int last_tok = min(grp * tw + tw, sq.len) - 1;
   const int cmax = last_tok / p.B;
   const int K = p.topk;
+  // chunks whose list bound is found first (where it pays for short lists)
+  constexpr int kPreChunks = KM <= 11 ? 2 : (KM <= 15 ? 1 : 0);
 
   // this lane's own row (insertion and output)
   const int i = 64 * wave + lane;
@@ -246,12 +254,12 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
     for (int j = 0; j < nmax; j++) scores[row * nmax + j] = j < c ? 0.0f : NAN;
   }
 
-  int32_t lk[KM > 0 ? KM : 1];
+  float lf[KM > 0 ? KM : 1];
   int li[KM > 0 ? KM : 1];
   if constexpr (KM > 0) {
 #pragma unroll
     for (int x = 0; x < KM; x++) {
-      lk[x] = x < KM - (K - 1) ? INT32_MAX : INT32_MIN;
+      lf[x] = x < KM - (K - 1) ? INFINITY : -INFINITY;
       li[x] = 0x7fffffff;
     }
   }
@@ -298,49 +306,95 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
           *reinterpret_cast<u32x4*>(&terms[m][jb][d0 + 8 * h2]) = pf[m][h2];
       if (jc + kChunk < cmax) fetch(jc + kChunk);  // lands during this chunk's products
       __syncthreads();
+      // S^T for both 32-row sets, one term at a time (lo, mid, hi), so a
+      // score is hi.q + (mid.q + lo.q) with each product summed over its
+      // k-steps in ascending order.  Each block-key operand is read once and
+      // feeds both sets' products; the reads run six products ahead of their
+      // use (scheduling groups), so the LDS latency hides behind the matrix
+      // core.
+      f32x16 part[2], acc[2];
+      u32x4 op[24];  // operand i: term 2 - i / 8, k-step i % 8
+#pragma unroll
+      for (int i = 0; i < 24; i++)
+        op[i] = *reinterpret_cast<const u32x4*>(&terms[2 - i / 8][qc][16 * (i % 8) + 8 * hh]);
+#pragma unroll
+      for (int mi = 0; mi < 3; mi++) {
+#pragma unroll
+        for (int set = 0; set < 2; set++)
+#pragma unroll
+          for (int e = 0; e < 16; e++) acc[set][e] = 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < 8; kk++) {
+          const bf16x8 a = __builtin_bit_cast(bf16x8, op[8 * mi + kk]);
+          acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][kk], acc[0], 0, 0, 0);
+          acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][kk], acc[1], 0, 0, 0);
+        }
+#pragma unroll
+        for (int set = 0; set < 2; set++) part[set] = mi == 0 ? acc[set] : acc[set] + part[set];
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+      for (int i = 0; i < 21; i++) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
 #pragma unroll
       for (int set = 0; set < 2; set++) {
-        f32x16 acc[3];
-#pragma unroll
-        for (int m = 0; m < 3; m++)
-#pragma unroll
-          for (int e = 0; e < 16; e++) acc[m][e] = 0.0f;
-#pragma unroll
-        for (int kk = 0; kk < 8; kk++)
-#pragma unroll
-          for (int m = 0; m < 3; m++)
-            acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                *reinterpret_cast<const bf16x8*>(&terms[m][qc][16 * kk + 8 * hh]), qf[set][kk],
-                acc[m], 0, 0, 0);
         // lane (qc, hh) holds row 32 set + qc, blocks 8 (e / 4) + 4 hh + e % 4
 #pragma unroll
         for (int e4 = 0; e4 < 4; e4++) {
           float4 v;
-          v.x = acc[0][4 * e4 + 0] + (acc[1][4 * e4 + 0] + acc[2][4 * e4 + 0]);
-          v.y = acc[0][4 * e4 + 1] + (acc[1][4 * e4 + 1] + acc[2][4 * e4 + 1]);
-          v.z = acc[0][4 * e4 + 2] + (acc[1][4 * e4 + 2] + acc[2][4 * e4 + 2]);
-          v.w = acc[0][4 * e4 + 3] + (acc[1][4 * e4 + 3] + acc[2][4 * e4 + 3]);
+          v.x = part[set][4 * e4 + 0];
+          v.y = part[set][4 * e4 + 1];
+          v.z = part[set][4 * e4 + 2];
+          v.w = part[set][4 * e4 + 3];
           *reinterpret_cast<float4*>(&st[wave][32 * set + qc][8 * e4 + 4 * hh]) = v;
         }
       }
       __builtin_amdgcn_wave_barrier();
-      // this lane's row: 32 scores in block order.  Only keys above the
+      // this lane's row: 32 scores in block order.  Only scores above the
       // list's last entry at the chunk start can enter it (the last entry
-      // only rises, and an equal later key never displaces an earlier one),
+      // only rises, and an equal later score never displaces an earlier one),
       // so those are marked and inserted in block order; the other
-      // insertions would leave the list unchanged.
+      // insertions would leave the list unchanged.  In the first chunks,
+      // where that bound is weak, the list's last score after the chunk is
+      // found first (the chunk's scores inserted into a value-only copy of
+      // the list); scores below it cannot be in the list after the chunk, so
+      // only those at or above it are marked.
       const int jend = min(kChunk, c - jc);  // blocks from c on never enter
       const uint32_t live = jend >= kChunk ? ~0u : (jend <= 0 ? 0u : (1u << jend) - 1u);
       uint32_t msk = 0;
-      // compared as floats: key(f) > thr iff f > key_floor(thr)
-      const float thr = key_floor(KM > 0 ? lk[KM > 0 ? KM - 1 : 0] : INT32_MAX);
+      if constexpr (KM > 0) {
+        if (jc < kPreChunks * kChunk) {
+          float lc[KM];
 #pragma unroll
-      for (int b4 = 0; b4 < kChunk / 4; b4++) {
-        const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
-        const float f[4] = {v.x, v.y, v.z, v.w};
+          for (int x = 0; x < KM; x++) lc[x] = lf[x];
 #pragma unroll
-        for (int e = 0; e < 4; e++)
-          if (KM > 0) msk |= (uint32_t)(f[e] > thr) << (4 * b4 + e);
+          for (int b4 = 0; b4 < kChunk / 4; b4++) {
+            const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
+            const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 4; e++) insert_value<KM>(lc, 4 * b4 + e < jend ? f[e] : -INFINITY);
+          }
+          const float thr = lc[KM - 1];
+#pragma unroll
+          for (int b4 = 0; b4 < kChunk / 4; b4++) {
+            const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
+            const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 4; e++) msk |= (uint32_t)(f[e] >= thr) << (4 * b4 + e);
+          }
+        } else {
+          const float thr = lf[KM - 1];
+#pragma unroll
+          for (int b4 = 0; b4 < kChunk / 4; b4++) {
+            const float4 v = *reinterpret_cast<const float4*>(&st[wave][lane][4 * b4]);
+            const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 4; e++) msk |= (uint32_t)(f[e] > thr) << (4 * b4 + e);
+          }
+        }
       }
       // a row with at most k - 1 past blocks keeps all of them (written
       // without the list)
@@ -349,10 +403,16 @@ __global__ __launch_bounds__(256) void gate_mfma_kernel(const __hip_bfloat16* __
         for (int b = 0; b < jend && jc + b < nmax; b++) scores[row * nmax + jc + b] = st[wave][lane][b];
       }
       if constexpr (KM > 0) {
+        // the next candidate's score is read before the current insertion
+        int b = __builtin_ctz(msk | (1u << 31));
+        float sb = st[wave][lane][b];
         while (msk) {
-          const int b = __builtin_ctz(msk);
           msk &= msk - 1;
-          insert_key<KM>(lk, li, score_key(st[wave][lane][b]), jc + b);
+          const int bn = __builtin_ctz(msk | (1u << 31));
+          const float sn = st[wave][lane][bn];
+          insert_f<KM>(lf, li, sb, jc + b);
+          b = bn;
+          sb = sn;
         }
       }
       __builtin_amdgcn_wave_barrier();
