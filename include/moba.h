@@ -261,7 +261,11 @@ moba_status moba_select(const moba_tensor* q, const moba_tensor* k, const moba_t
  *            ascending within a bin.  E must equal the number of history
  *            selections, sum over rows of min(topk - 1, c) (moba_route_size
  *            reports it).
- * num_kv_heads gives Hkv.  The current block is not routed.
+ * num_kv_heads gives Hkv.  The current block is not routed.  A history slot
+ * (x < min(topk - 1, c)) whose value is not a past block (outside [0, c)) is
+ * skipped, by the counts and the entries alike, so no access leaves the
+ * row's bins; offsets[last] then falls short of E and the rest of entries is
+ * left unwritten.  moba_select never writes such a slot.
  */
 moba_status moba_route(const moba_tensor* sel, const moba_tensor* cu_seqlens, int32_t block_size,
                        int32_t num_kv_heads, moba_tensor* counts, moba_tensor* offsets,

@@ -27,7 +27,10 @@
 //              does not fit in LDS, rounds of 256 rows write their entries
 //              one by one.
 // Entry value: r * (topk - 1) + slot, where slot is the position of the block
-// in the row's ascending selection.
+// in the row's ascending selection.  A history slot holding no past block of
+// its row (outside [0, c), which the gate never writes) is skipped by the
+// count and the scatter alike, so every LDS and global index stays within the
+// row's sequence.
 #include "moba_internal.h"
 
 namespace moba {
@@ -80,8 +83,11 @@ __global__ __launch_bounds__(256) void route_count_kernel(const int32_t* __restr
     const int x = w % p.topk;
     if (tk0 < tpb) {
       for (int tk = tk0; tk < cp.ntok; tk += tpb) {
-        const int nh = min(kh, (cp.tl0 + tk) / p.B);
-        if (x < nh) atomicAdd(&cnt[base[tk * tok_stride + w]], 1);
+        const int c = (cp.tl0 + tk) / p.B;
+        if (x < min(kh, c)) {
+          const int j = base[tk * tok_stride + w];
+          if ((unsigned)j < (unsigned)c) atomicAdd(&cnt[j], 1);
+        }
       }
     }
   } else {
@@ -89,8 +95,11 @@ __global__ __launch_bounds__(256) void route_count_kernel(const int32_t* __restr
     for (int e = threadIdx.x; e < n; e += 256) {
       const int tk = e / per_tok, w = e - tk * per_tok;
       const int x = w % p.topk;
-      const int nh = min(kh, (cp.tl0 + tk) / p.B);
-      if (x < nh) atomicAdd(&cnt[base[tk * tok_stride + w]], 1);
+      const int c = (cp.tl0 + tk) / p.B;
+      if (x < min(kh, c)) {
+        const int j = base[tk * tok_stride + w];
+        if ((unsigned)j < (unsigned)c) atomicAdd(&cnt[j], 1);
+      }
     }
   }
   __syncthreads();
@@ -215,7 +224,10 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
       hl = i % p.G;
       nh = min(kh, tl / p.B);
       row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;
-      for (int x = 0; x < nh; x++) atomicOr(&mask[word * nb + sel[row * p.topk + x]], 1u << bit);
+      for (int x = 0; x < nh; x++) {
+        const int j = sel[row * p.topk + x];
+        if ((unsigned)j < (unsigned)(tl / p.B)) atomicOr(&mask[word * nb + j], 1u << bit);
+      }
     }
     __syncthreads();
     if (use_pre) {
@@ -233,6 +245,7 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
       const uint64_t r = (uint64_t)g * TG + (uint64_t)(sq.tok_start + tl) * p.G + hl;
       for (int x = 0; x < nh; x++) {
         const int j = sel[row * p.topk + x];
+        if ((unsigned)j >= (unsigned)(tl / p.B)) continue;
         uint32_t rank = running[j] + __popc(mask[word * nb + j] & ((1u << bit) - 1u));
         if (use_pre) {
           rank += pre[word * nb + j];
@@ -301,10 +314,14 @@ __global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
   const bool valid = tid < nrow;
   const int tl = cp.tl0 + tid / p.G, hl = tid % p.G;
   const int nh = valid ? min(kh, tl / p.B) : 0;
+  // slots with a block outside [0, c) are skipped (-1), as by the count kernel
   int js[KH];
   const int32_t* mine = sel + ((int64_t)(sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl) * p.topk;
 #pragma unroll
-  for (int x = 0; x < KH; x++) js[x] = x < nh ? mine[x] : 0;
+  for (int x = 0; x < KH; x++) {
+    const int j = x < nh ? mine[x] : -1;
+    js[x] = (unsigned)j < (unsigned)(tl / p.B) ? j : -1;
+  }
   __syncthreads();
   // segment starts: exclusive scan of ccnt (wave 0, 64 blocks per step)
   if (wave == 0) {
@@ -324,7 +341,7 @@ __global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
   }
 #pragma unroll
   for (int x = 0; x < KH; x++)
-    if (x < nh) atomicOr(&mask[word * nb + js[x]], 1u << bit);
+    if (js[x] >= 0) atomicOr(&mask[word * nb + js[x]], 1u << bit);
   __syncthreads();
   // per block: rows of the chunk in the words below each word
   for (int j = tid; j < nb; j += kRouteRows) {
@@ -339,7 +356,7 @@ __global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
   if (valid) {
 #pragma unroll
     for (int x = 0; x < KH; x++) {
-      if (x < nh) {
+      if (js[x] >= 0) {
         const int j = js[x];
         const uint32_t rank = pre[word * nb + j] +
                               __popc(mask[word * nb + j] & ((1u << bit) - 1u));

@@ -143,19 +143,11 @@ ROUTE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("seqlens,hq,hkv,B,topk", ROUTE_CASES,
-                         ids=["-".join(map(str, c[0])) + "_h%dx%d_B%d_k%d" % c[1:]
-                              for c in ROUTE_CASES])
-def test_route_matches_cpu_inversion(seqlens, hq, hkv, B, topk):
-    """Algorithm 1's index_select step: every bin's list holds exactly the
-    history selections of its (kv-head, block), in row order."""
-    q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, offset=0.5, seed=11)
-    sel = binding.select(q, k, cu, B, topk)
-    counts, offsets, entries = binding.route(sel, cu, B, hkv)
-    sel_h = sel.cpu().numpy()
-    T = q.shape[0]
+def _cpu_route(sel_h, cun, T, hq, hkv, B, topk):
+    """The bins of Algorithm 1's index_select step, by direct enumeration:
+    for every row, in row order, its history slots x < min(topk - 1, c);
+    a slot holding a block outside [0, c) is not routed."""
     G = hq // hkv
-    cun = cu.numpy()
     boff = parity.block_offsets(cun, B)
     nb = oracle.num_blocks(cun, B)
     bins = [[] for _ in range(hkv * nb)]
@@ -167,13 +159,65 @@ def test_route_matches_cpu_inversion(seqlens, hq, hkv, B, topk):
             r = g * T * G + t * G + hl
             for x in range(min(topk - 1, c)):
                 j = int(sel_h[t, h, x])
-                bins[g * nb + boff[s] + j].append(r * (topk - 1) + x)
-    exp_counts = np.array([len(b) for b in bins])
-    exp_off = np.concatenate([[0], np.cumsum(exp_counts)])
-    exp_entries = np.array([e for b in bins for e in b], dtype=np.int64)
+                if 0 <= j < c:
+                    bins[g * nb + boff[s] + j].append(r * (topk - 1) + x)
+    counts = np.array([len(b) for b in bins])
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    entries = np.array([e for b in bins for e in b], dtype=np.int64)
+    return counts, offsets, entries
+
+
+def _check_route(sel, cu, T, hq, hkv, B, topk):
+    counts, offsets, entries = binding.route(sel, cu, B, hkv)
+    exp_counts, exp_off, exp_entries = _cpu_route(sel.cpu().numpy(), cu.numpy(), T, hq, hkv,
+                                                  B, topk)
     assert np.array_equal(counts.cpu().numpy(), exp_counts)
     assert np.array_equal(offsets.cpu().numpy(), exp_off)
-    assert np.array_equal(entries.cpu().numpy().astype(np.int64) & 0xffffffff, exp_entries)
+    n = int(exp_off[-1])
+    assert np.array_equal(entries[:n].cpu().numpy().astype(np.int64) & 0xffffffff, exp_entries)
+
+
+@pytest.mark.parametrize("seqlens,hq,hkv,B,topk", ROUTE_CASES,
+                         ids=["-".join(map(str, c[0])) + "_h%dx%d_B%d_k%d" % c[1:]
+                              for c in ROUTE_CASES])
+def test_route_matches_cpu_inversion(seqlens, hq, hkv, B, topk):
+    """Algorithm 1's index_select step: every bin's list holds exactly the
+    history selections of its (kv-head, block), in row order."""
+    q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, offset=0.5, seed=11)
+    sel = binding.select(q, k, cu, B, topk)
+    _check_route(sel, cu, q.shape[0], hq, hkv, B, topk)
+
+
+ROUTE_BAD_CASES = [ROUTE_CASES[i] for i in (1, 2, 3)]
+
+
+@pytest.mark.parametrize("seqlens,hq,hkv,B,topk", ROUTE_BAD_CASES,
+                         ids=["-".join(map(str, c[0])) + "_h%dx%d_B%d_k%d" % c[1:]
+                              for c in ROUTE_BAD_CASES])
+def test_route_skips_out_of_range_slots(seqlens, hq, hkv, B, topk):
+    """A history slot of a caller's sel that holds no past block (negative,
+    the current block or later) is skipped alike by the count and the scatter,
+    so the bins hold exactly the in-range selections."""
+    q, k, v, cu = make(seqlens, hq, hkv, torch.bfloat16, B, offset=0.5, seed=12)
+    sel = binding.select(q, k, cu, B, topk)
+    T = q.shape[0]
+    cun = cu.numpy()
+    rng = np.random.default_rng(5)
+    sel_h = sel.cpu().numpy().copy()
+    bad = [-1, -(2 ** 31), 0, 5, 10 ** 6]  # 0 and 5 become c + 0 and c + 5
+    planted = 0
+    for t in rng.choice(T, size=min(T, 400), replace=False):
+        s = int(parity.seq_of_tokens(cun, t))
+        c = (int(t) - cun[s]) // B
+        if min(topk - 1, c) == 0:
+            continue
+        h = int(rng.integers(hq))
+        x = int(rng.integers(min(topk - 1, c)))
+        v_ = bad[planted % len(bad)]
+        sel_h[t, h, x] = c + v_ if v_ in (0, 5) else v_
+        planted += 1
+    assert planted > 50
+    _check_route(torch.from_numpy(sel_h).to(sel.device), cu, T, hq, hkv, B, topk)
 
 
 def test_deterministic():
