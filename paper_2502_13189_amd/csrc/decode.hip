@@ -20,11 +20,11 @@
 //            counting the candidates that precede its own; beyond, by k-1
 //            rounds of a wave-wide argmax.  The selection is written
 //            ascending with the current block last.
-//   plan     (MoBA) one wave per (sequence, kv-head): the union of the
-//            blocks the group's query heads selected, ascending.
 //   attend   one work-group per (sequence, kv-head, 256-key chunk; chunks
 //            never cross a block boundary; in MoBA mode only the chunks of
-//            the group's selected blocks), all query heads of the group:
+//            the blocks the group's query heads selected, which each
+//            work-group finds from the selections itself: its slot's block
+//            in the ascending union), all query heads of the group:
 //            scores with one key per lane (bf16 dot2 against the packed
 //            query, fp32 sums), a per-head softmax over the chunk, P V with
 //            one dimension pair per lane and 64 keys per wave (dot2 over key
@@ -212,41 +212,6 @@ __global__ __launch_bounds__(256) void decode_gate_kernel(DecodeArgs a, Problem 
   for (int x = nh + 1 + lane; x < p.topk; x += 64) out[x] = -1;
 }
 
-// ================================================================== plan
-// One wave per (sequence, kv-head): a bitmask of the blocks any query head
-// of the group selected, written out ascending (lane w owns mask word w).
-__global__ __launch_bounds__(64) void decode_plan_kernel(DecodeArgs a, Problem p) {
-  __shared__ unsigned long long mask[kMaxBlocksPerSeq / 64];
-  const int lane = threadIdx.x;
-  const int s = blockIdx.x / p.Hkv, g = blockIdx.x % p.Hkv;
-  mask[lane] = 0;
-  __syncthreads();
-  for (int i = lane; i < p.G * p.topk; i += 64) {
-    const int h = g * p.G + i / p.topk;
-    const int j = a.sel[((int64_t)s * p.Hq + h) * p.topk + i % p.topk];
-    if (j >= 0) atomicOr(&mask[j >> 6], 1ull << (j & 63));
-  }
-  __syncthreads();
-  const unsigned long long w = mask[lane];
-  int before = __popcll(w);  // exclusive prefix of the set-bit counts over lanes
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int o = __shfl_up(before, d, 64);
-    if (lane >= d) before += o;
-  }
-  before -= __popcll(w);
-  int32_t* out = a.blocks + (int64_t)blockIdx.x * a.nunion;
-  unsigned long long rest = w;
-  int pos = before;
-  while (rest) {
-    const int b = __ffsll((long long)rest) - 1;
-    out[pos++] = 64 * lane + b;
-    rest &= rest - 1;
-  }
-  const int total = __shfl(before + __popcll(w), 63, 64);
-  for (int x = total + lane; x < a.nunion; x += 64) out[x] = -1;
-}
-
 // ================================================================ attend
 // GM: the group size rounded up to a power of two (sizes the LDS arrays, so
 // small groups leave room for more resident work-groups).
@@ -260,16 +225,48 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   // reused for the per-wave P V sums once the scores are taken
   __shared__ float2 accs[4][GM][64];
   __shared__ int use_head[GM];
+  __shared__ unsigned long long umask[kMaxBlocksPerSeq / 64];
+  __shared__ int ublock;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int s = blockIdx.y / p.Hkv, g = blockIdx.y % p.Hkv;
+  const int G = p.G;
   int x = blockIdx.x;  // chunk id: block * nsub + piece
-  if (!a.full) {       // MoBA: the grid runs over the group's selected blocks only
-    const int j = a.blocks[(int64_t)blockIdx.y * a.nunion + blockIdx.x / a.nsub];
+  if (!a.full) {
+    // MoBA: the grid runs over the group's selected blocks only.  Work-group
+    // slot blockIdx.x / nsub takes the slot-th smallest block any head of
+    // the group selected: the selections as a bitmask (lane w: blocks
+    // 64w .. 64w+63), a prefix count over the lanes, then the block.
+    const int slot = blockIdx.x / a.nsub;
+    if (tid < 64) umask[tid] = 0;
+    __syncthreads();
+    const int32_t* gs = a.sel + ((int64_t)s * p.Hq + (int64_t)g * G) * p.topk;
+    for (int i = tid; i < G * p.topk; i += 256) {
+      const int j = gs[i];
+      if (j >= 0) atomicOr(&umask[j >> 6], 1ull << (j & 63));
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const unsigned long long w = umask[tid];
+      const int n = __popcll(w);
+      int incl = n;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int o = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += o;
+      }
+      if (slot >= incl - n && slot < incl) {
+        unsigned long long r = w;
+        for (int k = slot - (incl - n); k > 0; k--) r &= r - 1;
+        ublock = 64 * tid + __ffsll((long long)r) - 1;
+      }
+      if (tid == 63 && slot >= incl) ublock = -1;  // fewer distinct blocks than slots
+    }
+    __syncthreads();
+    const int j = ublock;
     if (j < 0) return;
     x = j * a.nsub + blockIdx.x % a.nsub;
   }
   const SeqInfo sq = a.seqs[s];
-  const int G = p.G;
   int64_t u0, u1;
   chunk_range(x, a.nsub, a.chunk_block, sq.len, u0, u1);
   if (u0 >= u1) return;
@@ -535,12 +532,6 @@ hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t
   const int64_t rows = (int64_t)p.S * p.Hq;
   if (rows <= 0 || a.full) return hipSuccess;
   decode_gate_kernel<<<(unsigned)rows, 256, 0, st>>>(a, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_decode_plan(const DecodeArgs& a, const Problem& p, hipStream_t st) {
-  if (p.S <= 0 || a.full) return hipSuccess;
-  decode_plan_kernel<<<(unsigned)(p.S * p.Hkv), 64, 0, st>>>(a, p);
   return hipGetLastError();
 }
 

@@ -22,8 +22,8 @@ struct DecodeArgs {
   float* part_lse;       // [S * Hq, nchunk]
   __hip_bfloat16* out; int64_t o_ss, o_sh;  // [S, Hq, D]
   float* lse;            // [Hq, S]
-  int32_t* blocks;       // MoBA: [S * Hkv, nunion] union of the group's selected blocks, ascending, -1 padded
-  int nunion;            // MoBA: block slots per (sequence, kv-head)
+  int nunion;            // MoBA: block slots per (sequence, kv-head): the most distinct
+                         // blocks a group's query heads can select
   int nsub;              // chunks per block
   int nchunk;            // chunk slots per row
   int chunk_block;       // block length the chunks are cut at
@@ -37,8 +37,6 @@ struct DecodeArgs {
 // Every launcher enqueues on `st` and returns the launch status.  p.S is the
 // number of sequences (= queries), p.T the cache length.
 hipError_t launch_decode_gate(const DecodeArgs& a, const Problem& p, hipStream_t st);
-// MoBA: per (sequence, kv-head) the union of the group's selected blocks.
-hipError_t launch_decode_plan(const DecodeArgs& a, const Problem& p, hipStream_t st);
 hipError_t launch_decode_attend(const DecodeArgs& a, const Problem& p, hipStream_t st);
 // Two passes when nsplit > 1: shares of each row's partials, then the shares.
 hipError_t launch_decode_combine(const DecodeArgs& a, const Problem& p, hipStream_t st);

@@ -1142,12 +1142,10 @@ moba_status decode_impl(const moba_tensor* q, const moba_tensor* k_cache,
   const int64_t nslot = full ? nchunk : (int64_t)kk * nsub;
   const int nsplit = (int)std::min<int64_t>(kCombineMaxSplit, ceil_div(nslot, kCombineShare));
   const int split_len = (int)ceil_div(nslot, nsplit);
-  auto layout = [&](Bump* bp, float** kb, int32_t** sel, int32_t** blk, float** po, float** pls,
-                    float** mid) {
+  auto layout = [&](Bump* bp, float** kb, int32_t** sel, float** po, float** pls, float** mid) {
     if (noalloc) d_seqs = bp->take<SeqInfo>(S);  // the tables, first
     *kb = bp->take<float>(own_kbar ? (int64_t)p.nblk_total * Hkv * kHeadDim : 0);
     *sel = bp->take<int32_t>(full ? 0 : S * Hq * kk);
-    *blk = bp->take<int32_t>(S * Hkv * nunion);
     *po = bp->take<float>(S * Hq * nchunk * kHeadDim);
     *pls = bp->take<float>(S * Hq * nchunk);
     *mid = bp->take<float>(nsplit > 1 ? S * Hq * nsplit * (kHeadDim + 2) : 0);
@@ -1155,8 +1153,8 @@ moba_status decode_impl(const moba_tensor* q, const moba_tensor* k_cache,
   {
     Bump sz(nullptr);
     float *a0, *a2, *a3, *a5;
-    int32_t *a1, *a4;
-    layout(&sz, &a0, &a1, &a4, &a2, &a3, &a5);
+    int32_t* a1;
+    layout(&sz, &a0, &a1, &a2, &a3, &a5);
     if (noalloc) {
       if (sz.off > kNoAllocScratchBytes) return MOBA_ERR_NO_MEMORY;
     } else {
@@ -1167,7 +1165,7 @@ moba_status decode_impl(const moba_tensor* q, const moba_tensor* k_cache,
   Bump bp(noalloc ? static_cast<void*>(scratch_base) : dc->ws);
   DecodeArgs a{};
   float* kb_ws;
-  layout(&bp, &kb_ws, &a.sel, &a.blocks, &a.part_o, &a.part_lse, &a.mid);
+  layout(&bp, &kb_ws, &a.sel, &a.part_o, &a.part_lse, &a.mid);
   if (noalloc) {
     // the per-sequence table, written by kernels that receive it by value
     SeqInfo* dst = const_cast<SeqInfo*>(d_seqs);
@@ -1199,10 +1197,8 @@ moba_status decode_impl(const moba_tensor* q, const moba_tensor* k_cache,
     MOBA_LAUNCH(launch_pool(vk.data, true, vk.st, vk.sh, d_seqs, p, kb_ws, nullptr, stream));
   }
   if (!full) {
-    { Phase ph(noalloc ? nullptr : "decode_gate", stream);
-      MOBA_LAUNCH(launch_decode_gate(a, p, stream)); }
-    Phase ph(noalloc ? nullptr : "decode_plan", stream);
-    MOBA_LAUNCH(launch_decode_plan(a, p, stream));
+    Phase ph(noalloc ? nullptr : "decode_gate", stream);
+    MOBA_LAUNCH(launch_decode_gate(a, p, stream));
   }
   { Phase ph(noalloc ? nullptr : "decode_attend", stream);
     MOBA_LAUNCH(launch_decode_attend(a, p, stream)); }
