@@ -221,8 +221,7 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   __shared__ float ps[GM][kDecodeChunk];
   __shared__ uint32_t pw[GM][kDecodeChunk / 2];
   __shared__ float red[4][GM][2];
-  // K rows of the chunk (wave w: keys 64w..64w+63, rows of kKRow chunks);
-  // reused for the per-wave P V sums once the scores are taken
+  // per-wave P V sums of each head (dims 2*lane, 2*lane+1)
   __shared__ float2 accs[4][GM][64];
   __shared__ int use_head[GM];
   __shared__ unsigned long long umask[kMaxBlocksPerSeq / 64];
@@ -292,13 +291,9 @@ __global__ __launch_bounds__(256) void decode_attend_kernel(DecodeArgs a, Proble
   for (int hl = 0; hl < G; hl++) any |= use_head[hl];
   if (!any) return;
 
-  // scores: lane = key u0 + 64 * wave + lane.  The wave's key rows arrive
-  // by LDS DMA, 1 KiB of consecutive row bytes per instruction (lane L of
-  // instruction j fills chunk 64j + L: row (64j+L) / kKRow, column
-  // min((64j+L) % kKRow, 15); the pad chunk repeats column 15), so HBM is
-  // read in whole rows; each lane then reads its own row, and the pad makes
-  // 16 lanes at one column hit 16 distinct bank groups.  Rows past the chunk
-  // end load the chunk's first row (their scores are discarded).
+  // scores: lane = key u0 + 64 * wave + lane; each lane loads its own key
+  // row (16 loads of 16 bytes) into registers.  Rows past the chunk end load
+  // the chunk's first row (their scores are discarded).
   const int64_t u = u0 + 64 * wave + lane;
   const bool kv_ok = u < u1;
   const int kend = (int)min((int64_t)64, u1 - (u0 + 64 * wave));  // may be <= 0
@@ -419,11 +414,6 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
     wsum = wsum * sc + w;
     M = Mn;
   };
-  auto fold = [&](int x) {
-    const int64_t pr = row * a.nchunk + x;
-    const float4* op = reinterpret_cast<const float4*>(a.part_o + pr * kHeadDim + 8 * l16);
-    fold_loaded(a.part_lse[pr], op[0], op[1]);
-  };
   if (a.full) {
     // the group's partials x = grp + 16 i, eight loads in flight per round
     constexpr int kAhead = 8;
@@ -445,16 +435,36 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a, Probl
         if (x0 + 16 * e < n) fold_loaded(lv[e], o0[e], o1[e]);
     }
   } else {
-    // the row's chunks: z = y * nsub + i for selection entry y, piece i
+    // the row's chunks: z = y * nsub + i for selection entry y, piece i;
+    // the group's z = grp + 16 i, eight loads in flight per round
+    constexpr int kAhead = 8;
     const int32_t* sl = a.sel + row * p.topk;
     const int zend = min(p.topk * a.nsub, xb + a.split_len);
-    for (int z = xb + grp; z < zend; z += 16) {
-      const int y = z / a.nsub, i = z % a.nsub;
-      const int j = sl[y];
-      if (j < 0) continue;
-      const int64_t u0 = (int64_t)j * p.B + (int64_t)i * kDecodeChunk;
-      if (u0 >= min((int64_t)(j + 1) * p.B, (int64_t)sq.len)) continue;
-      fold(j * a.nsub + i);
+    for (int z0 = xb + grp; z0 < zend; z0 += 16 * kAhead) {
+      float lv[kAhead];
+      float4 o0[kAhead], o1[kAhead];
+      bool ok[kAhead];
+#pragma unroll
+      for (int e = 0; e < kAhead; e++) {
+        const int z = z0 + 16 * e;
+        ok[e] = false;
+        if (z < zend) {
+          const int y = z / a.nsub, i = z % a.nsub;
+          const int j = sl[y];
+          const int64_t u0 = (int64_t)j * p.B + (int64_t)i * kDecodeChunk;
+          if (j >= 0 && u0 < min((int64_t)(j + 1) * p.B, (int64_t)sq.len)) {
+            ok[e] = true;
+            const int64_t pr = row * a.nchunk + j * a.nsub + i;
+            const float4* op = reinterpret_cast<const float4*>(a.part_o + pr * kHeadDim + 8 * l16);
+            lv[e] = a.part_lse[pr];
+            o0[e] = op[0];
+            o1[e] = op[1];
+          }
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < kAhead; e++)
+        if (ok[e]) fold_loaded(lv[e], o0[e], o1[e]);
     }
   }
 #pragma unroll
