@@ -48,6 +48,7 @@ CASES = [
     ((24000, 300), 4, 1, 4096, 5),  # combine in two shares per row (80 MoBA / 94 full slots)
     ((1025, 1026), 2, 1, 1, 4),  # 1024 past blocks (the most the gate ranks in parallel), then 1025
     ((2600,), 2, 1, 2, 6),       # 1299 past blocks: the gate's argmax rounds
+    ((900,), 16, 1, 16, 24),     # 16 x 24 selections per group: the block union takes two passes
 ]
 
 
