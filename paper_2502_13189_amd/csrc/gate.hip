@@ -118,7 +118,8 @@ __global__ __launch_bounds__(256) void gate_kernel(const T* __restrict__ q, int6
   const int64_t t = (int64_t)sq.tok_start + tl;
   const int h = g * p.G + hl;
   const int K = p.topk;
-  const int64_t row = t * p.Hq + h;
+  const int64_t row = t * p.Hq + h;  // scores: [T, Hq, nmax]
+  const int64_t srow = t * p.sel_st + (int64_t)g * p.sel_sg + hl;
 
   if (valid && scores) {
     for (int j = 0; j < nmax; j++) scores[row * nmax + j] = j < c ? 0.0f : NAN;
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(256) void gate_kernel(const T* __restrict__ q, int6
     }
   }
   if (!valid) return;
-  write_sel<KM>(sel + row * K, id, c, K);
+  write_sel<KM>(sel + srow * K, id, c, K);
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -249,7 +250,8 @@ void gate_mfma_kernel(const __hip_bfloat16* __restrict__ q, int64_t q_st, int64_
   const int tl = grp * tw + i % tw;
   const bool valid = hl < p.G && tl < sq.len;
   const int c = valid ? tl / p.B : 0;
-  const int64_t row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;
+  const int64_t row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;  // scores
+  const int64_t srow = ((int64_t)sq.tok_start + tl) * p.sel_st + (int64_t)g * p.sel_sg + hl;
   if (valid && scores) {
     for (int j = 0; j < nmax; j++) scores[row * nmax + j] = j < c ? 0.0f : NAN;
   }
@@ -419,7 +421,7 @@ void gate_mfma_kernel(const __hip_bfloat16* __restrict__ q, int64_t q_st, int64_
     }
   }
   if (!valid) return;
-  write_sel<KM>(sel + row * K, li, c, K);
+  write_sel<KM>(sel + srow * K, li, c, K);
 }
 
 template <typename T, int KM>

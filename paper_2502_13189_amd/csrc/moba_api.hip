@@ -236,6 +236,8 @@ void build_plan(const std::vector<int32_t>& cu, int Hq, int Hkv, int B, int topk
   p.tile_rows = tile_rows;
   p.gate_tw = std::max(1, 256 / p.G);
   p.route_rt = std::max(1, kRouteRows / p.G);
+  p.sel_st = Hq;  // the callers' [T, Hq, topk]
+  p.sel_sg = p.G;
   pl->seqs.assign(S, SeqInfo{});
   int64_t blk = 0, vt = 0, gate = 0, rc = 0, hw = 0, hist = 0;
   int nbmax = 0;
@@ -712,7 +714,9 @@ moba_status moba_forward(const moba_tensor* q, const moba_tensor* k, const moba_
                      in.bf16 ? kTileRowsMfma : kTileRowsF32, &pl, &d_seqs, &d_tiles)) !=
       MOBA_OK)
     return st;
-  const Problem& p = pl->p;
+  Problem p = pl->p;  // the selection is private here: kv-head-major
+  p.sel_st = p.G;
+  p.sel_sg = p.T * p.G;
   const int64_t kh = kk - 1;
 
   // workspace: fixed part, then per-kv-head chunk part
@@ -854,7 +858,9 @@ moba_status backward_impl(const moba_tensor* q, const moba_tensor* k, const moba
   if ((st = get_plan(dc, stream, in.cu, in.Hq, in.Hkv, block_size, kk, kTilesCur, kTileRowsMfma, &pl,
                      &d_seqs, &d_tiles, &d_ktiles)) != MOBA_OK)
     return st;
-  const Problem& p = pl->p;
+  Problem p = pl->p;  // the selection is private here: kv-head-major
+  p.sel_st = p.G;
+  p.sel_sg = p.T * p.G;
   const int64_t kh = kk - 1;
   const int64_t TG = p.T * p.G;
   const int64_t nbins = (int64_t)p.Hkv * p.nblk_total;

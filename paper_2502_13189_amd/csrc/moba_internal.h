@@ -49,6 +49,12 @@ struct Problem {
   int64_t hist_words;     // routing-histogram words per kv-head
   int64_t hist_entries;   // history selections over all rows and heads
   int tile_rows;          // query rows per attention work-group (history and causal tiles)
+  // the selection's layout: row (t, kv-head g, head hl of the group) of sel
+  // starts at (t * sel_st + g * sel_sg + hl) * topk.  [T, Hq, topk] for the
+  // callers' arrays (sel_st = Hq, sel_sg = G); kv-head-major [Hkv, T, G, topk]
+  // inside moba_forward and moba_backward (sel_st = G, sel_sg = T * G), so
+  // a kv-head's rows are contiguous for the gate's writes and the routing.
+  int64_t sel_st, sel_sg;
 };
 
 // ---------------------------------------------------------------- launches

@@ -74,8 +74,8 @@ __global__ __launch_bounds__(256) void route_count_kernel(const int32_t* __restr
   // element e of the chunk: token cp.tl0 + e / (G topk), entry e % (G topk)
   // of the token's group of rows (head hl = entry / topk, slot x = entry % topk)
   const int per_tok = p.G * p.topk;
-  const int32_t* base = sel + ((int64_t)(sq.tok_start + cp.tl0) * p.Hq + (int64_t)g * p.G) * p.topk;
-  const int64_t tok_stride = (int64_t)p.Hq * p.topk;
+  const int32_t* base = sel + ((int64_t)(sq.tok_start + cp.tl0) * p.sel_st + (int64_t)g * p.sel_sg) * p.topk;
+  const int64_t tok_stride = p.sel_st * p.topk;
   if (per_tok <= 256) {
     // thread -> entry w of token tk0 + k * tpb: the divisions once per thread
     const int tpb = 256 / per_tok;
@@ -223,7 +223,7 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t* __res
       tl = cp.tl0 + i / p.G;
       hl = i % p.G;
       nh = min(kh, tl / p.B);
-      row = ((int64_t)sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl;
+      row = ((int64_t)sq.tok_start + tl) * p.sel_st + (int64_t)g * p.sel_sg + hl;
       for (int x = 0; x < nh; x++) {
         const int j = sel[row * p.topk + x];
         if ((unsigned)j < (unsigned)(tl / p.B)) atomicOr(&mask[word * nb + j], 1u << bit);
@@ -316,7 +316,8 @@ __global__ __launch_bounds__(kRouteRows) void route_scatter_staged_kernel(
   const int nh = valid ? min(kh, tl / p.B) : 0;
   // slots with a block outside [0, c) are skipped (-1), as by the count kernel
   int js[KH];
-  const int32_t* mine = sel + ((int64_t)(sq.tok_start + tl) * p.Hq + (int64_t)g * p.G + hl) * p.topk;
+  const int32_t* mine =
+      sel + ((int64_t)(sq.tok_start + tl) * p.sel_st + (int64_t)g * p.sel_sg + hl) * p.topk;
 #pragma unroll
   for (int x = 0; x < KH; x++) {
     const int j = x < nh ? mine[x] : -1;
