@@ -154,6 +154,21 @@ __device__ __forceinline__ void store_staged(const AttnArgs& a, const u32x4* sta
   }
 }
 
+// The same for the output rows of current-block and dense tiles: staged
+// destinations are element offsets into out.
+__device__ __forceinline__ void store_staged_out(const AttnArgs& a, const u32x4* stage,
+                                                 const int64_t* sdst, int wave, int lane) {
+  const int rsub = lane >> 4, ch = lane & 15;
+#pragma unroll
+  for (int j = 0; j < 8; j++) {
+    const int rr = 32 * wave + 4 * j + rsub;
+    const int64_t d = sdst[rr];
+    if (d >= 0)
+      reinterpret_cast<u32x4*>(static_cast<__hip_bfloat16*>(a.out) + d)[ch] =
+          stage[rr * kStageRow + ch];
+  }
+}
+
 template <int MODE>
 __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p) {
   __shared__ u32x4 lds[kLdsChunks];
@@ -315,22 +330,13 @@ __global__ __launch_bounds__(512, 1) void attn_mfma_kernel(AttnArgs a, Problem p
       __syncthreads();
       store_staged(a, stage, sdst, wave, lane);
     } else {
-      const float scale = inv, lse_out = lse;
-      if (r.valid) {
-        __hip_bfloat16* orow =
-            static_cast<__hip_bfloat16*>(a.out) + r.t * a.o_st + (int64_t)r.h * a.o_sh;
-#pragma unroll
-        for (int dt = 0; dt < 4; dt++)
-#pragma unroll
-          for (int r4 = 0; r4 < 4; r4++) {
-            const int d = 32 * dt + 8 * r4 + 4 * hh;
-            uint2 w;
-            w.x = pack_bf16(og[dt][4 * r4 + 0] * scale, og[dt][4 * r4 + 1] * scale);
-            w.y = pack_bf16(og[dt][4 * r4 + 2] * scale, og[dt][4 * r4 + 3] * scale);
-            *reinterpret_cast<uint2*>(orow + d) = w;
-          }
-        if (hh == 0) a.lse[(int64_t)r.h * p.T + r.t] = lse_out;
-      }
+      // the output rows leave the same way, as whole rows
+      u32x4* stage = lds;
+      int64_t* sdst = reinterpret_cast<int64_t*>(lds + kRows * kStageRow);
+      stage_row(og, inv, stage, sdst, rloc, hh, r.valid, r.t * a.o_st + (int64_t)r.h * a.o_sh);
+      if (r.valid && hh == 0) a.lse[(int64_t)r.h * p.T + r.t] = lse;
+      __syncthreads();
+      store_staged_out(a, stage, sdst, wave, lane);
     }
   }
 }
