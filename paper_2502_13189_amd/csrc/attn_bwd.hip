@@ -590,13 +590,16 @@ __device__ __forceinline__ void ds_weights(const f32x16& dpv, const RowTab& R, i
   sb[1] = as_bf16x8(u32x4{w[4], w[5], w[6], w[7]});
 }
 
-// Work-group: 4 pairs of waves, pair q on SIMD q (waves q and q + 4), each
-// pair owning 32 keys.  The P-wave holds K, computes S and P and accumulates
-// dV^T; the D-wave holds V, computes dP and dS (with the P-wave's P, passed
-// through LDS with a per-pair flag for each 32-row subtile) and accumulates
-// dK^T one subtile late.
+// Work-group: 4 pairs of waves, each pair owning 32 keys.  The P-wave holds
+// K, computes S and P and accumulates dV^T; the D-wave holds V, computes dP
+// and dS (with the P-wave's P, passed through LDS with a per-pair flag for
+// each 32-row subtile) and accumulates dK^T one subtile late.
 // Each wave so holds one 32-key operand set and one 32x128 accumulator, and
 // the two waves of a SIMD run matrix and vector work beside each other.
+// Waves w and w + 4 share a SIMD; P-wave q (wave q) is paired with D-wave
+// 4 + (q + 2) % 4, so the two waves of a SIMD belong to different pairs and
+// neither waits on the other's progress (2.7% faster than pairing the two
+// waves of one SIMD, whose phases then lock together).
 __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a, Problem p) {
   __shared__ u32x4 lds[5 * kBufR];  // Q chunk x3 (dK runs a subtile late), dO chunk x2
   __shared__ RowTab R;
@@ -607,7 +610,7 @@ __global__ __launch_bounds__(64 * kDkdvWaves, 1) void bwd_dkdv_kernel(BwdArgs a,
   const int lane = tid & 63, wave = tid >> 6;
   const int qc = lane & 31, hh = lane >> 5;
   // role 0: P-wave, 1: D-wave (wave-uniform: scalar branches)
-  const int pair = wave & 3, role = __builtin_amdgcn_readfirstlane(wave >> 2);
+  const int role = __builtin_amdgcn_readfirstlane(wave >> 2), pair = (wave + 2 * role) & 3;
 
   // work-group -> (kv-head, key tile): each XCD takes a contiguous run (the
   // key tiles of one bin read the same rows), early blocks (longest row
