@@ -189,10 +189,12 @@ __device__ __forceinline__ void dma_vrow(const Dma& D, const VDma& V, int i, u32
 }
 
 constexpr int kDqStage = 2 * kBufK + kBufV;  // K, V (row-major), K^T (packed)
+constexpr int kDqRow = kHeadDim / 4 + 1;  // 16-byte chunks per staged fp32 dQ row (one pad)
+constexpr int kDqLds = 2 * kDqStage > kRows * kDqRow + kRows / 2 ? 2 * kDqStage : kRows * kDqRow + kRows / 2;
 
 template <int MODE>
 __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
-  __shared__ u32x4 lds[2 * kDqStage];
+  __shared__ u32x4 lds[kDqLds];
   __shared__ RowInfo rtab[MODE == kHist ? 1 : kRows];  // current-block rows (see below)
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -337,17 +339,29 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(BwdArgs a, Problem p) {
 
   // -------------------------------------------------------------- epilogue
   const RowInfo r = MODE == kHist ? ri : rtab[rloc];
-  if (!r.valid) return;
+  if (MODE != kHist && !r.valid) return;
   const float scl = a.scale;
   if constexpr (MODE == kHist) {
-    float* dst = a.dq_part + r.dst * kHeadDim;
+    // the rows leave whole: staged in LDS (free after the loop's last
+    // barrier), then 32 lanes x 16 bytes per row, two rows per instruction
+    float4* stg = reinterpret_cast<float4*>(lds);
+    int64_t* sdst = reinterpret_cast<int64_t*>(lds + kRows * kDqRow);
 #pragma unroll
     for (int dt = 0; dt < 4; dt++)
 #pragma unroll
       for (int r4 = 0; r4 < 4; r4++)
-        *reinterpret_cast<float4*>(dst + 32 * dt + 8 * r4 + 4 * hh) =
+        stg[rloc * kDqRow + 8 * dt + 2 * r4 + hh] =
             make_float4(acc[dt][4 * r4] * scl, acc[dt][4 * r4 + 1] * scl,
                         acc[dt][4 * r4 + 2] * scl, acc[dt][4 * r4 + 3] * scl);
+    if (hh == 0) sdst[rloc] = r.valid ? r.dst : -1;
+    __syncthreads();
+    const int ch = lane & 31;
+#pragma unroll
+    for (int j = 0; j < 16; j++) {
+      const int rr = 32 * wave + 2 * j + hh;
+      const int64_t d = sdst[rr];
+      if (d >= 0) reinterpret_cast<float4*>(a.dq_part + d * kHeadDim)[ch] = stg[rr * kDqRow + ch];
+    }
   } else {
 #pragma unroll
     for (int dt = 0; dt < 4; dt++)
