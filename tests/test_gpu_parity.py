@@ -57,6 +57,9 @@ SMALL = [
     ((3000, 70), 4, 2, 16, 12, torch.bfloat16),
     ((2500,), 2, 1, 8, 16, torch.bfloat16),
     ((1500, 300), 4, 2, 16, 40, torch.bfloat16),  # k-1 = 39: the 63-place gate list, entries routed one by one
+    ((1500, 300), 4, 2, 16, 24, torch.bfloat16),  # k-1 = 23 in the 31-place list (8 places blocked)
+    ((1000, 0, 333), 8, 2, 8, 32, torch.bfloat16),  # k-1 = 31 fills the 31-place list, up to 124 blocks
+    ((900, 77), 2, 1, 16, 24, torch.float32),       # fp32 gate, 31-place list: selection bit-exact
     ((300,), 2, 2, 64, 3, torch.float32),
     ((600, 250), 4, 2, 128, 4, torch.float32),
     ((515,), 2, 1, 50, 3, torch.float32),
@@ -91,7 +94,8 @@ def test_pool_matches_oracle(dtype):
     assert np.all(np.abs(kbar - ref) <= tol)
 
 
-@pytest.mark.parametrize("B,L,topk", [(64, 900, 4), (16, 900, 4), (8, 1200, 12), (4, 1000, 16)])
+@pytest.mark.parametrize("B,L,topk", [(64, 900, 4), (16, 900, 4), (8, 1200, 12), (4, 1000, 16),
+                                      (4, 1000, 32)])
 def test_select_constructed_ties(B, L, topk):
     """Every block holds the same keys: all scores tie exactly and the lower
     block index must win on the GPU too (also where rows have more than one
