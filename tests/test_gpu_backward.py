@@ -40,6 +40,8 @@ CASES = [
     ((40, 17), 2, 1, 1, 4),      # one-key blocks
     ((600, 45), 16, 1, 64, 3),   # 16 query heads per kv-head
     ((200, 37), 64, 1, 32, 4),   # 64 query heads per kv-head
+    ((1500, 300), 4, 2, 16, 24),  # 23 history slots: long row lists per 16-key block
+    ((1000, 0, 333), 8, 2, 8, 32),  # 31 history slots over up to 124 blocks
 ]
 
 
